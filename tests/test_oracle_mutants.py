@@ -1,0 +1,55 @@
+"""Every plausible mistake planted in the oracle must fail at least one pin.
+
+Each mutant is a copy of the oracle source with one textual change (a
+dropped term, a wrong sign, a wrong index or bound, a skipped sort, a broken
+mask test), compiled with gcc into a temporary library on the CPU.  The pin
+suite of ``oracle_pins.py`` is then run against it and has to fail.
+"""
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import oracle_pins as pins
+
+MUTANTS = {
+    "sign": ("acc[i] += prod;", "acc[i] -= prod;"),
+    "drop_x": ("double prod = cvals[p] * xj;", "double prod = cvals[p];"),
+    "wrong_row": ("            int32_t i = row_idx[p];\n            if (!row_allowed(mask, complement, i)) continue;\n            double prod",
+                  "            int32_t i = row_idx[p] % (j + 1);\n            if (!row_allowed(mask, complement, i)) continue;\n            double prod"),
+    "drop_last_entry": ("        double xj = x_val[t];\n        for (int64_t p = col_ptr[j]; p < col_ptr[j + 1]; ++p)",
+                        "        double xj = x_val[t];\n        for (int64_t p = col_ptr[j]; p < col_ptr[j + 1] - 1; ++p)"),
+    "abs_scale": ("sabs[i] += prod < 0 ? -prod : prod;", "sabs[i] += prod;"),
+    "unsorted_y": ("    qsort(touched, (size_t)nt, sizeof(int32_t), cmp_i32);\n", ""),
+    "mask_inverted": ("return complement ? !bit : bit;", "return complement ? bit : !bit;"),
+    "mask_bit_order": ("(mask[i >> 5] >> (i & 31)) & 1u", "(mask[i >> 5] >> (31 - (i & 31))) & 1u"),
+    "bool_dupes": ("            if (!seen[i]) { seen[i] = 1; y_idx[nt++] = i; }",
+                   "            if (!seen[i]) { seen[i] = 1; y_idx[nt++] = i; } else if (nt < m) { y_idx[nt++] = i; }"),
+    "csc_shifted": ("            row_idx[q] = i;", "            row_idx[q] = i > 0 ? i - 1 : i;"),
+    "bfs_no_sort": ("        qsort(frontier, (size_t)nf, sizeof(int32_t), cmp_i32);\n", ""),
+    "bfs_parent_self": ("                    parent[v] = u;", "                    parent[v] = v;"),
+    "bfs_level_off": ("                    level[v] = L + 1;", "                    level[v] = L;"),
+    "bfs_last_parent": ("                if (level[v] == -1) {",
+                        "                if (level[v] == L + 1) parent[v] = u;\n                if (level[v] == -1) {"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(oracle._SRC).read()
+    assert src.count(old) >= 1, f"mutation anchor for {name} not found"
+    mutated = src.replace(old, new, 1)
+    msrc = tmp_path / "oracle_mut.c"
+    msrc.write_text(mutated)
+    lib = str(tmp_path / f"liboracle_{name}.so")
+    subprocess.run(["gcc", "-O1", "-std=c11", "-fPIC", "-shared", "-o", lib, str(msrc)], check=True)
+    caught = []
+    for check in pins.ALL_CHECKS:
+        try:
+            check(lib_path=lib)
+        except (AssertionError, ValueError, IndexError) as e:  # noqa: PERF203
+            caught.append((check.__name__, type(e).__name__))
+    assert caught, f"mutant {name} survived every pin"
+    os.remove(lib)
