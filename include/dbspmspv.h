@@ -1,0 +1,291 @@
+/*
+ * dbspmspv.h -- C ABI of the MI355X (gfx950) dual-view blocked SpMSpV library.
+ *
+ * Implements the DB-SpMSpV method: y = A x with A and x both sparse
+ * (Sec. 2.1), over a matrix cut once into 16x16 blocks that carries a
+ * block-level CSR view and a block-level CSC view over ONE shared block
+ * payload (Sec. 3.2.1), with per-call vector blocking (Sec. 3.2.2, 4.1), a
+ * global push/pull choice (Sec. 3.3.1), per-block microkernels (Alg. 2-4,
+ * Sec. 3.3.3), load-balanced scheduling (Sec. 3.3.2) and hierarchical
+ * writeback (Sec. 3.3.3).  BFS (Sec. 4.2, Alg. 5) and sparse decoding
+ * (Sec. 4.3) run on the same engine.
+ *
+ * General conventions
+ * -------------------
+ *  - Every call returns a dbs_status; no exception crosses the ABI.  On a
+ *    non-OK status, dbs_last_error() returns a thread-local message.
+ *  - Host-detectable argument errors are reported before anything is
+ *    launched.  HIP runtime errors map to DBS_ERR_DEVICE.
+ *  - Pointers named d_* are caller-owned DEVICE memory on the current HIP
+ *    device; all other pointers are host memory.  The library never frees
+ *    caller memory.  dbs_host_matrix, dbs_matrix and dbs_ctx objects are
+ *    library-owned and released by their destroy calls (NULL is accepted).
+ *  - Indices are 0-based int32.  Vector index lists must be unique and lie
+ *    in [0, n); order is free.
+ *  - Device calls are asynchronous on the context's stream unless a stats
+ *    struct is requested, in which case they synchronize that stream.
+ *  - A dbs_matrix is immutable after build and may be shared read-only by
+ *    several contexts; one dbs_ctx must not be used by two host threads at
+ *    once, and calls on one context run in stream order.
+ *  - Output bitmaps/masks hold bit (i & 31) of 32-bit word (i >> 5) for row i.
+ */
+#ifndef DBSPMSPV_H
+#define DBSPMSPV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DBS_OK = 0,
+    DBS_ERR_ARG = 1,          /* invalid argument (null, range, duplicate, dtype mismatch) */
+    DBS_ERR_ALLOC = 2,        /* host or device allocation failed */
+    DBS_ERR_DEVICE = 3,       /* HIP runtime error or no usable gfx950 device */
+    DBS_ERR_UNSUPPORTED = 4,  /* size or combination outside what this build supports */
+    DBS_ERR_STATE = 5         /* object used in a wrong state */
+} dbs_status;
+
+typedef enum { DBS_F32 = 0, DBS_F16 = 1, DBS_PATTERN = 2 } dbs_dtype;
+typedef enum { DBS_PLUS_TIMES = 0, DBS_OR_AND = 1 } dbs_semiring;
+typedef enum { DBS_PATH_AUTO = 0, DBS_PATH_PUSH = 1, DBS_PATH_PULL = 2 } dbs_path;
+
+/* Low-level block formats (Sec. 3.2.1). */
+typedef enum {
+    DBS_BLK_COO = 0,    /* packed COO: 4-bit row | 4-bit column per entry    */
+    DBS_BLK_DENSE = 1,  /* 256 values row-major, explicit zeros + row masks   */
+    DBS_BLK_FCSR = 2,   /* ForceCSR: 16 row masks + row starts, row-major     */
+    DBS_BLK_FCSC = 3,   /* ForceCSC: 16 column masks + column starts          */
+    DBS_BLK_CSR = 4     /* patched CSR: row view + column starts + row_idx_csc2csr */
+} dbs_block_type;
+#define DBS_NUM_BLOCK_TYPES 5
+
+/* Build options.  Defaults are the paper's constants: th0 = 32, th1 = 128,
+ * th2 = 2.0 (Sec. 3.2.1, taken from CB-SpMV) and a pull segment closes once
+ * its accumulated format weight reaches 16 (Sec. 3.3.2).  force_type = -1
+ * classifies each block; 0..4 stores every block in that one format (the
+ * format ablation of Sec. 5.3).                                             */
+typedef struct {
+    int32_t th0;        /* nnz < th0            -> COO   */
+    int32_t th1;        /* nnz > th1            -> Dense */
+    float th2;          /* skew ratio threshold -> ForceCSR / ForceCSC */
+    int32_t seg_close;  /* pull segment closes when its weight >= seg_close (1..16 blocks) */
+    int32_t force_type; /* -1 auto, else a dbs_block_type */
+} dbs_build_opts;
+
+/* Fills *o with the paper's defaults. */
+void dbs_build_opts_default(dbs_build_opts *o);
+
+typedef struct {
+    int32_t m, n;               /* matrix shape */
+    int64_t nnz;                /* stored entries */
+    int32_t dtype;              /* dbs_dtype */
+    int32_t nbr, nbc;           /* block rows / block columns, ceil(m/16), ceil(n/16) */
+    int64_t nblk;               /* nonzero 16x16 blocks */
+    int64_t nseg;               /* pull segments */
+    int64_t blocks_by_type[DBS_NUM_BLOCK_TYPES];
+    int64_t payload_bytes;      /* low-level block payload */
+    int64_t db_bytes;           /* every array of the format (views, metadata, payload, segments) */
+    int64_t csr_bytes;          /* plain CSR of the same matrix: (v + 4) nnz + 4 (m + 1) */
+    int64_t csr_csc_bytes;      /* CSR plus CSC: csr_bytes + (v + 4) nnz + 4 (n + 1) */
+} dbs_matrix_info;
+
+typedef struct dbs_host_matrix dbs_host_matrix;  /* DB format in host memory (CPU only) */
+typedef struct dbs_matrix dbs_matrix;            /* DB format resident on the GPU      */
+typedef struct dbs_ctx dbs_ctx;                  /* per-stream workspace              */
+
+/* ---------------------------------------------------------------------- */
+/* Offline conversion (Sec. 3.1, 3.2.1; done once and reused, Sec. 5.4).  */
+/* ---------------------------------------------------------------------- */
+
+/* Converts a host CSR matrix into the DB format in host memory.
+ *   m, n       shape (>= 0, < 2^31); nnz = row_ptr[m]
+ *   row_ptr    int64[m+1], non-decreasing, row_ptr[0] = 0
+ *   col_idx    int32[nnz] in [0, n); any order within a row; no duplicate (i,j)
+ *   vals       nnz values of type vt (float for DBS_F32, IEEE binary16 bits
+ *              for DBS_F16), ignored (may be NULL) for DBS_PATTERN
+ *   opts       NULL for the defaults
+ * Errors: DBS_ERR_ARG for malformed CSR or duplicates, DBS_ERR_UNSUPPORTED
+ * when the number of nonzero blocks reaches 2^31.  Uses host threads only;
+ * never touches a GPU.  The caller keeps ownership of the input arrays.     */
+dbs_status dbs_host_build_csr(int32_t m, int32_t n, int64_t nnz, const int64_t *row_ptr,
+                              const int32_t *col_idx, const void *vals, dbs_dtype vt,
+                              const dbs_build_opts *opts, dbs_host_matrix **out);
+
+dbs_status dbs_host_info(const dbs_host_matrix *h, dbs_matrix_info *out);
+
+/* Read-only views of the host-side format, valid until dbs_host_destroy.
+ * Layout (all little-endian):
+ *   rb_ptr[nbr+1]   block-CSR row pointer (global_block_csr_row_ptr)
+ *   cb_col[nblk]    block column of each block, primary order (global_block_csr_col_idx)
+ *   cb_ptr[nbc+1]   block-CSC column pointer (global_block_csc_col_ptr)
+ *   csc_row[nblk]   block row per CSC position (global_block_csc_row_idx)
+ *   csc2csr[nblk]   primary block id per CSC position (global_block_csc2csr)
+ *   desc[nblk]      bits 63..16 payload byte offset, 15..8 nnz-1, 2..0 block type
+ *   payload         one record per block in primary order, V = value bytes
+ *                   (4 for F32, 2 for F16, 0 for PATTERN), entries of a block
+ *                   ordered by (local row, local column):
+ *       COO    V*nnz values, then nnz coordinate bytes (row << 4 | col);
+ *              record aligned to max(V, 1)
+ *       DENSE  uint16 row_mask[16] (bit c = local column c), then 256 values
+ *              row-major with explicit zeros; aligned to 16
+ *       FCSR   uint16 row_mask[16], uint8 row_start[16], nnz values row-major
+ *       FCSC   uint16 col_mask[16] (bit r = local row r), uint8 col_start[16],
+ *              nnz values column-major
+ *       CSR    uint16 row_mask[16], uint8 row_start[16], uint8 col_start[16],
+ *              nnz bytes row_idx_csc2csr in column-major entry order
+ *              (row << 4 | rank of the entry within its row) padded to 16,
+ *              then nnz values row-major; the value of an entry is at
+ *              row_start[row] + rank
+ *   seg[nseg]       bits 31..0 first block, 58..32 block row, 62..59 blocks-1,
+ *                   63 = the row block has exactly one segment              */
+typedef struct {
+    const int32_t *rb_ptr;
+    const int32_t *cb_col;
+    const int32_t *cb_ptr;
+    const int32_t *csc_row;
+    const int32_t *csc2csr;
+    const uint64_t *desc;
+    const uint8_t *payload;
+    int64_t payload_bytes;
+    const uint64_t *seg;
+    int64_t nseg;
+} dbs_host_arrays;
+
+dbs_status dbs_host_arrays_get(const dbs_host_matrix *h, dbs_host_arrays *out);
+void dbs_host_destroy(dbs_host_matrix *h);
+
+/* The storage accounting used for the CSR and CSR+CSC columns of the
+ * memory-overhead comparison (Table 4): CSR = (value_bytes + 4) nnz +
+ * 4 (rows + 1); CSR+CSC adds (value_bytes + 4) nnz + 4 (cols + 1).         */
+dbs_status dbs_storage_model(int64_t rows, int64_t cols, int64_t nnz, int32_t value_bytes,
+                             int64_t *csr_bytes, int64_t *csr_csc_bytes);
+
+/* ---------------------------------------------------------------------- */
+/* Device-resident matrix.                                                */
+/* ---------------------------------------------------------------------- */
+
+/* Copies a host-side DB matrix to the current device (one upload). */
+dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **out);
+
+/* dbs_host_build_csr + dbs_matrix_upload + dbs_host_destroy. */
+dbs_status dbs_matrix_build_csr(int32_t m, int32_t n, int64_t nnz, const int64_t *row_ptr,
+                                const int32_t *col_idx, const void *vals, dbs_dtype vt,
+                                const dbs_build_opts *opts, dbs_matrix **out);
+
+dbs_status dbs_matrix_info_get(const dbs_matrix *A, dbs_matrix_info *out);
+void dbs_matrix_destroy(dbs_matrix *A);
+
+/* ---------------------------------------------------------------------- */
+/* Per-stream context: scratch masks, lists, dense x and y accumulators.  */
+/* ---------------------------------------------------------------------- */
+
+/* Creates a context sized for matrices up to sizing's shape (any matrix
+ * with m and n not larger may be used with it).  stream is a hipStream_t
+ * (NULL = the default stream).  Allocates O(m + n) device memory.          */
+dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs_ctx **out);
+dbs_status dbs_ctx_set_stream(dbs_ctx *ctx, void *stream);
+void dbs_ctx_destroy(dbs_ctx *ctx);
+
+typedef struct {
+    int32_t path;         /* dbs_path actually taken (PUSH or PULL) */
+    int32_t n_nzblk;      /* nonzero vector blocks, N_nzblk (Sec. 3.3.1) */
+    int32_t n_blk;        /* vector blocks, N_blk = ceil(n/16) */
+    int32_t y_nnz;        /* entries written to y */
+    int64_t tasks;        /* push: block tasks; pull: segments scanned */
+    int32_t error_flags;  /* bit 0: x index out of range (skipped); bit 1: duplicate x index */
+    int32_t reserved;
+} dbs_call_stats;
+
+/* SpMSpV y = A x (Sec. 2.1) under plus-times or Boolean OR-AND, with an
+ * optional structural output mask.
+ *   x_nnz, d_x_idx     k unique indices in [0, n), int32, any order
+ *   d_x_val            k values of A's dtype (float / binary16); ignored for
+ *                      DBS_OR_AND (may be NULL).  A listed index is active
+ *                      whatever its value.
+ *   d_mask             NULL, or ceil(m/32) uint32 words; with complement_mask
+ *                      = 0 only rows whose bit is set may appear in y, with
+ *                      complement_mask = 1 only rows whose bit is clear.
+ *   path               AUTO: push iff N_nzblk < th3 N_blk (Sec. 3.3.1); or forced
+ *   th3                <= 0 selects the paper's 0.01
+ *   d_y_idx            capacity m: the structural pattern of y ascending
+ *                      (every row with a stored A[i][j] at a listed j that the
+ *                      mask admits, including entries that sum to 0)
+ *   d_y_val            capacity m values of A's dtype (NULL for DBS_OR_AND)
+ *   d_y_nnz            one int32: nnz(y)
+ *   stats              NULL, or filled after a stream synchronization
+ * PATTERN matrices accept only DBS_OR_AND.  Values are accumulated in fp32
+ * within a block segment and in fp64 across segments, then rounded once.
+ * Out-of-range or duplicate x indices are not detected on the host; they are
+ * skipped / flagged on the device and reported through stats.             */
+dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring sr, int32_t x_nnz,
+                      const int32_t *d_x_idx, const void *d_x_val, const uint32_t *d_mask,
+                      int complement_mask, dbs_path path, float th3, int32_t *d_y_idx,
+                      void *d_y_val, int32_t *d_y_nnz, dbs_call_stats *stats);
+
+/* Sparse decode linear layer (Sec. 4.3): y = A a with a DENSE activation a
+ * of length n in A's dtype whose entries are active iff nonzero (+0 and -0
+ * are inactive); the vector blocks are built on the GPU by a wave ballot
+ * (Sec. 4.1).  d_y_dense receives all m outputs in A's dtype (rows with no
+ * active product are 0), rounded to nearest even from the fp64 sum.
+ * d_y_f32 (NULL allowed) receives the same sums rounded to fp32.
+ * F32 and F16 matrices only.                                               */
+dbs_status dbs_spmspv_dense(dbs_ctx *ctx, const dbs_matrix *A, const void *d_x_dense,
+                            dbs_path path, float th3, void *d_y_dense, float *d_y_f32,
+                            dbs_call_stats *stats);
+
+#define DBS_BFS_MAX_LEVEL_STATS 64
+typedef struct {
+    int32_t levels;               /* nonempty levels including the source's */
+    int32_t reached;              /* vertices with level >= 0 */
+    int32_t path[DBS_BFS_MAX_LEVEL_STATS];      /* per level: DBS_PATH_PUSH / PULL */
+    int32_t frontier[DBS_BFS_MAX_LEVEL_STATS];  /* per level: frontier size */
+} dbs_bfs_stats;
+
+/* BFS from `source` (Sec. 4.2, Alg. 5): each level's frontier is the sparse
+ * x of a Boolean SpMSpV masked by the complement of the visited set; push or
+ * pull is chosen per level by the same rule as dbs_spmspv (or forced).
+ * Edge u -> v iff A[v][u] is stored; A must be square.
+ *   d_level[n]   level of each vertex, -1 if unreachable, level[source] = 0
+ *   d_parent[n]  smallest-id vertex of the previous level with an edge to v;
+ *                parent[source] = source; -1 if unreachable
+ * The host reads one small counter per level to detect termination.
+ * stats (NULL allowed) is filled on return.                                */
+dbs_status dbs_bfs(dbs_ctx *ctx, const dbs_matrix *A, int32_t source, int32_t *d_level,
+                   int32_t *d_parent, dbs_path policy, float th3, dbs_bfs_stats *stats);
+
+/* ---------------------------------------------------------------------- */
+/* Measurement hooks.                                                     */
+/* ---------------------------------------------------------------------- */
+
+/* Kernel classes timed with HIP events on the context's stream. */
+typedef enum {
+    DBS_K_SCATTER = 0,   /* vector blocker: scatter x or ballot a dense x     */
+    DBS_K_SCAN = 1,      /* active vector-block list, task offsets, selector  */
+    DBS_K_MAIN = 2,      /* push or pull traversal with block microkernels    */
+    DBS_K_FINALIZE = 3,  /* compaction / conversion of y, scratch reset       */
+    DBS_K_BFS_UPDATE = 4,/* BFS level, visited and frontier update            */
+    DBS_K_OTHER = 5,     /* BFS init / finish                                 */
+    DBS_K_COUNT = 6
+} dbs_kernel_class;
+
+typedef struct {
+    double ms[DBS_K_COUNT];        /* summed event time per class */
+    int64_t launches[DBS_K_COUNT]; /* launches per class */
+} dbs_timing;
+
+/* enable != 0 records a HIP event pair around every kernel launched on the
+ * context from now on.  dbs_ctx_read_timing synchronizes the stream, returns
+ * the sums since the last read, and clears them.                          */
+dbs_status dbs_ctx_enable_timing(dbs_ctx *ctx, int enable);
+dbs_status dbs_ctx_read_timing(dbs_ctx *ctx, dbs_timing *out);
+
+const char *dbs_last_error(void);
+const char *dbs_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DBSPMSPV_H */

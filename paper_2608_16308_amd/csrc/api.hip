@@ -1,0 +1,459 @@
+// C ABI of the library: device matrix upload, per-stream contexts, and the
+// SpMSpV / dense-activation / BFS entry points (argument checks, launches,
+// optional statistics and HIP-event timing).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "internal.hpp"
+#include "kernels.hpp"
+
+using namespace dbs;
+
+namespace {
+
+dbs_status hip_fail(hipError_t e, const char *what)
+{
+    return dbs_fail(DBS_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                          \
+    do {                                             \
+        hipError_t e_ = (expr);                      \
+        if (e_ != hipSuccess) return hip_fail(e_, what); \
+    } while (0)
+
+dbs_status check_device()
+{
+    int cnt = 0;
+    hipError_t e = hipGetDeviceCount(&cnt);
+    if (e != hipSuccess || cnt <= 0) return dbs_fail(DBS_ERR_DEVICE, "no HIP device available");
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+    hipDeviceProp_t prop;
+    HIP_TRY(hipGetDeviceProperties(&prop, dev), "hipGetDeviceProperties");
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return dbs_fail(DBS_ERR_DEVICE, "device %d is %s; this library is built for gfx950 only", dev,
+                        prop.gcnArchName);
+    return DBS_OK;
+}
+
+template <class T>
+dbs_status dev_upload(std::vector<void *> &allocs, const std::vector<T> &h, const T **out)
+{
+    size_t bytes = std::max<size_t>(h.size() * sizeof(T), 16);
+    void *p = nullptr;
+    HIP_TRY(hipMalloc(&p, bytes), "hipMalloc (matrix)");
+    allocs.push_back(p);
+    if (!h.empty()) HIP_TRY(hipMemcpy(p, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice), "hipMemcpy (matrix)");
+    *out = (const T *)p;
+    return DBS_OK;
+}
+
+template <class T>
+dbs_status dev_zeros(std::vector<void *> &allocs, size_t count, T **out)
+{
+    size_t bytes = std::max<size_t>(count * sizeof(T), 16);
+    void *p = nullptr;
+    HIP_TRY(hipMalloc(&p, bytes), "hipMalloc (context)");
+    allocs.push_back(p);
+    HIP_TRY(hipMemset(p, 0, bytes), "hipMemset (context)");
+    *out = (T *)p;
+    return DBS_OK;
+}
+
+}  // namespace
+
+struct dbs_matrix {
+    DevMatrix d;
+    dbs_matrix_info info{};
+    std::vector<void *> allocs;
+};
+
+struct TimedLaunch {
+    int cls;
+    hipEvent_t a, b;
+};
+
+struct dbs_ctx {
+    int32_t max_m = 0, max_n = 0, max_nbr = 0, max_nbc = 0;
+    hipStream_t stream = nullptr;
+    DevCtx c;
+    std::vector<void *> allocs;
+    int32_t *h_counters = nullptr;  // pinned
+    bool timing = false;
+    std::vector<TimedLaunch> pending;
+    std::vector<hipEvent_t> pool;
+    double ms[DBS_K_COUNT] = {0};
+    int64_t launches[DBS_K_COUNT] = {0};
+    bool broken = false;
+};
+
+namespace {
+
+void free_all(std::vector<void *> &allocs)
+{
+    for (void *p : allocs) (void)hipFree(p);
+    allocs.clear();
+}
+
+hipEvent_t take_event(dbs_ctx *ctx)
+{
+    if (!ctx->pool.empty()) {
+        hipEvent_t e = ctx->pool.back();
+        ctx->pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Brackets one kernel launch with an event pair when timing is on.
+struct Timer {
+    dbs_ctx *ctx;
+    int cls;
+    hipEvent_t a = nullptr, b = nullptr;
+    Timer(dbs_ctx *c, int k) : ctx(c), cls(k)
+    {
+        if (ctx->timing) {
+            a = take_event(ctx);
+            b = take_event(ctx);
+            if (a) (void)hipEventRecord(a, ctx->stream);
+        }
+    }
+    ~Timer()
+    {
+        if (ctx->timing && a && b) {
+            (void)hipEventRecord(b, ctx->stream);
+            ctx->pending.push_back({cls, a, b});
+        }
+    }
+};
+
+dbs_status sync_counters(dbs_ctx *ctx)
+{
+    HIP_TRY(hipMemcpyAsync(ctx->h_counters, ctx->c.counters, sizeof(int32_t) * C_COUNT,
+                           hipMemcpyDeviceToHost, ctx->stream),
+            "hipMemcpyAsync (counters)");
+    HIP_TRY(hipStreamSynchronize(ctx->stream), "hipStreamSynchronize");
+    return DBS_OK;
+}
+
+dbs_status check_ctx(dbs_ctx *ctx, const dbs_matrix *A)
+{
+    if (!ctx || !A) return dbs_fail(DBS_ERR_ARG, "NULL context or matrix");
+    if (ctx->broken) return dbs_fail(DBS_ERR_STATE, "context unusable after an earlier device error");
+    if (A->d.m > ctx->max_m || A->d.n > ctx->max_n)
+        return dbs_fail(DBS_ERR_ARG, "matrix %dx%d exceeds the context's %dx%d", A->d.m, A->d.n,
+                        ctx->max_m, ctx->max_n);
+    return DBS_OK;
+}
+
+#define LAUNCH(ctx, cls, expr)                                   \
+    do {                                                         \
+        Timer t_(ctx, cls);                                      \
+        hipError_t e_ = (expr);                                  \
+        if (e_ != hipSuccess) {                                  \
+            (ctx)->broken = true;                                \
+            return hip_fail(e_, "kernel launch");                \
+        }                                                        \
+    } while (0)
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// matrix
+// ---------------------------------------------------------------------------
+extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **out)
+{
+    if (!h || !out) return dbs_fail(DBS_ERR_ARG, "dbs_matrix_upload: NULL argument");
+    *out = nullptr;
+    dbs_status st = check_device();
+    if (st != DBS_OK) return st;
+    dbs_matrix *A = new (std::nothrow) dbs_matrix();
+    if (!A) return dbs_fail(DBS_ERR_ALLOC, "host allocation failed");
+    DevMatrix &d = A->d;
+    d.m = h->m;
+    d.n = h->n;
+    d.nbr = h->nbr;
+    d.nbc = h->nbc;
+    d.nblk = h->nblk;
+    d.nseg = h->nseg;
+    d.dtype = h->dtype;
+    dbs_status s2 = DBS_OK;
+    if ((s2 = dev_upload(A->allocs, h->rb_ptr, &d.rb_ptr)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, h->cb_col, &d.cb_col)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, h->cb_ptr, &d.cb_ptr)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, h->csc_row, &d.csc_row)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, h->csc2csr, &d.csc2csr)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, h->desc, &d.desc)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, h->seg, &d.seg)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, h->payload, &d.pay)) != DBS_OK) {
+        free_all(A->allocs);
+        delete A;
+        return s2;
+    }
+    fill_info(*h, &A->info);
+    *out = A;
+    return DBS_OK;
+}
+
+extern "C" dbs_status dbs_matrix_build_csr(int32_t m, int32_t n, int64_t nnz, const int64_t *row_ptr,
+                                           const int32_t *col_idx, const void *vals, dbs_dtype vt,
+                                           const dbs_build_opts *opts, dbs_matrix **out)
+{
+    dbs_host_matrix *h = nullptr;
+    dbs_status st = dbs_host_build_csr(m, n, nnz, row_ptr, col_idx, vals, vt, opts, &h);
+    if (st != DBS_OK) return st;
+    st = dbs_matrix_upload(h, out);
+    dbs_host_destroy(h);
+    return st;
+}
+
+extern "C" dbs_status dbs_matrix_info_get(const dbs_matrix *A, dbs_matrix_info *out)
+{
+    if (!A || !out) return dbs_fail(DBS_ERR_ARG, "dbs_matrix_info_get: NULL argument");
+    *out = A->info;
+    return DBS_OK;
+}
+
+extern "C" void dbs_matrix_destroy(dbs_matrix *A)
+{
+    if (!A) return;
+    free_all(A->allocs);
+    delete A;
+}
+
+// ---------------------------------------------------------------------------
+// context
+// ---------------------------------------------------------------------------
+extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs_ctx **out)
+{
+    if (!sizing || !out) return dbs_fail(DBS_ERR_ARG, "dbs_ctx_create: NULL argument");
+    *out = nullptr;
+    dbs_status st = check_device();
+    if (st != DBS_OK) return st;
+    dbs_ctx *ctx = new (std::nothrow) dbs_ctx();
+    if (!ctx) return dbs_fail(DBS_ERR_ALLOC, "host allocation failed");
+    ctx->max_m = sizing->d.m;
+    ctx->max_n = sizing->d.n;
+    ctx->max_nbr = sizing->d.nbr;
+    ctx->max_nbc = sizing->d.nbc;
+    ctx->stream = (hipStream_t)stream;
+    DevCtx &c = ctx->c;
+    const int32_t nbr = std::max(ctx->max_nbr, 1), nbc = std::max(ctx->max_nbc, 1);
+    // BFS reuses the vector-block masks as row-block masks, so size both by
+    // the larger of the two.
+    const int32_t nb = std::max(nbr, nbc);
+    c.nxwords = (nb + 1) / 2 + 2;
+    c.nywords = (nbr + 1) / 2 + 2;
+    c.n_st_scan = (nbc + 1023) / 1024 + 1;
+    c.n_st_fin = ((nbr + 1) / 2 + 511) / 512 + 1;
+    uint32_t *xmask = nullptr, *ybits = nullptr, *visited = nullptr, *nextm = nullptr;
+    float *xd = nullptr;
+    if ((st = dev_zeros(ctx->allocs, (size_t)16 * nb, &xd)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &xmask)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)nbc + 1, &c.act)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)nbc + 2, &c.task_off)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)16 * nbr, &c.yacc)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)c.nywords, &ybits)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &visited)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &nextm)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)C_COUNT, &c.counters)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)c.n_st_scan, &c.st_scan)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)c.n_st_fin, &c.st_fin)) != DBS_OK) {
+        free_all(ctx->allocs);
+        delete ctx;
+        return st;
+    }
+    c.xd = xd;
+    c.xmask = xmask;
+    c.ybits = ybits;
+    c.visited = visited;
+    c.nextm = nextm;
+    hipError_t e = hipHostMalloc((void **)&ctx->h_counters, sizeof(int32_t) * C_COUNT, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        free_all(ctx->allocs);
+        delete ctx;
+        return hip_fail(e, "hipHostMalloc");
+    }
+    *out = ctx;
+    return DBS_OK;
+}
+
+extern "C" dbs_status dbs_ctx_set_stream(dbs_ctx *ctx, void *stream)
+{
+    if (!ctx) return dbs_fail(DBS_ERR_ARG, "NULL context");
+    ctx->stream = (hipStream_t)stream;
+    return DBS_OK;
+}
+
+extern "C" void dbs_ctx_destroy(dbs_ctx *ctx)
+{
+    if (!ctx) return;
+    (void)hipStreamSynchronize(ctx->stream);
+    for (auto &p : ctx->pending) {
+        (void)hipEventDestroy(p.a);
+        (void)hipEventDestroy(p.b);
+    }
+    for (auto e : ctx->pool) (void)hipEventDestroy(e);
+    free_all(ctx->allocs);
+    if (ctx->h_counters) (void)hipHostFree(ctx->h_counters);
+    delete ctx;
+}
+
+extern "C" dbs_status dbs_ctx_enable_timing(dbs_ctx *ctx, int enable)
+{
+    if (!ctx) return dbs_fail(DBS_ERR_ARG, "NULL context");
+    ctx->timing = enable != 0;
+    return DBS_OK;
+}
+
+extern "C" dbs_status dbs_ctx_read_timing(dbs_ctx *ctx, dbs_timing *out)
+{
+    if (!ctx || !out) return dbs_fail(DBS_ERR_ARG, "NULL argument");
+    HIP_TRY(hipStreamSynchronize(ctx->stream), "hipStreamSynchronize");
+    for (auto &p : ctx->pending) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
+            ctx->ms[p.cls] += ms;
+            ctx->launches[p.cls] += 1;
+        }
+        ctx->pool.push_back(p.a);
+        ctx->pool.push_back(p.b);
+    }
+    ctx->pending.clear();
+    for (int k = 0; k < DBS_K_COUNT; ++k) {
+        out->ms[k] = ctx->ms[k];
+        out->launches[k] = ctx->launches[k];
+        ctx->ms[k] = 0;
+        ctx->launches[k] = 0;
+    }
+    return DBS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// SpMSpV
+// ---------------------------------------------------------------------------
+static float norm_th3(float th3) { return th3 > 0.f ? th3 : 0.01f; }
+
+extern "C" dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring sr, int32_t x_nnz,
+                                 const int32_t *d_x_idx, const void *d_x_val, const uint32_t *d_mask,
+                                 int complement_mask, dbs_path path, float th3, int32_t *d_y_idx,
+                                 void *d_y_val, int32_t *d_y_nnz, dbs_call_stats *stats)
+{
+    dbs_status st = check_ctx(ctx, A);
+    if (st != DBS_OK) return st;
+    if (sr != DBS_PLUS_TIMES && sr != DBS_OR_AND) return dbs_fail(DBS_ERR_ARG, "unknown semiring");
+    if (path < DBS_PATH_AUTO || path > DBS_PATH_PULL) return dbs_fail(DBS_ERR_ARG, "unknown path");
+    if (x_nnz < 0 || x_nnz > A->d.n)
+        return dbs_fail(DBS_ERR_ARG, "x_nnz %d outside [0, n=%d]", x_nnz, A->d.n);
+    if (x_nnz > 0 && !d_x_idx) return dbs_fail(DBS_ERR_ARG, "d_x_idx is NULL");
+    if (!d_y_idx || !d_y_nnz) return dbs_fail(DBS_ERR_ARG, "d_y_idx / d_y_nnz is NULL");
+    int mode;
+    if (sr == DBS_OR_AND) {
+        mode = M_BOOL;
+    } else {
+        if (A->d.dtype == DBS_PATTERN)
+            return dbs_fail(DBS_ERR_ARG, "a pattern matrix supports only the OR-AND semiring");
+        if (x_nnz > 0 && !d_x_val) return dbs_fail(DBS_ERR_ARG, "d_x_val is NULL");
+        if (!d_y_val) return dbs_fail(DBS_ERR_ARG, "d_y_val is NULL");
+        mode = A->d.dtype == DBS_F16 ? M_F16 : M_F32;
+    }
+    const hipStream_t s = ctx->stream;
+    LAUNCH(ctx, DBS_K_SCATTER, launch_scatter(A->d, ctx->c, mode, x_nnz, d_x_idx, d_x_val, s));
+    LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, (int)path, (double)norm_th3(th3), s));
+    LAUNCH(ctx, DBS_K_MAIN,
+           launch_main(A->d, ctx->c, mode, ctx->c.xd, d_mask, complement_mask ? 1 : 0, nullptr, s));
+    LAUNCH(ctx, DBS_K_FINALIZE,
+           launch_finalize(A->d, ctx->c, mode, d_y_idx, sr == DBS_OR_AND ? nullptr : d_y_val, d_y_nnz, s));
+    if (stats) {
+        if ((st = sync_counters(ctx)) != DBS_OK) return st;
+        const int32_t *h = ctx->h_counters;
+        std::memset(stats, 0, sizeof *stats);
+        stats->path = h[C_PATH];
+        stats->n_nzblk = h[C_NZBLK];
+        stats->n_blk = A->d.nbc;
+        stats->y_nnz = h[C_YNNZ];
+        stats->tasks = h[C_PATH] == PATH_PUSH ? (int64_t)h[C_TASKS] : A->d.nseg;
+        stats->error_flags = h[C_ERR_LAST];
+    }
+    return DBS_OK;
+}
+
+extern "C" dbs_status dbs_spmspv_dense(dbs_ctx *ctx, const dbs_matrix *A, const void *d_x_dense,
+                                       dbs_path path, float th3, void *d_y_dense, float *d_y_f32,
+                                       dbs_call_stats *stats)
+{
+    dbs_status st = check_ctx(ctx, A);
+    if (st != DBS_OK) return st;
+    if (A->d.dtype == DBS_PATTERN) return dbs_fail(DBS_ERR_ARG, "dense activation needs a valued matrix");
+    if (path < DBS_PATH_AUTO || path > DBS_PATH_PULL) return dbs_fail(DBS_ERR_ARG, "unknown path");
+    if (!d_x_dense || !d_y_dense) return dbs_fail(DBS_ERR_ARG, "NULL activation or output");
+    const int mode = A->d.dtype == DBS_F16 ? M_F16 : M_F32;
+    const hipStream_t s = ctx->stream;
+    LAUNCH(ctx, DBS_K_SCATTER, launch_ballot(A->d, ctx->c, mode, d_x_dense, s));
+    LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, (int)path, (double)norm_th3(th3), s));
+    LAUNCH(ctx, DBS_K_MAIN, launch_main(A->d, ctx->c, mode, ctx->c.xd, nullptr, 0, nullptr, s));
+    LAUNCH(ctx, DBS_K_FINALIZE, launch_finalize_dense(A->d, ctx->c, mode, d_y_dense, d_y_f32, s));
+    if (stats) {
+        if ((st = sync_counters(ctx)) != DBS_OK) return st;
+        const int32_t *h = ctx->h_counters;
+        std::memset(stats, 0, sizeof *stats);
+        stats->path = h[C_PATH];
+        stats->n_nzblk = h[C_NZBLK];
+        stats->n_blk = A->d.nbc;
+        stats->y_nnz = A->d.m;
+        stats->tasks = h[C_PATH] == PATH_PUSH ? (int64_t)h[C_TASKS] : A->d.nseg;
+        stats->error_flags = h[C_ERR_LAST];
+    }
+    return DBS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// BFS
+// ---------------------------------------------------------------------------
+extern "C" dbs_status dbs_bfs(dbs_ctx *ctx, const dbs_matrix *A, int32_t source, int32_t *d_level,
+                              int32_t *d_parent, dbs_path policy, float th3, dbs_bfs_stats *stats)
+{
+    dbs_status st = check_ctx(ctx, A);
+    if (st != DBS_OK) return st;
+    if (A->d.m != A->d.n) return dbs_fail(DBS_ERR_ARG, "BFS needs a square matrix (%dx%d)", A->d.m, A->d.n);
+    if (source < 0 || source >= A->d.n) return dbs_fail(DBS_ERR_ARG, "source %d outside [0, %d)", source, A->d.n);
+    if (!d_level || !d_parent) return dbs_fail(DBS_ERR_ARG, "NULL level or parent");
+    if (policy < DBS_PATH_AUTO || policy > DBS_PATH_PULL) return dbs_fail(DBS_ERR_ARG, "unknown path");
+    const hipStream_t s = ctx->stream;
+    if (stats) std::memset(stats, 0, sizeof *stats);
+    LAUNCH(ctx, DBS_K_OTHER, launch_bfs_init(A->d, ctx->c, source, d_level, d_parent, s));
+    int32_t level = 0, reached = 1, frontier = 1;
+    for (;;) {
+        LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, (int)policy, (double)norm_th3(th3), s));
+        if ((st = sync_counters(ctx)) != DBS_OK) {
+            ctx->broken = true;
+            return st;
+        }
+        const int32_t *h = ctx->h_counters;
+        if (level > 0) {
+            frontier = h[C_FRONTIER];
+            reached += frontier;
+        }
+        if (h[C_NZBLK] == 0) break;
+        if (stats && level < DBS_BFS_MAX_LEVEL_STATS) {
+            stats->path[level] = h[C_PATH];
+            stats->frontier[level] = frontier;
+        }
+        LAUNCH(ctx, DBS_K_MAIN, launch_main(A->d, ctx->c, M_BFS, nullptr, ctx->c.visited, 1, d_parent, s));
+        LAUNCH(ctx, DBS_K_BFS_UPDATE, launch_bfs_update(A->d, ctx->c, level + 1, d_level, s));
+        ++level;
+    }
+    LAUNCH(ctx, DBS_K_OTHER, launch_bfs_finish(A->d, d_parent, s));
+    if (stats) {
+        stats->levels = level;
+        stats->reached = reached;
+    }
+    return DBS_OK;
+}

@@ -1,0 +1,93 @@
+// Layout constants of the dual-view blocked (DB) format, shared by the host
+// builder and the gfx950 kernels of this library.
+//
+// Sec. 3.2.1: the matrix is cut into uniform 16x16 blocks; a block-level CSR
+// view and a block-level CSC view index ONE payload stored in primary
+// (block-CSR) order.  Per-block metadata is packed into one 64-bit word:
+//   bits 63..16  payload byte offset
+//   bits 15..8   nnz - 1          (1..256)
+//   bits  2..0   block type       (dbs_block_type)
+// Pull segments (Sec. 3.3.2) are packed into one 64-bit word:
+//   bits 31..0   first block (primary id)
+//   bits 58..32  block row
+//   bits 62..59  number of blocks - 1 (a segment holds at most 16 blocks)
+//   bit  63      the block row has exactly one segment (plain-store commit)
+#pragma once
+#include <cstdint>
+
+#ifdef __HIPCC__
+#define DBS_HD __host__ __device__ __forceinline__
+#else
+#define DBS_HD inline
+#endif
+
+namespace dbs {
+
+constexpr int BS = 16;            // block edge (Sec. 3.2.1)
+constexpr int MAX_SEG_BLOCKS = 16;
+
+enum BlockType : uint32_t { T_COO = 0, T_DENSE = 1, T_FCSR = 2, T_FCSC = 3, T_CSR = 4 };
+
+// Header offsets inside a block record (bytes).
+constexpr uint32_t HDR_MASK = 0;     // uint16 mask[16]: row masks, or column masks for FCSC
+constexpr uint32_t HDR_START = 32;   // uint8 start[16]: row starts, or column starts for FCSC
+constexpr uint32_t HDR_START2 = 48;  // uint8 col_start[16] (patched CSR only)
+constexpr uint32_t HDR_RCSC = 64;    // row_idx_csc2csr bytes (patched CSR only)
+
+DBS_HD uint64_t desc_make(uint64_t off, uint32_t nnz, uint32_t type)
+{
+    return (off << 16) | ((uint64_t)(nnz - 1) << 8) | (uint64_t)type;
+}
+DBS_HD uint64_t desc_off(uint64_t d) { return d >> 16; }
+DBS_HD uint32_t desc_nnz(uint64_t d) { return (uint32_t)((d >> 8) & 0xFFu) + 1u; }
+DBS_HD uint32_t desc_type(uint64_t d) { return (uint32_t)(d & 7u); }
+
+DBS_HD uint64_t seg_make(uint32_t first, uint32_t brow, uint32_t nb, bool single)
+{
+    return (uint64_t)first | ((uint64_t)brow << 32) | ((uint64_t)(nb - 1) << 59) |
+           ((uint64_t)(single ? 1u : 0u) << 63);
+}
+DBS_HD uint32_t seg_first(uint64_t s) { return (uint32_t)(s & 0xFFFFFFFFu); }
+DBS_HD uint32_t seg_brow(uint64_t s) { return (uint32_t)((s >> 32) & 0x7FFFFFFu); }
+DBS_HD uint32_t seg_nb(uint64_t s) { return (uint32_t)((s >> 59) & 0xFu) + 1u; }
+DBS_HD bool seg_single(uint64_t s) { return (s >> 63) != 0; }
+
+DBS_HD uint32_t round_up(uint32_t v, uint32_t a) { return (v + a - 1) / a * a; }
+
+// Byte offset of the first value inside a block record.
+DBS_HD uint32_t values_at(uint32_t type, uint32_t nnz)
+{
+    switch (type) {
+    case T_COO: return 0;
+    case T_DENSE: return HDR_START;            // after the 32-byte row masks
+    case T_FCSR:
+    case T_FCSC: return HDR_START2;            // after masks + starts
+    default: return HDR_RCSC + round_up(nnz, 16);
+    }
+}
+
+// Total bytes of a block record (before alignment of the next record).
+DBS_HD uint32_t record_bytes(uint32_t type, uint32_t nnz, uint32_t vbytes)
+{
+    switch (type) {
+    case T_COO: return vbytes * nnz + nnz;     // values, then coordinates
+    case T_DENSE: return HDR_START + 256u * vbytes;
+    case T_FCSR:
+    case T_FCSC: return HDR_START2 + nnz * vbytes;
+    default: return HDR_RCSC + round_up(nnz, 16) + nnz * vbytes;
+    }
+}
+
+DBS_HD uint32_t record_align(uint32_t type, uint32_t vbytes)
+{
+    return type == T_COO ? (vbytes > 1 ? vbytes : 1u) : 16u;
+}
+
+// Pull segment weights by format (Sec. 3.3.2): Dense 4, ForceCSR / ForceCSC /
+// patched CSR 2, COO 1.
+DBS_HD uint32_t seg_weight(uint32_t type)
+{
+    return type == T_DENSE ? 4u : (type == T_COO ? 1u : 2u);
+}
+
+}  // namespace dbs

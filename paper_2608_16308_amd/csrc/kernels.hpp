@@ -1,0 +1,76 @@
+// Host-side launch interface of the gfx950 kernels (implemented in kernels.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace dbs {
+
+// Device-resident DB matrix (Sec. 3.2.1): dual block views over one payload.
+struct DevMatrix {
+    int32_t m = 0, n = 0, nbr = 0, nbc = 0;
+    int64_t nblk = 0, nseg = 0;
+    int32_t dtype = 0;  // dbs_dtype
+    const int32_t *rb_ptr = nullptr, *cb_col = nullptr;
+    const int32_t *cb_ptr = nullptr, *csc_row = nullptr, *csc2csr = nullptr;
+    const uint64_t *desc = nullptr, *seg = nullptr;
+    const uint8_t *pay = nullptr;
+};
+
+// Counter slots in the context's device counter array.
+enum Counter : int {
+    C_NZBLK = 0,     // nonzero vector blocks of this call
+    C_TASKS = 1,     // push block tasks (sum of block-CSC lengths of active columns)
+    C_PATH = 2,      // 1 push, 2 pull
+    C_YNNZ = 3,      // entries written to y
+    C_ERR = 4,       // error bits raised by the blocker during this call
+    C_ERR_LAST = 5,  // error bits of the last completed call
+    C_FRONTIER = 6,  // BFS: vertices in the next frontier
+    C_COUNT = 8
+};
+constexpr int PATH_PUSH = 1, PATH_PULL = 2;
+
+// Per-context scratch.  Every buffer is sized for the largest matrix the
+// context was created for and is all-zero between calls (each call clears
+// exactly what it touched).
+struct DevCtx {
+    void *xd = nullptr;           // dense x values, 16 * nbc entries (fp32 or fp16)
+    uint32_t *xmask = nullptr;    // blk_x_mask, two 16-bit masks per word
+    int32_t nxwords = 0;
+    int32_t *act = nullptr;       // active vector blocks, ascending (nbc)
+    int32_t *task_off = nullptr;  // exclusive scan of their block-CSC lengths (nbc + 1)
+    double *yacc = nullptr;       // y accumulators (16 * nbr)
+    uint32_t *ybits = nullptr;    // y structure, two 16-bit row-block masks per word
+    int32_t nywords = 0;
+    uint32_t *visited = nullptr;  // BFS visited bitmap (row-block words)
+    uint32_t *nextm = nullptr;    // BFS next-frontier bitmap
+    int32_t *counters = nullptr;  // C_COUNT int32
+    uint64_t *st_scan = nullptr;  // look-back status of the active-block scan
+    int32_t n_st_scan = 0;
+    uint64_t *st_fin = nullptr;   // look-back status of the y compaction
+    int32_t n_st_fin = 0;
+};
+
+enum Mode : int { M_F32 = 0, M_F16 = 1, M_BOOL = 2, M_BFS = 3 };
+
+hipError_t launch_scatter(const DevMatrix &A, const DevCtx &C, int mode, int32_t k,
+                          const int32_t *x_idx, const void *x_val, hipStream_t s);
+hipError_t launch_ballot(const DevMatrix &A, const DevCtx &C, int mode, const void *x_dense,
+                         hipStream_t s);
+hipError_t launch_scan(const DevMatrix &A, const DevCtx &C, int forced_path, double th3,
+                       hipStream_t s);
+hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
+                       const uint32_t *omask, int complement, int32_t *parent, hipStream_t s);
+hipError_t launch_finalize(const DevMatrix &A, const DevCtx &C, int mode, int32_t *y_idx,
+                           void *y_val, int32_t *y_nnz, hipStream_t s);
+hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, void *y,
+                                 float *y32, hipStream_t s);
+hipError_t launch_bfs_init(const DevMatrix &A, const DevCtx &C, int32_t source, int32_t *level,
+                           int32_t *parent, hipStream_t s);
+hipError_t launch_bfs_update(const DevMatrix &A, const DevCtx &C, int32_t next_level,
+                             int32_t *level, hipStream_t s);
+hipError_t launch_bfs_finish(const DevMatrix &A, int32_t *parent, hipStream_t s);
+
+int main_grid(const DevMatrix &A);
+
+}  // namespace dbs

@@ -1,0 +1,149 @@
+"""GPU parity of dbs_spmspv_dense (sparse decode layer, Sec. 4.3) and dbs_bfs
+(Sec. 4.2) against the CPU oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import oracle_pins
+import paper_2608_16308_amd as dbs
+import workloads as wl
+from gpu_helpers import REL_TOL, f16_ulp_dist, gpu_matrix, log, oracle_matrix, to_dev, torch_mod
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    t = torch_mod()
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+def check_decode(ctx, A, om, a16, path, label):
+    torch = torch_mod()
+    x = to_dev(a16)
+    y32 = torch.empty(om.m, dtype=torch.float32, device="cuda:0")
+    y, st = ctx.spmspv_dense(A, x, path=path, y32=y32, stats=True)
+    torch.cuda.synchronize()
+    y64, S, y16 = oracle.decode_linear(om, a16)
+    g16 = y.cpu().numpy()
+    d = f16_ulp_dist(g16, y16)
+    assert d.max(initial=0) <= 1, f"{label}: fp16 output off by {d.max()} ulp"
+    ok = oracle.within_tol(y32.cpu().numpy(), y64, S, REL_TOL)
+    assert ok.all(), f"{label}: {np.sum(~ok)} fp32 sums out of tolerance"
+    return st
+
+
+@pytest.mark.parametrize("shape", [(200, 320), (33, 1000), (1024, 256)])
+def test_decode_small(torch, shape):
+    out_f, in_f = shape
+    w = wl.decode_layer(out_f, in_f)
+    A, om = gpu_matrix(w), oracle_matrix(w)
+    ctx = dbs.Context(A)
+    for key in range(3):
+        a16 = wl.decode_activation(in_f, key=key) if in_f % 64 == 0 else \
+            np.where(wl.rng_for(wl.W_RAND, 40, key).random(in_f) < 0.1,
+                     np.float16(0.5), np.float16(0.0)).astype(np.float16)
+        a16[0] = np.float16(-0.0)  # signed zero stays inactive
+        for p in ("auto", "push", "pull"):
+            label = f"decode {out_f}x{in_f} act={key} path={p}"
+            log(label)
+            check_decode(ctx, A, om, a16, p, label)
+
+
+def test_decode_f32_matrix_dense_activation(torch):
+    a = wl.random_csr(150, 260, 0.4, key=(41, 0))
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    rng = wl.rng_for(wl.W_RAND, 41, 1)
+    x = np.where(rng.random(260) < 0.2, rng.uniform(-1, 1, 260), 0.0).astype(np.float32)
+    log("dense-activation f32 matrix")
+    torch = torch_mod()
+    y = ctx.spmspv_dense(A, to_dev(x))
+    torch.cuda.synchronize()
+    idx = np.nonzero(x)[0].astype(np.int32)
+    ri, rv, rs = om.spmspv(idx, x[idx].astype(np.float64))
+    ref = np.zeros(a.m)
+    S = np.zeros(a.m)
+    ref[ri] = rv
+    S[ri] = rs
+    assert oracle.within_tol(y.cpu().numpy(), ref, S, REL_TOL).all()
+
+
+# ---------------------------------------------------------------- BFS
+def bfs_check(ctx, A, om, source, policy, label):
+    torch = torch_mod()
+    level, parent, st = ctx.bfs(A, source, policy=policy, stats=True)
+    torch.cuda.synchronize()
+    el, ep, nl = om.bfs(source)
+    gl, gp = level.cpu().numpy(), parent.cpu().numpy()
+    if not np.array_equal(gl, el):
+        bad = np.nonzero(gl != el)[0][:5]
+        raise AssertionError(f"{label}: level differs at {bad}: gpu {gl[bad]} ref {el[bad]}")
+    if not np.array_equal(gp, ep):
+        bad = np.nonzero(gp != ep)[0][:5]
+        raise AssertionError(f"{label}: parent differs at {bad}: gpu {gp[bad]} ref {ep[bad]}")
+    assert st["levels"] == nl, (st["levels"], nl)
+    assert st["reached"] == int(np.sum(el >= 0))
+    return st
+
+
+def small_graphs():
+    g = {}
+    g["path"] = oracle_pins._graph(50, [(i, i + 1) for i in range(49)])
+    g["star"] = oracle_pins._graph(70, [(0, i) for i in range(1, 70)])
+    R, C = 19, 23
+    e = [(r * C + c, r * C + c + 1) for r in range(R) for c in range(C - 1)]
+    e += [(r * C + c, (r + 1) * C + c) for r in range(R - 1) for c in range(C)]
+    g["grid"] = oracle_pins._graph(R * C, e)
+    g["tree"] = oracle_pins._graph(255, [((v - 1) // 2, v) for v in range(1, 255)])
+    g["directed_chain"] = oracle_pins._graph(40, [(i, i + 1) for i in range(39)], symmetric=False)
+    rng = wl.rng_for(wl.W_RAND, 42, 0)
+    n = 300
+    e = [(int(u), int(v)) for u, v in zip(rng.integers(0, n, 900), rng.integers(0, n, 900))]
+    g["random_sym"] = oracle_pins._graph(n, e)
+    g["random_dir"] = oracle_pins._graph(n, e, symmetric=False)
+    # dense clusters exercise the non-COO Boolean microkernels
+    e = [(u, v) for u in range(64) for v in range(64) if u != v and (u * 7 + v) % 3 == 0]
+    e += [(u, u + 64) for u in range(64)]
+    g["dense_blocks"] = oracle_pins._graph(140, e)
+    return g
+
+
+@pytest.mark.parametrize("name", sorted(small_graphs()))
+def test_bfs_small_graphs(torch, name):
+    a = small_graphs()[name]
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    for s in sorted({0, a.n // 2, a.n - 1}):
+        for pol in ("auto", "push", "pull"):
+            label = f"bfs {name} src={s} policy={pol}"
+            log(label)
+            bfs_check(ctx, A, om, s, pol, label)
+
+
+@pytest.mark.parametrize("force", [-1, 1, 2, 3, 4])
+def test_bfs_forced_formats(torch, force):
+    a = small_graphs()["dense_blocks"]
+    A = gpu_matrix(a, dbs.default_opts(force_type=force))
+    om = oracle_matrix(a)
+    ctx = dbs.Context(A)
+    for pol in ("push", "pull"):
+        label = f"bfs dense_blocks force={force} policy={pol}"
+        log(label)
+        bfs_check(ctx, A, om, 3, pol, label)
+
+
+def test_bfs_rmat_small(torch):
+    a = wl.rmat(12, values=False)
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    srcs = wl.bfs_sources(a, 4, key=1)
+    for s in srcs:
+        for pol in ("auto", "push", "pull"):
+            label = f"bfs rmat12 src={s} policy={pol}"
+            log(label)
+            st = bfs_check(ctx, A, om, int(s), pol, label)
+            if pol == "auto":
+                log(f"  levels={st['levels']} paths={st['path']} frontier={st['frontier']}")

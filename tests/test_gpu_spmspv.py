@@ -1,0 +1,181 @@
+"""GPU parity of dbs_spmspv (plus-times and OR-AND, push / pull / auto, output
+masks, every block format) against the CPU oracle, through the C ABI."""
+import numpy as np
+import pytest
+
+import paper_2608_16308_amd as dbs
+import workloads as wl
+from gpu_helpers import check_spmspv, gpu_matrix, log, mask_words, oracle_matrix, to_dev, torch_mod
+
+pytestmark = pytest.mark.gpu
+
+PATHS = ["auto", "push", "pull"]
+
+
+@pytest.fixture(scope="module")
+def torch():
+    t = torch_mod()
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+def x_kinds(n, key):
+    """Vector supports that drive every microkernel choice: isolated entries
+    (sparse vector blocks), whole vector blocks (dense), random 30%, one entry,
+    everything."""
+    rng = wl.rng_for(wl.W_RAND, 31, key)
+    out = {}
+    out["sparse"] = np.sort(rng.choice(n, max(1, n // 40), replace=False))
+    nvb = (n + 15) // 16
+    blocks = rng.choice(nvb, max(1, nvb // 3), replace=False)
+    full = np.concatenate([np.arange(b * 16, min(n, b * 16 + 16)) for b in blocks])
+    out["blocks"] = np.sort(full)
+    out["rand30"] = np.sort(rng.choice(n, max(1, int(0.3 * n)), replace=False))
+    out["one"] = np.array([n - 1])
+    out["all"] = np.arange(n)
+    vals = {k: wl._nonzero_uniform(wl.rng_for(wl.W_RAND, 32, key, i), -1.0, 1.0, v.size)
+            for i, (k, v) in enumerate(out.items())}
+    return {k: (out[k].astype(np.int32), vals[k]) for k in out}
+
+
+def test_tiny_config(torch):
+    a = wl.tiny()
+    x_idx, x_val = wl.sparse_x(a.n, 0.01, "uniform", key=(1,), lo=-1.0, hi=1.0)
+    assert x_idx.size == 41
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    for p in PATHS:
+        log(f"tiny 4096x4096 k=41 path={p}")
+        st = check_spmspv(ctx, A, om, a, x_idx, x_val, path=p, label=f"tiny/{p}")
+        if p == "auto":
+            assert st["path"] == "pull"  # s_b ~ 0.14 >= 0.01
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+def test_crafted_all_formats(torch, dtype):
+    npdt = np.float32 if dtype == "f32" else np.float16
+    a = wl.crafted(npdt, key=11)
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    info = A.info()
+    assert all(v > 0 for v in info["blocks_by_type"].values())
+    ctx = dbs.Context(A)
+    rng = wl.rng_for(wl.W_RAND, 33, 0)
+    bits = rng.random(a.m) < 0.6
+    mw = mask_words(bits)
+    for kind, (xi, xv) in x_kinds(a.n, 1).items():
+        xv = xv.astype(npdt)
+        for p in PATHS:
+            for mask, comp in ((None, False), (mw, False), (mw, True)):
+                label = f"crafted {dtype} x={kind} path={p} mask={'none' if mask is None else ('comp' if comp else 'on')}"
+                log(label)
+                check_spmspv(ctx, A, om, a, xi, xv.astype(np.float64), path=p, mask=mask, complement=comp,
+                             label=label)
+
+
+@pytest.mark.parametrize("force", [0, 1, 2, 3, 4])
+def test_forced_single_format(torch, force):
+    a = wl.crafted(np.float32, key=12)
+    A = gpu_matrix(a, dbs.default_opts(force_type=force))
+    om = oracle_matrix(a)
+    ctx = dbs.Context(A)
+    for kind, (xi, xv) in x_kinds(a.n, 2).items():
+        for p in ("push", "pull"):
+            label = f"force_type={force} x={kind} path={p}"
+            log(label)
+            check_spmspv(ctx, A, om, a, xi, xv, path=p, label=label)
+
+
+def test_or_and_and_path_equivalence(torch):
+    for key, dt in ((13, None), (14, np.float32)):
+        a = wl.crafted(dt, key=key)
+        A, om = gpu_matrix(a), oracle_matrix(a)
+        ctx = dbs.Context(A)
+        rng = wl.rng_for(wl.W_RAND, 34, key)
+        mw = mask_words(rng.random(a.m) < 0.5)
+        for kind, (xi, _) in x_kinds(a.n, 3).items():
+            outs = []
+            for p in PATHS:
+                for mask, comp in ((None, False), (mw, True)):
+                    label = f"or_and key={key} x={kind} path={p} comp={comp}"
+                    log(label)
+                    check_spmspv(ctx, A, om, a, xi, None, path=p, mask=mask, complement=comp,
+                                 semiring="or_and", label=label)
+            del outs
+
+
+@pytest.mark.parametrize("shape,density", [((77, 131), 0.08), ((300, 45), 0.5), ((1, 1), 1.0),
+                                           ((1, 200), 0.3), ((200, 1), 0.3), ((513, 257), 0.02),
+                                           ((64, 64), 0.0)])
+def test_random_shapes(torch, shape, density):
+    m, n = shape
+    a = wl.random_csr(m, n, density, key=(35, m, n))
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    for kind, (xi, xv) in x_kinds(n, 4).items():
+        for p in PATHS:
+            label = f"random {m}x{n} d={density} x={kind} path={p}"
+            log(label)
+            check_spmspv(ctx, A, om, a, xi, xv, path=p, label=label)
+
+
+def test_empty_x_and_threshold(torch):
+    a = wl.random_csr(400, 400, 0.05, key=(36, 0))
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    log("empty x")
+    st = check_spmspv(ctx, A, om, a, np.zeros(0, np.int32), np.zeros(0, np.float32), label="empty x")
+    assert st["y_nnz"] == 0 and st["n_nzblk"] == 0
+    # N_blk = 25: push iff N_nzblk < 0.25 -> never push with one active block;
+    # the explicit th3 moves the boundary.
+    xi = np.array([5, 6], dtype=np.int32)
+    xv = np.array([0.5, -2.0], dtype=np.float32)
+    log("threshold default")
+    check_spmspv(ctx, A, om, a, xi, xv, expect_path="pull", label="th default")
+    torch = torch_mod()
+    y_idx, y_val, st = ctx.spmspv(A, to_dev(xi), to_dev(xv), th3=0.05, stats=True)
+    assert st["path"] == "push" and st["n_nzblk"] == 1 and st["n_blk"] == 25
+
+
+def test_context_reuse_across_matrices(torch):
+    """One context, a large then a smaller matrix, many calls: the scratch it
+    resets after every call must leave no trace."""
+    big = wl.random_csr(700, 650, 0.03, key=(37, 0))
+    small = wl.crafted(np.float32, key=15)
+    Ab, As = gpu_matrix(big), gpu_matrix(small)
+    ob, os_ = oracle_matrix(big), oracle_matrix(small)
+    ctx = dbs.Context(Ab)
+    for it in range(6):
+        for a, A, om in ((big, Ab, ob), (small, As, os_)):
+            xs = x_kinds(a.n, 100 + it)
+            kind = list(xs)[it % len(xs)]
+            xi, xv = xs[kind]
+            p = PATHS[it % 3]
+            label = f"reuse it={it} {a.m}x{a.n} x={kind} path={p}"
+            log(label)
+            check_spmspv(ctx, A, om, a, xi, xv, path=p, label=label)
+
+
+def test_error_flags(torch):
+    a = wl.random_csr(100, 100, 0.1, key=(38, 0))
+    A = gpu_matrix(a)
+    ctx = dbs.Context(A)
+    log("duplicate index flag")
+    xi = to_dev(np.array([3, 7, 3], dtype=np.int32))
+    xv = to_dev(np.array([1.0, 2.0, 3.0], dtype=np.float32))
+    _, _, st = ctx.spmspv(A, xi, xv, stats=True)
+    assert st["error_flags"] & 2
+    log("out-of-range index flag")
+    xi = to_dev(np.array([3, 100, -1], dtype=np.int32))
+    _, _, st = ctx.spmspv(A, xi, xv, stats=True)
+    assert st["error_flags"] & 1
+    log("clean call after errors")
+    om = oracle_matrix(a)
+    check_spmspv(ctx, A, om, a, np.array([1, 2], np.int32), np.array([1.0, 1.0], np.float32), label="after errors")
+    # host-side argument errors
+    with pytest.raises(dbs.DbsError):
+        ctx.spmspv(A, to_dev(np.arange(101, dtype=np.int32)), to_dev(np.ones(101, np.float32)))
+    pat = wl.random_csr(50, 50, 0.1, key=(38, 1), dtype=None)
+    Ap = gpu_matrix(pat)
+    with pytest.raises(dbs.DbsError):
+        ctx.spmspv(Ap, to_dev(np.array([1], np.int32)), to_dev(np.ones(1, np.float32)))
