@@ -1,0 +1,265 @@
+#!/usr/bin/env python3
+"""Benchmark of the dual-view blocked SpMSpV on one MI355X.
+
+Workload (one "step"): y = A x on a power-law R-MAT scale-20 matrix
+(a,b,c,d = .57,.19,.19,.05, edge factor 16, symmetrised, de-duplicated, fp32
+U(0,1) values; 1,048,576 x 1,048,576, ~31.4M nonzeros) for eight sparse x:
+densities 0.01%, 0.1%, 1%, 10%, each with uniform indices and with indices
+clustered in 64-aligned runs of 64 (values U(0,1)); plus-times, automatic
+push/pull choice.  Every call runs the whole path: vector blocker, active
+block scan + path choice, push or pull traversal with block microkernels and
+LDS writeback, and compaction of the sparse y.  Inputs are resident in HBM
+when timing starts.
+
+`value` is GB/s of algorithmic bytes (paper_2608_16308_amd.bytes_model) over
+the timed steps.  Also reported: per-density GB/s and GFLOP/s (useful flops
+2 * sum of nnz of the active columns, and the paper's SpMV convention
+2 * nnz(A)), the roofline of the traversal kernel from HIP events on the
+library's stream, the CPU oracle on the same inputs, and BFS GTEPS on an
+R-MAT scale-22 graph from 16 sources (--bfs-scale 0 to skip).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+DENSITIES = [1e-4, 1e-3, 1e-2, 1e-1]
+KINDS = ["uniform", "clustered"]
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "main_rmat20_sweep_traffic.md")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_sources_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "device_common.hpp", "db_format.hpp", "kernels.hpp"):
+        with open(os.path.join(ROOT, "paper_2608_16308_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(digest: str):
+    """HBM bytes per traversal launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel sources."""
+    if not os.path.exists(PROFILE_TRAFFIC):
+        return None
+    for line in open(PROFILE_TRAFFIC):
+        if line.startswith("traffic_json:"):
+            d = json.loads(line.split(":", 1)[1])
+            if d.get("kernel_sources") == digest:
+                return d.get("bytes_per_launch")
+    return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--scale", type=int, default=20)
+    ap.add_argument("--bfs-scale", type=int, default=22)
+    ap.add_argument("--bfs-sources", type=int, default=16)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--point-reps", type=int, default=20)
+    ap.add_argument("--json-out", default=None)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only (single-GPU kernel library; "
+              "the multi-GPU row-slab sharding is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2608_16308_amd as dbs
+    import workloads as wl
+    from paper_2608_16308_amd.bytes_model import BytesModel
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+
+    # ------------------------------------------------------------ inputs
+    t0 = time.time()
+    a = wl.rmat(args.scale)
+    log(f"[bench] R-MAT {args.scale}: n={a.n} nnz={a.nnz} generated in {time.time() - t0:.1f}s")
+    t0 = time.time()
+    hm = dbs.HostMatrix.from_csr(a.m, a.n, a.row_ptr, a.col_idx, a.vals)
+    build_s = time.time() - t0
+    info = hm.info()
+    log(f"[bench] DB build {build_s:.2f}s: nblk={info['nblk']} nseg={info['nseg']} types={info['blocks_by_type']}")
+    A = dbs.Matrix.upload(hm)
+    t0 = time.time()
+    model = BytesModel(a.m, a.n, a.row_ptr, a.col_idx, hm.arrays(), info, 4)
+    log(f"[bench] bytes model ready in {time.time() - t0:.1f}s")
+    del hm
+    ctx = dbs.Context(A)
+    points = []
+    for di, d in enumerate(DENSITIES):
+        for kind in KINDS:
+            xi, xv = wl.sparse_x(a.n, d, kind, key=(20, di, KINDS.index(kind)))
+            points.append({"density": d, "kind": kind, "x_idx": xi, "x_val": xv,
+                           "d_idx": torch.from_numpy(xi).to(dev), "d_val": torch.from_numpy(xv).to(dev)})
+    m = a.m
+    y_idx = torch.empty(m, dtype=torch.int32, device=dev)
+    y_val = torch.empty(m, dtype=torch.float32, device=dev)
+    y_nnz = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def run(p, path="auto"):
+        ctx.spmspv_raw(A, p["d_idx"], p["d_val"], y_idx, y_val, y_nnz, path=path)
+
+    # path actually taken per point, and the bytes of each call
+    for p in points:
+        st = ctx.spmspv_raw(A, p["d_idx"], p["d_val"], y_idx, y_val, y_nnz, stats=True)
+        p["path"] = st["path"]
+        p["model"] = model.call(p["x_idx"], st["path"])
+        assert p["model"]["n_nzblk"] == st["n_nzblk"] and p["model"]["y_nnz"] == st["y_nnz"]
+    step_bytes = sum(p["model"]["bytes_total"] for p in points)
+    step_main_bytes = sum(p["model"]["bytes_main"] for p in points)
+    step_useful = sum(p["model"]["useful_nnz"] for p in points)
+
+    # ------------------------------------------------------------ timed steps
+    for _ in range(args.warmup):
+        for p in points:
+            run(p)
+    torch.cuda.synchronize()
+    ctx.enable_timing(True)
+    ctx.read_timing()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        for p in points:
+            run(p)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    timing = ctx.read_timing()
+    ctx.enable_timing(False)
+    ms_per_step = 1e3 * elapsed / args.steps
+    value = step_bytes * args.steps / elapsed / 1e9
+    main_ms, main_launches = timing["main"]
+    assert main_launches == args.steps * len(points)
+    main_avg_ms = main_ms / main_launches
+    achieved = step_main_bytes * args.steps / (main_ms * 1e-3) / 1e9
+    log(f"[bench] {ms_per_step:.3f} ms/step, {value:.1f} GB/s whole path; traversal kernel "
+        f"{main_avg_ms * 1e3:.1f} us/launch avg, {achieved:.1f} GB/s; per-class ms {timing}")
+
+    # ------------------------------------------------------------ per point
+    sweep = []
+    for p in points:
+        row = {"density": p["density"], "x": p["kind"], "k": p["model"]["k"], "path": p["path"],
+               "n_nzblk": p["model"]["n_nzblk"], "useful_nnz": p["model"]["useful_nnz"],
+               "y_nnz": p["model"]["y_nnz"], "bytes": p["model"]["bytes_total"]}
+        for path in ("auto", "push", "pull"):
+            mod = p["model"] if path == "auto" else model.call(p["x_idx"], path)
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            for _ in range(3):
+                run(p, path)
+            ev0.record()
+            for _ in range(args.point_reps):
+                run(p, path)
+            ev1.record()
+            torch.cuda.synchronize()
+            us = ev0.elapsed_time(ev1) * 1e3 / args.point_reps
+            row[f"{path}_us"] = round(us, 2)
+            row[f"{path}_GBs"] = round(mod["bytes_total"] / (us * 1e-6) / 1e9, 1)
+            if path == "auto":
+                row["useful_GFLOPs"] = round(2 * p["model"]["useful_nnz"] / (us * 1e-6) / 1e9, 2)
+                row["spmv_conv_GFLOPs"] = round(2 * a.nnz / (us * 1e-6) / 1e9, 1)
+        sweep.append(row)
+        log(f"[bench] {row}")
+
+    # ------------------------------------------------------------ CPU oracle
+    import oracle
+    om = oracle.OracleMatrix(a.m, a.n, a.row_ptr, a.col_idx, a.vals)
+    xs = [(p["x_idx"], p["x_val"].astype(np.float64)) for p in points]
+    one = om.time_spmspv(xs, 1)
+    reps = max(1, int(args.cpu_seconds / max(one, 1e-6)))
+    cpu_s = om.time_spmspv(xs, reps)
+    cpu_value = step_bytes * reps / cpu_s / 1e9
+    log(f"[bench] oracle: {reps} passes of the 8-point sweep in {cpu_s:.2f}s -> {cpu_value:.3f} GB/s")
+    del om
+
+    result = {
+        "metric": "SpMSpV GB/s (fraction of HBM peak) + GFLOP/s vs x density; BFS GTEPS",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"rmat{args.scale}_spmspv_density_sweep", "scale": args.scale,
+                   "edge_factor": 16, "n": a.n, "nnz": a.nnz, "densities": DENSITIES, "x_kinds": KINDS,
+                   "calls_per_step": len(points), "semiring": "plus_times", "path": "auto", "th3": 0.01,
+                   "nblk": info["nblk"], "db_build_s": round(build_s, 2),
+                   "useful_GFLOPs": round(2 * step_useful * args.steps / elapsed / 1e9, 2)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_traffic(kernel_sources_digest()),
+                     "kernel": "k_main (push/pull traversal)", "avg_launch_us": round(main_avg_ms * 1e3, 2),
+                     "algorithmic_bytes_per_launch": round(step_main_bytes / len(points))},
+        "cpu_baseline": {"value": round(cpu_value, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                         "sample": f"{reps} passes over the same 8 x vectors on R-MAT {args.scale} "
+                                   f"({cpu_s:.1f} s, CSC built once outside the timing)"},
+        "sweep": sweep,
+    }
+
+    # ------------------------------------------------------------ BFS GTEPS
+    if args.bfs_scale > 0:
+        del A, ctx
+        torch.cuda.empty_cache()
+        t0 = time.time()
+        g = wl.rmat(args.bfs_scale, values=False)
+        srcs = wl.bfs_sources(g, args.bfs_sources, key=0)
+        comp = wl.components(g)
+        log(f"[bench] BFS graph R-MAT {args.bfs_scale}: n={g.n} nnz={g.nnz} in {time.time() - t0:.1f}s")
+        t0 = time.time()
+        G = dbs.Matrix.from_csr(g.m, g.n, g.row_ptr, g.col_idx, None)
+        gbuild = time.time() - t0
+        gctx = dbs.Context(G)
+        deg = np.diff(g.row_ptr)
+        level = torch.empty(g.n, dtype=torch.int32, device=dev)
+        parent = torch.empty(g.n, dtype=torch.int32, device=dev)
+        gteps, times, per_src = [], [], []
+        for s in srcs:
+            edges = int(deg[comp == comp[s]].sum()) // 2
+            gctx.bfs(G, int(s), level=level, parent=parent)  # warm-up
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            _, _, st = gctx.bfs(G, int(s), level=level, parent=parent, stats=True)
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t1
+            times.append(dt)
+            gteps.append(edges / dt / 1e9)
+            per_src.append({"source": int(s), "ms": round(dt * 1e3, 3), "levels": st["levels"],
+                            "paths": st["path"]})
+        hm_gteps = len(gteps) / sum(1.0 / x for x in gteps)
+        log(f"[bench] BFS: harmonic mean {hm_gteps:.2f} GTEPS over {len(srcs)} sources; {per_src[:3]}")
+        result["bfs"] = {"workload": f"rmat{args.bfs_scale}_bfs_{len(srcs)}_sources", "gteps_hmean": round(hm_gteps, 3),
+                         "gteps_min": round(min(gteps), 3), "gteps_max": round(max(gteps), 3),
+                         "ms_mean": round(1e3 * float(np.mean(times)), 3), "db_build_s": round(gbuild, 2),
+                         "edges_counted": "undirected edges of the source's component", "per_source": per_src}
+
+    line = json.dumps(result)
+    if args.json_out:
+        with open(args.json_out, "w") as fh:
+            fh.write(line + "\n")
+    print(line, flush=True)
+
+
+if __name__ == "__main__":
+    main()

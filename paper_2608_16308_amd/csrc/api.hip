@@ -264,8 +264,10 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
         (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &visited)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &nextm)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)C_COUNT, &c.counters)) != DBS_OK ||
-        (st = dev_zeros(ctx->allocs, (size_t)c.n_st_scan, &c.st_scan)) != DBS_OK ||
-        (st = dev_zeros(ctx->allocs, (size_t)c.n_st_fin, &c.st_fin)) != DBS_OK) {
+        (st = dev_zeros(ctx->allocs, (size_t)c.n_st_scan, &c.st_scan[0])) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)c.n_st_scan, &c.st_scan[1])) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)c.n_st_fin, &c.st_fin[0])) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)c.n_st_fin, &c.st_fin[1])) != DBS_OK) {
         free_all(ctx->allocs);
         delete ctx;
         return st;

@@ -185,13 +185,14 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
                                               const int32_t *__restrict__ cb_ptr, int32_t nbc,
                                               int32_t *__restrict__ act, int32_t *__restrict__ task_off,
                                               int32_t *__restrict__ counters, uint64_t *status,
-                                              uint64_t *other_status, int32_t other_n,
+                                              uint64_t *next_status, int32_t n_status,
                                               int32_t forced_path, double th3)
 {
     __shared__ uint64_t lds4[TPB / WAVE];
     __shared__ uint64_t s_prefix;
-    for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < other_n; i += gridDim.x * TPB)
-        other_status[i] = 0;
+    // clear the other copy of the status words for the next scan
+    for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < n_status; i += gridDim.x * TPB)
+        next_status[i] = 0;
     const int tile = blockIdx.x;
     const int32_t base = tile * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
     uint32_t am[SCAN_ITEMS];
@@ -519,8 +520,6 @@ struct MainArgs {
     double *yacc;
     uint32_t *ybits;        // y structure; BFS: next-frontier bitmap
     int32_t *parent;        // BFS only
-    uint64_t *scan_status;  // reset here for the next scan
-    int32_t n_scan_status;
 };
 
 template <int MODE>
@@ -659,8 +658,6 @@ __global__ __launch_bounds__(TPB) void k_main(MainArgs a)
 {
     __shared__ float s_y[TPB / WAVE][WAVE];
     __shared__ int32_t s_p[TPB / WAVE][WAVE];
-    for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < a.n_scan_status; i += gridDim.x * TPB)
-        a.scan_status[i] = 0;
     if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
     if (a.counters[C_NZBLK] == 0) return;
     const int w = threadIdx.x >> 6, lane = lane_id();
@@ -683,11 +680,14 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
                                                   int32_t *__restrict__ y_idx, void *__restrict__ y_val,
                                                   int32_t *__restrict__ y_nnz,
                                                   int32_t *__restrict__ counters, uint64_t *status,
+                                                  uint64_t *next_status, int32_t n_status,
                                                   uint32_t *__restrict__ xmask,
                                                   const int32_t *__restrict__ act)
 {
     __shared__ uint64_t lds4[TPB / WAVE];
     __shared__ uint64_t s_prefix;
+    for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < n_status; i += gridDim.x * TPB)
+        next_status[i] = 0;
     // clear blk_x_mask of this call's active vector blocks
     const int32_t N = counters[C_NZBLK];
     for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < N; i += gridDim.x * TPB)
@@ -803,11 +803,8 @@ __global__ __launch_bounds__(TPB) void k_bfs_update(int32_t nwords, int32_t next
                                                     uint32_t *__restrict__ visited,
                                                     uint32_t *__restrict__ nextm,
                                                     uint32_t *__restrict__ xmask,
-                                                    int32_t *__restrict__ counters,
-                                                    uint64_t *scan_status, int32_t n_scan_status)
+                                                    int32_t *__restrict__ counters)
 {
-    for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < n_scan_status; i += gridDim.x * TPB)
-        scan_status[i] = 0;
     int32_t w = blockIdx.x * TPB + threadIdx.x;
     uint32_t cnt = 0;
     if (w < nwords) {
@@ -877,12 +874,15 @@ hipError_t launch_ballot(const DevMatrix &A, const DevCtx &C, int mode, const vo
     return hipGetLastError();
 }
 
-hipError_t launch_scan(const DevMatrix &A, const DevCtx &C, int forced_path, double th3, hipStream_t s)
+hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th3, hipStream_t s)
 {
     dim3 g(grid_for(A.nbc, SCAN_TILE, INT_MAX)), b(TPB);
+    const int p = C.scan_parity;
     hipLaunchKernelGGL(k_scan, g, b, 0, s, C.xmask, A.cb_ptr, A.nbc, C.act, C.task_off, C.counters,
-                       C.st_scan, C.st_fin, C.n_st_fin, forced_path, th3);
-    return hipGetLastError();
+                       C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) C.scan_parity = 1 - p;
+    return e;
 }
 
 hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
@@ -908,8 +908,6 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
     a.yacc = C.yacc;
     a.ybits = mode == M_BFS ? C.nextm : C.ybits;
     a.parent = parent;
-    a.scan_status = C.st_scan;
-    a.n_scan_status = C.n_st_scan;
     dim3 g(main_grid(A)), b(TPB);
     switch (mode) {
     case M_F32: hipLaunchKernelGGL(k_main<M_F32>, g, b, 0, s, a); break;
@@ -920,17 +918,22 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
     return hipGetLastError();
 }
 
-hipError_t launch_finalize(const DevMatrix &A, const DevCtx &C, int mode, int32_t *y_idx, void *y_val,
+hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_idx, void *y_val,
                            int32_t *y_nnz, hipStream_t s)
 {
     int32_t nyw = (A.nbr + 1) / 2;
     dim3 g(grid_for(nyw, TPB * 2, INT_MAX)), b(TPB);
+    const int p = C.fin_parity;
+    uint64_t *st = C.st_fin[p], *nx = C.st_fin[1 - p];
+    const int32_t ns = C.n_st_fin;
     switch (mode) {
-    case M_F32: hipLaunchKernelGGL(k_finalize<M_F32>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, C.st_fin, C.xmask, C.act); break;
-    case M_F16: hipLaunchKernelGGL(k_finalize<M_F16>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, C.st_fin, C.xmask, C.act); break;
-    default: hipLaunchKernelGGL(k_finalize<M_BOOL>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, C.st_fin, C.xmask, C.act); break;
+    case M_F32: hipLaunchKernelGGL(k_finalize<M_F32>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, C.act); break;
+    case M_F16: hipLaunchKernelGGL(k_finalize<M_F16>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, C.act); break;
+    default: hipLaunchKernelGGL(k_finalize<M_BOOL>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, C.act); break;
     }
-    return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) C.fin_parity = 1 - p;
+    return e;
 }
 
 hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, void *y, float *y32,
@@ -961,7 +964,7 @@ hipError_t launch_bfs_update(const DevMatrix &A, const DevCtx &C, int32_t next_l
     int32_t nwords = (A.nbr + 1) / 2;
     dim3 g(grid_for(nwords, TPB, INT_MAX)), b(TPB);
     hipLaunchKernelGGL(k_bfs_update, g, b, 0, s, nwords, next_level, level, C.visited, C.nextm, C.xmask,
-                       C.counters, C.st_scan, C.n_st_scan);
+                       C.counters);
     return hipGetLastError();
 }
 

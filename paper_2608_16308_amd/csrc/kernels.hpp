@@ -45,10 +45,14 @@ struct DevCtx {
     uint32_t *visited = nullptr;  // BFS visited bitmap (row-block words)
     uint32_t *nextm = nullptr;    // BFS next-frontier bitmap
     int32_t *counters = nullptr;  // C_COUNT int32
-    uint64_t *st_scan = nullptr;  // look-back status of the active-block scan
+    // Look-back status words of the two scans, in two copies each: a call
+    // uses copy `parity` and clears the other copy for the next call, so no
+    // other kernel has to clean up after a scan.
+    uint64_t *st_scan[2] = {nullptr, nullptr};  // active-block scan
     int32_t n_st_scan = 0;
-    uint64_t *st_fin = nullptr;   // look-back status of the y compaction
+    uint64_t *st_fin[2] = {nullptr, nullptr};   // y compaction
     int32_t n_st_fin = 0;
+    int scan_parity = 0, fin_parity = 0;
 };
 
 enum Mode : int { M_F32 = 0, M_F16 = 1, M_BOOL = 2, M_BFS = 3 };
@@ -57,11 +61,11 @@ hipError_t launch_scatter(const DevMatrix &A, const DevCtx &C, int mode, int32_t
                           const int32_t *x_idx, const void *x_val, hipStream_t s);
 hipError_t launch_ballot(const DevMatrix &A, const DevCtx &C, int mode, const void *x_dense,
                          hipStream_t s);
-hipError_t launch_scan(const DevMatrix &A, const DevCtx &C, int forced_path, double th3,
+hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th3,
                        hipStream_t s);
 hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
                        const uint32_t *omask, int complement, int32_t *parent, hipStream_t s);
-hipError_t launch_finalize(const DevMatrix &A, const DevCtx &C, int mode, int32_t *y_idx,
+hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_idx,
                            void *y_val, int32_t *y_nnz, hipStream_t s);
 hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, void *y,
                                  float *y32, hipStream_t s);
