@@ -74,6 +74,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--point-reps", type=int, default=20)
     ap.add_argument("--json-out", default=None)
+    ap.add_argument("--profile-run", action="store_true",
+                    help="short run for rocprofv3 counter passes: a 1 GiB device copy (counter "
+                         "calibration) then warm-up + timed steps of the sweep only")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py: this build runs on one GPU only (single-GPU kernel library; "
@@ -89,6 +92,14 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
+    if args.profile_run:
+        # plain copy of known size: 1 GiB read + 1 GiB written per launch
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ------------------------------------------------------------ inputs
     t0 = time.time()
@@ -153,6 +164,13 @@ def main():
     achieved = step_main_bytes * args.steps / (main_ms * 1e-3) / 1e9
     log(f"[bench] {ms_per_step:.3f} ms/step, {value:.1f} GB/s whole path; traversal kernel "
         f"{main_avg_ms * 1e3:.1f} us/launch avg, {achieved:.1f} GB/s; per-class ms {timing}")
+    if args.profile_run:
+        per_launch = [{"density": p["density"], "x": p["kind"], "path": p["path"],
+                       "bytes_main": p["model"]["bytes_main"]} for p in points]
+        print(json.dumps({"profile_run": True, "steps": args.steps, "warmup": args.warmup,
+                          "main_bytes_per_step": step_main_bytes, "launch_order": per_launch,
+                          "kernel_sources": kernel_sources_digest()}), flush=True)
+        return
 
     # ------------------------------------------------------------ per point
     sweep = []

@@ -252,7 +252,7 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
     c.nxwords = (nb + 1) / 2 + 2;
     c.nywords = (nbr + 1) / 2 + 2;
     c.n_st_scan = (nbc + 1023) / 1024 + 1;
-    c.n_st_fin = ((nbr + 1) / 2 + 511) / 512 + 1;
+    c.n_st_fin = ((nbr + 1) / 2 + 255) / 256 + 1;
     uint32_t *xmask = nullptr, *ybits = nullptr, *visited = nullptr, *nextm = nullptr;
     float *xd = nullptr;
     if ((st = dev_zeros(ctx->allocs, (size_t)16 * nb, &xd)) != DBS_OK ||

@@ -674,6 +674,12 @@ __global__ __launch_bounds__(TPB) void k_main(MainArgs a)
 // ---------------------------------------------------------------------------
 // finalize: ascending sparse y from the row-block structure masks
 // ---------------------------------------------------------------------------
+// A tile is 256 structure words (8192 rows).  Thread t first owns word t
+// (its popcount enters the tile scan and the look-back); the rows are then
+// written in 32 rounds where thread t handles row t + 256 r of the tile, so
+// consecutive lanes touch consecutive accumulators and output slots.
+constexpr int FIN_WORDS = TPB;
+
 template <int MODE>
 __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, int32_t nywords,
                                                   double *__restrict__ yacc, int32_t m,
@@ -686,24 +692,21 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
 {
     __shared__ uint64_t lds4[TPB / WAVE];
     __shared__ uint64_t s_prefix;
+    __shared__ uint32_t s_word[FIN_WORDS];
+    __shared__ uint32_t s_wpos[FIN_WORDS];
     for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < n_status; i += gridDim.x * TPB)
         next_status[i] = 0;
     // clear blk_x_mask of this call's active vector blocks
     const int32_t N = counters[C_NZBLK];
     for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < N; i += gridDim.x * TPB)
         xmask[act[i] >> 1] = 0u;
-    // each thread owns 2 words = 4 row blocks
     const int tile = blockIdx.x;
-    const int32_t w0 = (tile * TPB + threadIdx.x) * 2;
-    uint32_t wv[2];
-    uint64_t mine = 0;
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-        wv[k] = (w0 + k) < nywords ? ybits[w0 + k] : 0u;
-        mine += (uint64_t)__popc(wv[k]);
-    }
+    const int32_t w = tile * FIN_WORDS + threadIdx.x;
+    const uint32_t word = w < nywords ? ybits[w] : 0u;
     uint64_t total;
-    uint64_t excl = block_exclusive_scan(mine, &total, lds4);
+    const uint64_t excl = block_exclusive_scan((uint64_t)__popc(word), &total, lds4);
+    s_word[threadIdx.x] = word;
+    s_wpos[threadIdx.x] = (uint32_t)excl;
     if (threadIdx.x < WAVE) {
         uint64_t prefix = 0;
         if (tile == 0) {
@@ -716,27 +719,26 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
         if (threadIdx.x == 0) s_prefix = prefix;
     }
     __syncthreads();
-    int64_t pos = (int64_t)(s_prefix + excl);
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-        uint32_t bits = wv[k];
-        if (!bits) continue;
-        while (bits) {
-            int bpos = ctz32(bits);
-            bits &= bits - 1;
-            int64_t i = (int64_t)(w0 + k) * 32 + bpos;  // word w covers rows 32w..32w+31
-            y_idx[pos] = (int32_t)i;
-            if constexpr (MODE == M_F32) {
-                ((float *)y_val)[pos] = (float)yacc[i];
-                yacc[i] = 0.0;
-            }
-            if constexpr (MODE == M_F16) {
-                ((uint16_t *)y_val)[pos] = f64_to_f16_rne(yacc[i]);
-                yacc[i] = 0.0;
-            }
-            ++pos;
+    if (word) ybits[w] = 0u;
+    const int64_t base_pos = (int64_t)s_prefix;
+    const int64_t row0 = (int64_t)tile * FIN_WORDS * 32;
+#pragma unroll 4
+    for (int r = 0; r < 32; ++r) {
+        const int lr = r * TPB + threadIdx.x;  // row within the tile
+        const uint32_t wd = s_word[lr >> 5];
+        const uint32_t bit = lr & 31;
+        if (!((wd >> bit) & 1u)) continue;
+        const int64_t pos = base_pos + s_wpos[lr >> 5] + __popc(wd & ((1u << bit) - 1u));
+        const int64_t i = row0 + lr;
+        y_idx[pos] = (int32_t)i;
+        if constexpr (MODE == M_F32) {
+            ((float *)y_val)[pos] = (float)yacc[i];
+            yacc[i] = 0.0;
         }
-        ybits[w0 + k] = 0u;
+        if constexpr (MODE == M_F16) {
+            ((uint16_t *)y_val)[pos] = f64_to_f16_rne(yacc[i]);
+            yacc[i] = 0.0;
+        }
     }
     if (tile == (int)gridDim.x - 1 && threadIdx.x == 0) {
         int32_t tot = (int32_t)(s_prefix + total);
@@ -922,7 +924,7 @@ hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_i
                            int32_t *y_nnz, hipStream_t s)
 {
     int32_t nyw = (A.nbr + 1) / 2;
-    dim3 g(grid_for(nyw, TPB * 2, INT_MAX)), b(TPB);
+    dim3 g(grid_for(nyw, FIN_WORDS, INT_MAX)), b(TPB);
     const int p = C.fin_parity;
     uint64_t *st = C.st_fin[p], *nx = C.st_fin[1 - p];
     const int32_t ns = C.n_st_fin;
