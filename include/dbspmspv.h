@@ -73,6 +73,8 @@ typedef struct {
     float th2;          /* skew ratio threshold -> ForceCSR / ForceCSC */
     int32_t seg_close;  /* pull segment closes when its weight >= seg_close (1..16 blocks) */
     int32_t force_type; /* -1 auto, else a dbs_block_type */
+    int32_t inline_small; /* 1: COO blocks that fit (1 fp32, 2 fp16 or 6 pattern entries)
+                             live in the descriptor word, no payload record; 0: never */
 } dbs_build_opts;
 
 /* Fills *o with the paper's defaults. */
@@ -123,7 +125,9 @@ dbs_status dbs_host_info(const dbs_host_matrix *h, dbs_matrix_info *out);
  *   cb_ptr[nbc+1]   block-CSC column pointer (global_block_csc_col_ptr)
  *   csc_row[nblk]   block row per CSC position (global_block_csc_row_idx)
  *   csc2csr[nblk]   primary block id per CSC position (global_block_csc2csr)
- *   desc[nblk]      bits 63..16 payload byte offset, 15..8 nnz-1, 2..0 block type
+ *   desc[nblk]      bits 63..16 payload byte offset, 15..8 nnz-1, 2..0 block type;
+ *                   bit 3 set: a COO block held inline, entry e at bits
+ *                   16 + e (8 + 8V): coordinate byte, then the V value bytes
  *   payload         one record per block in primary order, V = value bytes
  *                   (4 for F32, 2 for F16, 0 for PATTERN), entries of a block
  *                   ordered by (local row, local column):

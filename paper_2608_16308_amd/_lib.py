@@ -31,7 +31,8 @@ EXPORTED = [
 
 class BuildOpts(ctypes.Structure):
     _fields_ = [("th0", ctypes.c_int32), ("th1", ctypes.c_int32), ("th2", ctypes.c_float),
-                ("seg_close", ctypes.c_int32), ("force_type", ctypes.c_int32)]
+                ("seg_close", ctypes.c_int32), ("force_type", ctypes.c_int32),
+                ("inline_small", ctypes.c_int32)]
 
 
 class MatrixInfo(ctypes.Structure):
@@ -82,6 +83,14 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         return _lib
     if not os.path.exists(path):
         raise ImportError(f"{path} is not built; run __graft_entry__.build() (no CPU fallback exists)")
+    # torch ships its own HIP runtime (same soname as the system one).  Load it
+    # first so that this library binds to it: device pointers and streams
+    # from torch must belong to the runtime the library calls, and a second
+    # runtime in the process would hide the GPU from torch.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
     P = ctypes.POINTER

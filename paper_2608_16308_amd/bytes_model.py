@@ -24,7 +24,8 @@ distinct element once per kernel that needs it:
             per active vector block
 
 Record bytes read per visited block (V = value bytes):
-  COO   nnz coordinates + V per matching entry
+  COO   nnz coordinates + V per matching entry (none when held inline in the
+        descriptor)
   Dense 32 B masks + 256 V
   ForceCSR / ForceCSC / row-wise patched CSR   48 B header + V per matching entry
   column-wise patched CSR (fewer than 8 active columns)
@@ -46,6 +47,7 @@ class BytesModel:
         self.nnz = int(row_ptr[-1])
         desc = arrays["desc"]
         self.btype = (desc & np.uint64(7)).astype(np.int8)
+        self.binline = ((desc >> np.uint64(3)) & np.uint64(1)).astype(bool)
         self.bnnz = (((desc >> np.uint64(8)) & np.uint64(0xFF)) + np.uint64(1)).astype(np.int32)
         self.bcol = arrays["cb_col"].astype(np.int64)
         rb = arrays["rb_ptr"].astype(np.int64)
@@ -87,7 +89,7 @@ class BytesModel:
         popc_b = _POPC16[mx_b]
         t = self.btype
         rec = np.zeros(self.nblk, dtype=np.int64)
-        sel = act_b & (t == COO)
+        sel = act_b & (t == COO) & ~self.binline   # inline blocks live in the descriptor
         rec[sel] = self.bnnz[sel] + V * match_b[sel]
         sel = act_b & (t == DENSE)
         rec[sel] = 32 + 256 * V

@@ -80,6 +80,7 @@ struct TimedLaunch {
 
 struct dbs_ctx {
     int32_t max_m = 0, max_n = 0, max_nbr = 0, max_nbc = 0;
+    int64_t max_nblk = 0;
     hipStream_t stream = nullptr;
     DevCtx c;
     std::vector<void *> allocs;
@@ -147,9 +148,10 @@ dbs_status check_ctx(dbs_ctx *ctx, const dbs_matrix *A)
 {
     if (!ctx || !A) return dbs_fail(DBS_ERR_ARG, "NULL context or matrix");
     if (ctx->broken) return dbs_fail(DBS_ERR_STATE, "context unusable after an earlier device error");
-    if (A->d.m > ctx->max_m || A->d.n > ctx->max_n)
-        return dbs_fail(DBS_ERR_ARG, "matrix %dx%d exceeds the context's %dx%d", A->d.m, A->d.n,
-                        ctx->max_m, ctx->max_n);
+    if (A->d.m > ctx->max_m || A->d.n > ctx->max_n || A->d.nblk > ctx->max_nblk)
+        return dbs_fail(DBS_ERR_ARG, "matrix %dx%d with %lld blocks exceeds the context's %dx%d / %lld",
+                        A->d.m, A->d.n, (long long)A->d.nblk, ctx->max_m, ctx->max_n,
+                        (long long)ctx->max_nblk);
     return DBS_OK;
 }
 
@@ -243,6 +245,7 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
     ctx->max_n = sizing->d.n;
     ctx->max_nbr = sizing->d.nbr;
     ctx->max_nbc = sizing->d.nbc;
+    ctx->max_nblk = sizing->d.nblk;
     ctx->stream = (hipStream_t)stream;
     DevCtx &c = ctx->c;
     const int32_t nbr = std::max(ctx->max_nbr, 1), nbc = std::max(ctx->max_nbc, 1);
@@ -259,6 +262,7 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
         (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &xmask)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)nbc + 1, &c.act)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)nbc + 2, &c.task_off)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)nbc + 1, &c.pbase)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)16 * nbr, &c.yacc)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.nywords, &ybits)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &visited)) != DBS_OK ||
@@ -370,9 +374,10 @@ extern "C" dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring
     LAUNCH(ctx, DBS_K_SCATTER, launch_scatter(A->d, ctx->c, mode, x_nnz, d_x_idx, d_x_val, s));
     LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, (int)path, (double)norm_th3(th3), s));
     LAUNCH(ctx, DBS_K_MAIN,
-           launch_main(A->d, ctx->c, mode, ctx->c.xd, d_mask, complement_mask ? 1 : 0, nullptr, s));
+           launch_main(A->d, ctx->c, mode, ctx->c.xd, d_mask, complement_mask ? 1 : 0, nullptr, (int)path, s));
     LAUNCH(ctx, DBS_K_FINALIZE,
-           launch_finalize(A->d, ctx->c, mode, d_y_idx, sr == DBS_OR_AND ? nullptr : d_y_val, d_y_nnz, s));
+           launch_finalize(A->d, ctx->c, mode, d_y_idx, sr == DBS_OR_AND ? nullptr : d_y_val, d_y_nnz,
+                           d_x_idx, x_nnz, s));
     if (stats) {
         if ((st = sync_counters(ctx)) != DBS_OK) return st;
         const int32_t *h = ctx->h_counters;
@@ -400,7 +405,7 @@ extern "C" dbs_status dbs_spmspv_dense(dbs_ctx *ctx, const dbs_matrix *A, const 
     const hipStream_t s = ctx->stream;
     LAUNCH(ctx, DBS_K_SCATTER, launch_ballot(A->d, ctx->c, mode, d_x_dense, s));
     LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, (int)path, (double)norm_th3(th3), s));
-    LAUNCH(ctx, DBS_K_MAIN, launch_main(A->d, ctx->c, mode, ctx->c.xd, nullptr, 0, nullptr, s));
+    LAUNCH(ctx, DBS_K_MAIN, launch_main(A->d, ctx->c, mode, ctx->c.xd, nullptr, 0, nullptr, (int)path, s));
     LAUNCH(ctx, DBS_K_FINALIZE, launch_finalize_dense(A->d, ctx->c, mode, d_y_dense, d_y_f32, s));
     if (stats) {
         if ((st = sync_counters(ctx)) != DBS_OK) return st;
@@ -448,7 +453,8 @@ extern "C" dbs_status dbs_bfs(dbs_ctx *ctx, const dbs_matrix *A, int32_t source,
             stats->path[level] = h[C_PATH];
             stats->frontier[level] = frontier;
         }
-        LAUNCH(ctx, DBS_K_MAIN, launch_main(A->d, ctx->c, M_BFS, nullptr, ctx->c.visited, 1, d_parent, s));
+        LAUNCH(ctx, DBS_K_MAIN,
+               launch_main(A->d, ctx->c, M_BFS, nullptr, ctx->c.visited, 1, d_parent, (int)policy, s));
         LAUNCH(ctx, DBS_K_BFS_UPDATE, launch_bfs_update(A->d, ctx->c, level + 1, d_level, s));
         ++level;
     }

@@ -50,6 +50,7 @@ extern "C" void dbs_build_opts_default(dbs_build_opts *o)
     o->th2 = 2.0f;
     o->seg_close = 16;
     o->force_type = -1;
+    o->inline_small = 1;
 }
 
 namespace {
@@ -237,6 +238,22 @@ void write_record(uint8_t *dst, uint32_t type, const Entry *e, uint32_t nnz, con
     }
 }
 
+// Descriptor of a COO block small enough to live inline (bit 3 set).
+uint64_t inline_desc(const Entry *e, uint32_t nnz, const void *vals, uint32_t vb)
+{
+    uint64_t d = ((uint64_t)(nnz - 1) << 8) | DESC_INLINE | (uint64_t)T_COO;
+    for (uint32_t k = 0; k < nnz; ++k) {
+        const uint32_t sh = inline_shift(k, vb);
+        d |= (uint64_t)(e[k].key & 0xFF) << sh;
+        if (vb) {
+            uint64_t bits = 0;
+            std::memcpy(&bits, (const uint8_t *)vals + e[k].p * vb, vb);
+            d |= bits << (sh + 8);
+        }
+    }
+    return d;
+}
+
 struct RowBlockSizes {
     int64_t nblk = 0, bytes = 0, nseg = 0;
 };
@@ -260,9 +277,11 @@ RowBlockSizes walk_block_row(const std::vector<Entry> &ents, const dbs_build_opt
         while (e < ents.size() && (ents[e].key >> 8) == J) ++e;
         uint32_t nnz = (uint32_t)(e - k);
         uint32_t type = classify(&ents[k], nnz, o);
-        cursor = (cursor + record_align(type, vb) - 1) / record_align(type, vb) * record_align(type, vb);
-        on_block(k, nnz, type, cursor, (int32_t)J);
-        cursor += record_bytes(type, nnz, vb);
+        const bool inl = o.inline_small && type == T_COO && nnz <= inline_capacity(vb);
+        if (!inl)
+            cursor = (cursor + record_align(type, vb) - 1) / record_align(type, vb) * record_align(type, vb);
+        on_block(k, nnz, type, inl ? ~0ull : cursor, (int32_t)J);
+        if (!inl) cursor += record_bytes(type, nnz, vb);
         seg_w += seg_weight(type);
         seg_cnt += 1;
         if ((int32_t)seg_w >= o.seg_close || seg_cnt == (uint32_t)MAX_SEG_BLOCKS) {
@@ -333,7 +352,7 @@ extern "C" dbs_status dbs_host_build_csr(int32_t m, int32_t n, int64_t nnz, cons
     dbs_build_opts_default(&o);
     if (opts) o = *opts;
     if (o.th0 < 0 || o.th1 < 0 || !(o.th2 > 0.0f) || o.seg_close < 1 || o.force_type < -1 ||
-        o.force_type >= DBS_NUM_BLOCK_TYPES)
+        o.force_type >= DBS_NUM_BLOCK_TYPES || (o.inline_small != 0 && o.inline_small != 1))
         return dbs_fail(DBS_ERR_ARG, "invalid build options");
     if (row_ptr[0] != 0 || row_ptr[m] != nnz)
         return dbs_fail(DBS_ERR_ARG, "row_ptr[0] must be 0 and row_ptr[m] must equal nnz");
@@ -414,9 +433,13 @@ extern "C" dbs_status dbs_host_build_csr(int32_t m, int32_t n, int64_t nnz, cons
                 walk_block_row(
                     ents, o, vb,
                     [&](size_t k, uint32_t nnz, uint32_t type, uint64_t off, int32_t J) {
-                        write_record(h->payload.data() + base + off, type, &ents[k], nnz, vals, vb);
                         h->cb_col[b] = J;
-                        h->desc[b] = desc_make(base + off, nnz, type);
+                        if (off == ~0ull) {
+                            h->desc[b] = inline_desc(&ents[k], nnz, vals, vb);
+                        } else {
+                            write_record(h->payload.data() + base + off, type, &ents[k], nnz, vals, vb);
+                            h->desc[b] = desc_make(base + off, nnz, type);
+                        }
                         ++b;
                     },
                     [&](int64_t first_local, uint32_t cnt) {

@@ -42,6 +42,15 @@ DBS_HD uint64_t desc_off(uint64_t d) { return d >> 16; }
 DBS_HD uint32_t desc_nnz(uint64_t d) { return (uint32_t)((d >> 8) & 0xFFu) + 1u; }
 DBS_HD uint32_t desc_type(uint64_t d) { return (uint32_t)(d & 7u); }
 
+// Small COO blocks are stored inside the descriptor instead of the payload
+// (bit 3 set): entry e occupies bits [16 + e (8 + 8V), ...) as the
+// coordinate byte followed by the V value bytes.  Capacity: 1 entry for
+// fp32, 2 for fp16, 6 for pattern matrices.
+constexpr uint64_t DESC_INLINE = 8u;
+DBS_HD bool desc_inline(uint64_t d) { return (d & DESC_INLINE) != 0; }
+DBS_HD uint32_t inline_capacity(uint32_t vbytes) { return 48u / (8u + 8u * vbytes); }
+DBS_HD uint32_t inline_shift(uint32_t e, uint32_t vbytes) { return 16u + e * (8u + 8u * vbytes); }
+
 DBS_HD uint64_t seg_make(uint32_t first, uint32_t brow, uint32_t nb, bool single)
 {
     return (uint64_t)first | ((uint64_t)brow << 32) | ((uint64_t)(nb - 1) << 59) |

@@ -44,6 +44,13 @@ __device__ __forceinline__ T wave_sum(T v)
     return v;
 }
 
+__device__ __forceinline__ uint32_t wave_or(uint32_t v)
+{
+#pragma unroll
+    for (int o = 1; o < WAVE; o <<= 1) v |= __shfl_xor(v, o, WAVE);
+    return v;
+}
+
 __device__ __forceinline__ uint32_t or16_in_quarter(uint32_t v)
 {
     // OR over the 16 lanes of this lane's quarter-wave.

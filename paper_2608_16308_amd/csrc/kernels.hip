@@ -7,7 +7,7 @@
 //                         ascending list of nonzero vector blocks, N_nzblk, the
 //                         push task offsets, and the global push/pull choice
 //                         s_b = N_nzblk / N_blk < th3 (Sec. 3.3.1)
-//   k_main                push (block tasks flattened over the block-CSC lists
+//   k_traverse            push (block tasks flattened over the block-CSC lists
 //                         of the active column blocks, fetched grid-stride) or
 //                         pull (weighted row-block segments), with a per-block
 //                         microkernel chosen from the block format and the
@@ -36,7 +36,7 @@ namespace dbs {
 constexpr int TPB = 256;            // threads per workgroup (4 waves)
 constexpr int SCAN_ITEMS = 4;       // items per thread in the look-back scans
 constexpr int SCAN_TILE = TPB * SCAN_ITEMS;
-constexpr int MAX_MAIN_GRID = 2048; // 256 CUs x 8 workgroups
+constexpr int MAX_MAIN_GRID = 4096; // upper bound: 256 CUs x 16 workgroups
 
 constexpr uint64_t ST_AGG = 1ull << 62, ST_INC = 2ull << 62, ST_PAYLOAD = (1ull << 62) - 1;
 
@@ -129,25 +129,38 @@ __device__ uint64_t block_exclusive_scan(uint64_t v, uint64_t *total, uint64_t *
 // ---------------------------------------------------------------------------
 // vector blocker
 // ---------------------------------------------------------------------------
+// Sparse x: scatter the values into the dense scratch and set the mask bits.
+// The first index that lands in a vector block counts it (N_nzblk, Sec. 3.3.1);
+// an index whose bit is already set is a duplicate and is flagged.
 template <int MODE>
 __global__ __launch_bounds__(TPB) void k_scatter(const int32_t *__restrict__ xi,
                                                  const void *__restrict__ xv, int32_t k, int32_t n,
                                                  void *__restrict__ xd, uint32_t *__restrict__ xmask,
                                                  int32_t *__restrict__ counters)
 {
-    int32_t t = blockIdx.x * TPB + threadIdx.x;
-    if (t >= k) return;
-    int32_t j = xi[t];
-    if (j < 0 || j >= n) {
-        atomicOr(&counters[C_ERR], 1);
-        return;
+    const int32_t t = blockIdx.x * TPB + threadIdx.x;
+    bool first = false, bad = false, dup = false;
+    if (t < k) {
+        const int32_t j = xi[t];
+        if (j < 0 || j >= n) {
+            bad = true;
+        } else {
+            if constexpr (MODE == M_F32) ((float *)xd)[j] = ((const float *)xv)[t];
+            if constexpr (MODE == M_F16) ((uint16_t *)xd)[j] = ((const uint16_t *)xv)[t];
+            const uint32_t J = (uint32_t)j >> 4;
+            const uint32_t half = (J & 1) * 16;
+            const uint32_t bit = 1u << (half + (j & 15));
+            const uint32_t old = atomicOr(&xmask[J >> 1], bit);
+            dup = (old & bit) != 0;
+            first = !dup && ((old >> half) & 0xFFFFu) == 0;
+        }
     }
-    if constexpr (MODE == M_F32) ((float *)xd)[j] = ((const float *)xv)[t];
-    if constexpr (MODE == M_F16) ((uint16_t *)xd)[j] = ((const uint16_t *)xv)[t];
-    uint32_t J = (uint32_t)j >> 4;
-    uint32_t bit = 1u << ((J & 1) * 16 + (j & 15));
-    uint32_t old = atomicOr(&xmask[J >> 1], bit);
-    if (old & bit) atomicOr(&counters[C_ERR], 2);
+    // one counter update per wave
+    const uint64_t fm = ballot(first), bm = ballot(bad), dm = ballot(dup);
+    if (lane_id() == 0) {
+        if (fm) atomicAdd(&counters[C_NZACC], (int32_t)__popcll(fm));
+        if (bm | dm) atomicOr(&counters[C_ERR], (bm ? 1 : 0) | (dm ? 2 : 0));
+    }
 }
 
 // Dense activation (Sec. 4.1): each wave reads 64 consecutive entries and
@@ -157,7 +170,8 @@ __global__ __launch_bounds__(TPB) void k_scatter(const int32_t *__restrict__ xi,
 template <int MODE>
 __global__ __launch_bounds__(TPB) void k_ballot(const void *__restrict__ x, int32_t n,
                                                 void *__restrict__ xd,
-                                                uint32_t *__restrict__ xmask, int32_t nwords)
+                                                uint32_t *__restrict__ xmask, int32_t nwords,
+                                                int32_t *__restrict__ counters)
 {
     int64_t j = (int64_t)blockIdx.x * TPB + threadIdx.x;
     bool nz = false;
@@ -177,13 +191,23 @@ __global__ __launch_bounds__(TPB) void k_ballot(const void *__restrict__ x, int3
         int64_t w = (j - lane_id()) >> 5;
         if (w < nwords) xmask[w] = (uint32_t)b;
         if (w + 1 < nwords) xmask[w + 1] = (uint32_t)(b >> 32);
+        int cnt = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) cnt += ((b >> (16 * q)) & 0xFFFFull) != 0;
+        if (cnt) atomicAdd(&counters[C_NZACC], cnt);
     }
 }
 
-// Active vector blocks, their push task offsets and the path choice.
+// Single-pass scan over vector blocks.  Every nonzero vector block J whose
+// block column holds matrix blocks becomes one push work item:
+//   act[a] = J, task_off[a] = first task, pbase[a] = cb_ptr[J] - task_off[a]
+// so that task t of item a visits block-CSC position pbase[a] + t.  The last
+// tile fixes N_nzblk (counted by the blocker), the task totals and the
+// global path: push iff N_nzblk < th3 N_blk (Sec. 3.3.1).
 __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask,
                                               const int32_t *__restrict__ cb_ptr, int32_t nbc,
                                               int32_t *__restrict__ act, int32_t *__restrict__ task_off,
+                                              int32_t *__restrict__ pbase,
                                               int32_t *__restrict__ counters, uint64_t *status,
                                               uint64_t *next_status, int32_t n_status,
                                               int32_t forced_path, double th3)
@@ -195,15 +219,16 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
         next_status[i] = 0;
     const int tile = blockIdx.x;
     const int32_t base = tile * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
-    uint32_t am[SCAN_ITEMS];
+    int32_t start[SCAN_ITEMS];
     uint32_t len[SCAN_ITEMS];
     uint64_t mine = 0;
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
-        int32_t J = base + k;
-        am[k] = J < nbc ? mask16(xmask, J) : 0u;
-        len[k] = am[k] ? (uint32_t)(cb_ptr[J + 1] - cb_ptr[J]) : 0u;
-        if (am[k]) mine += (1ull << 34) + len[k];
+        const int32_t J = base + k;
+        const uint32_t am = J < nbc ? mask16(xmask, J) : 0u;
+        start[k] = am ? cb_ptr[J] : 0;
+        len[k] = am ? (uint32_t)(cb_ptr[J + 1] - start[k]) : 0u;
+        if (len[k]) mine += (1ull << 34) + len[k];
     }
     uint64_t total;
     uint64_t excl = block_exclusive_scan(mine, &total, lds4);
@@ -219,25 +244,29 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
         if (threadIdx.x == 0) s_prefix = prefix;
     }
     __syncthreads();
-    uint64_t pos = s_prefix + excl;
+    const uint64_t pos = s_prefix + excl;
     int64_t idx = (int64_t)(pos >> 34);
     int64_t off = (int64_t)(pos & ((1ull << 34) - 1));
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
-        if (am[k]) {
+        if (len[k]) {
             act[idx] = base + k;
             task_off[idx] = (int32_t)off;
+            pbase[idx] = start[k] - (int32_t)off;
             ++idx;
             off += len[k];
         }
     }
     if (tile == (int)gridDim.x - 1 && threadIdx.x == 0) {
-        uint64_t all = s_prefix + total;
-        int32_t N = (int32_t)(all >> 34);
-        int32_t T = (int32_t)(all & ((1ull << 34) - 1));
+        const uint64_t all = s_prefix + total;
+        const int32_t NT = (int32_t)(all >> 34);
+        const int32_t T = (int32_t)(all & ((1ull << 34) - 1));
+        const int32_t N = counters[C_NZACC];
+        counters[C_NZACC] = 0;
         counters[C_NZBLK] = N;
+        counters[C_NTB] = NT;
         counters[C_TASKS] = T;
-        task_off[N] = T;
+        task_off[NT] = T;
         int path = forced_path;
         if (path == 0) path = ((double)N < th3 * (double)nbc) ? PATH_PUSH : PATH_PULL;
         counters[C_PATH] = path;
@@ -248,11 +277,59 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
 // block microkernels
 // ---------------------------------------------------------------------------
 
-// One lane, one COO block (packed 4-bit row | 4-bit column coordinates,
-// entries in row-major order).  Adds the products of entries whose column is
-// active and whose row is admitted into dst16[row] (LDS), merging runs of
-// one row first; for BFS records the smallest active column per row (the
-// first one met, since columns ascend within a row).  Returns the rows hit.
+// Coordinate bytes (row << 4 | col) of a COO block with at most 8 entries,
+// byte e of the result for entry e: from the descriptor when the block is
+// held inline, else with at most three aligned dword loads covering the
+// record's coordinate bytes (the payload is padded to 16 bytes, so the last
+// covering dword is inside it).
+__device__ __forceinline__ uint64_t coo_coords(uint64_t d, const uint8_t *rec, uint32_t vb, uint32_t nnz)
+{
+    if (desc_inline(d)) {
+        if (nnz == 1) return (d >> 16) & 0xFFull;  // the common hypersparse case
+        uint64_t c = 0;
+        for (uint32_t e = 0; e < nnz; ++e) c |= ((d >> inline_shift(e, vb)) & 0xFFull) << (8 * e);
+        return c;
+    }
+    const uintptr_t a = (uintptr_t)(rec + vb * nnz);  // coordinates follow the values
+    const uint32_t mis = (uint32_t)(a & 3u);
+    const uint32_t *w = (const uint32_t *)(a - mis);
+    const uint32_t nw = (mis + nnz + 3) / 4;
+    const uint32_t w0 = w[0], w1 = nw > 1 ? w[1] : 0u, w2 = nw > 2 ? w[2] : 0u;
+    const uint64_t lo = ((uint64_t)w1 << 32) | w0;
+    return mis ? ((lo >> (8 * mis)) | ((uint64_t)w2 << (64 - 8 * mis))) : lo;
+}
+
+// Value of entry e of a COO block (inline or from its record).
+template <int MODE>
+__device__ __forceinline__ float coo_value(uint64_t d, const uint8_t *rec, uint32_t vb, uint32_t e)
+{
+    if constexpr (MODE == M_F32) {
+        if (desc_inline(d)) return __uint_as_float((uint32_t)(d >> (inline_shift(e, vb) + 8)));
+        return VT<MODE>::load(rec, e);
+    } else if constexpr (MODE == M_F16) {
+        if (desc_inline(d)) return h2f((uint16_t)(d >> (inline_shift(e, vb) + 8)));
+        return VT<MODE>::load(rec, e);
+    } else {
+        return 0.f;
+    }
+}
+
+// Bit e set for every entry e of a COO block whose column is active in the
+// vector-block mask and whose row is admitted.
+__device__ __forceinline__ uint32_t coo_matches(uint64_t cds, uint32_t nnz, uint32_t mx, uint32_t am)
+{
+    uint32_t mm = 0;
+    for (uint32_t e = 0; e < nnz; ++e) {
+        const uint32_t cd = (uint32_t)(cds >> (8 * e)) & 0xFFu;
+        mm |= ((mx >> (cd & 15u)) & (am >> (cd >> 4)) & 1u) << e;
+    }
+    return mm;
+}
+
+// One lane, one COO block of at most 8 entries (entries in row-major order).
+// Adds the products of the matching entries into dst16[row] (LDS), merging
+// runs of one row first; for BFS records the smallest active column per row
+// (the first match met, columns ascend within a row).  Returns the rows hit.
 template <int MODE>
 __device__ __forceinline__ uint32_t coo_block(const uint8_t *__restrict__ pay, uint32_t vb, uint64_t d,
                                               int32_t J, uint32_t mx, uint32_t am,
@@ -260,17 +337,18 @@ __device__ __forceinline__ uint32_t coo_block(const uint8_t *__restrict__ pay, u
                                               int32_t *pdst16)
 {
     const uint32_t nnz = desc_nnz(d);
-    const uint8_t *rec = pay + desc_off(d);
-    const uint8_t *crd = rec + vb * nnz;  // coordinates follow the matrix's values
+    const uint8_t *rec = desc_inline(d) ? nullptr : pay + desc_off(d);
+    const uint64_t cds = coo_coords(d, rec, vb, nnz);
+    uint32_t mm = coo_matches(cds, nnz, mx, am);
     uint32_t hit = 0;
     int cur = -1;
     float acc = 0.f;
-    for (uint32_t e = 0; e < nnz; ++e) {
-        uint32_t cd = crd[e];
-        uint32_t r = cd >> 4, c = cd & 15u;
-        if (!((mx >> c) & (am >> r) & 1u)) continue;
+    while (mm) {
+        const uint32_t e = ctz32(mm);
+        mm &= mm - 1;
+        const uint32_t cd = (uint32_t)(cds >> (8 * e)) & 0xFFu, r = cd >> 4, c = cd & 15u;
         if constexpr (valued<MODE>()) {
-            float prod = VT<MODE>::load(rec, e) * VT<MODE>::x(xd, (int64_t)J * BS + c);
+            const float prod = coo_value<MODE>(d, rec, vb, e) * VT<MODE>::x(xd, (int64_t)J * BS + c);
             if ((int)r != cur) {
                 if (cur >= 0) atomicAdd(&dst16[cur], acc);
                 cur = (int)r;
@@ -298,17 +376,18 @@ __device__ __forceinline__ uint32_t coo_block_push(const uint8_t *__restrict__ p
                                                    double *yacc, int32_t *parent)
 {
     const uint32_t nnz = desc_nnz(d);
-    const uint8_t *rec = pay + desc_off(d);
-    const uint8_t *crd = rec + vb * nnz;
+    const uint8_t *rec = desc_inline(d) ? nullptr : pay + desc_off(d);
+    const uint64_t cds = coo_coords(d, rec, vb, nnz);
+    uint32_t mm = coo_matches(cds, nnz, mx, am);
     uint32_t hit = 0;
     int cur = -1;
     float acc = 0.f;
-    for (uint32_t e = 0; e < nnz; ++e) {
-        uint32_t cd = crd[e];
-        uint32_t r = cd >> 4, c = cd & 15u;
-        if (!((mx >> c) & (am >> r) & 1u)) continue;
+    while (mm) {
+        const uint32_t e = ctz32(mm);
+        mm &= mm - 1;
+        const uint32_t cd = (uint32_t)(cds >> (8 * e)) & 0xFFu, r = cd >> 4, c = cd & 15u;
         if constexpr (valued<MODE>()) {
-            float prod = VT<MODE>::load(rec, e) * VT<MODE>::x(xd, (int64_t)J * BS + c);
+            const float prod = coo_value<MODE>(d, rec, vb, e) * VT<MODE>::x(xd, (int64_t)J * BS + c);
             if ((int)r != cur) {
                 if (cur >= 0) atomicAdd(&yacc[(int64_t)R * BS + cur], (double)acc);
                 cur = (int)r;
@@ -328,6 +407,15 @@ __device__ __forceinline__ uint32_t coo_block_push(const uint8_t *__restrict__ p
     return hit;
 }
 
+// COO blocks with at most this many entries are processed by one lane;
+// longer ones by the whole wave.
+constexpr uint32_t COO_LANE_MAX = 8;
+static_assert(COO_LANE_MAX <= 8, "coo_coords gathers at most 8 coordinate bytes");
+__device__ __forceinline__ bool lane_coo(uint64_t d)
+{
+    return desc_type(d) == T_COO && desc_nnz(d) <= COO_LANE_MAX;
+}
+
 // i-th set bit of v (i >= 0), or -1.
 __device__ __forceinline__ int nth_set_bit(uint32_t v, int i)
 {
@@ -339,7 +427,7 @@ __device__ __forceinline__ int nth_set_bit(uint32_t v, int i)
 // admitted rows into dst16 (LDS); for BFS records the smallest active
 // column per row in pdst16.  Returns the rows hit (uniform).
 template <int MODE>
-__device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint64_t d, int32_t J,
+__device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint32_t vb, uint64_t d, int32_t J,
                                 uint32_t mx, uint32_t am, const void *__restrict__ xd, float *dst16,
                                 int32_t *pdst16)
 {
@@ -349,6 +437,21 @@ __device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint64_t d, int
     const uint16_t *msk = (const uint16_t *)(rec + HDR_MASK);
     const uint8_t *st = rec + HDR_START;
     const int64_t xb = (int64_t)J * BS;
+
+    if (type == T_COO) {
+        // A COO block too long for one lane: one entry per lane (Sec. 3.3.3:
+        // COO blocks scan their packed coordinates and accumulate in LDS).
+        const uint8_t *crd = rec + vb * nnz;
+        uint32_t hl = 0;
+        for (uint32_t e = lane; e < nnz; e += WAVE) {
+            const uint32_t cd = crd[e], r = cd >> 4, c = cd & 15u;
+            if (!((mx >> c) & (am >> r) & 1u)) continue;
+            if constexpr (valued<MODE>()) atomicAdd(&dst16[r], VT<MODE>::load(rec, e) * VT<MODE>::x(xd, xb + c));
+            if constexpr (MODE == M_BFS) atomicMin(&pdst16[r], (int32_t)xb + (int32_t)c);
+            hl |= 1u << r;
+        }
+        return wave_or(hl);
+    }
 
     if constexpr (!valued<MODE>()) {
         // Boolean propagation (Alg. 5): per row lane, the active columns with a
@@ -486,16 +589,11 @@ __device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint64_t d, int
                 }
                 for (int q = 0; q < 4 && cols; ++q) cols &= cols - 1;
             }
-            hl |= __shfl_xor(hl, 1, WAVE);
-            hl |= __shfl_xor(hl, 2, WAVE);
-            hl |= __shfl_xor(hl, 4, WAVE);
-            hl |= __shfl_xor(hl, 8, WAVE);
-            hl |= __shfl_xor(hl, 16, WAVE);
-            hl |= __shfl_xor(hl, 32, WAVE);
-            return hl;
+            return wave_or(hl);
         }
     }
 }
+
 
 // ---------------------------------------------------------------------------
 // main traversal kernel
@@ -505,15 +603,16 @@ struct MainArgs {
     const uint64_t *desc;
     const uint8_t *pay;
     uint32_t vb;            // value bytes of the matrix (4, 2 or 0)
-    const int32_t *cb_ptr;
+    int32_t nbc;
     const int32_t *csc_row;
     const int32_t *csc2csr;
     const uint64_t *seg;
     int64_t nseg;
     const void *xd;
     const uint32_t *xmask;
-    const int32_t *act;
+    const int32_t *act;          // push work items (see k_scan)
     const int32_t *task_off;
+    const int32_t *pbase;
     int32_t *counters;
     const uint32_t *omask;  // output mask bitmap (NULL = none); BFS: visited
     int32_t complement;
@@ -522,153 +621,343 @@ struct MainArgs {
     int32_t *parent;        // BFS only
 };
 
-template <int MODE>
+// Independent work units per lane and loop iteration: four segments per
+// quarter-wave (pull) or four 64-task chunks per wave (push), so that four
+// dependent load chains are in flight per lane instead of one.
+constexpr int SLOTS = 4;
+
 __device__ __forceinline__ uint32_t row_admit(const MainArgs &a, int32_t R)
 {
     return allowed16(a.omask, a.complement, R);
 }
 
-// Pull (Sec. 3.3.2): one quarter-wave per row-block segment, 4 segments per
-// wave, grid-stride over segments.
+// Blocks staged for whole-wave processing: slot-major, one entry per lane.
+// After an entry is processed its J word carries the rows hit back to the
+// lane that staged it (5 KB per wave, so that the traversal kernels' LDS
+// stays well inside the compute unit's 160 KB at full occupancy).
+struct HeavyStage {
+    uint64_t d[SLOTS * WAVE];
+    int32_t J[SLOTS * WAVE];      // block column; rows hit once processed
+    int32_t R[SLOTS * WAVE];
+    uint32_t mxam[SLOTS * WAVE];  // vector-block mask | admitted rows << 16
+    __device__ __forceinline__ void stage(int e, uint64_t dd, int32_t j, uint32_t mx, uint32_t am, int32_t r)
+    {
+        d[e] = dd;
+        J[e] = j;
+        R[e] = r;
+        mxam[e] = mx | (am << 16);
+    }
+    __device__ __forceinline__ uint32_t hits(int e) const { return (uint32_t)J[e]; }
+};
+
+// Processes the staged blocks of the wave one at a time with the whole wave.
+// Pull: the partial row sums go to the owning quarter's LDS accumulators of
+// that slot.  Push: each block's row sums are committed to HBM at once.  The
+// rows hit are handed back through hs->hits to the lane that staged the block.
 template <int MODE>
-__device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp)
+__device__ void run_staged(const MainArgs &a, HeavyStage *hs, const uint64_t (&hv)[SLOTS], float *sy,
+                           int32_t *sp, bool push)
+{
+    const int lane = lane_id();
+    for (int k = 0; k < SLOTS; ++k) {
+        uint64_t m = k == 0 ? hv[0] : k == 1 ? hv[1] : k == 2 ? hv[2] : hv[3];
+        while (m) {
+            const int L = ctz64(m);
+            m &= m - 1;
+            const int e = k * WAVE + L;
+            const uint64_t dL = hs->d[e];
+            const int32_t JL = hs->J[e];
+            const uint32_t mxam = hs->mxam[e];
+            float *dst = push ? sy : sy + k * WAVE + (L >> 4) * 16;
+            int32_t *pdst = push ? sp : sp + k * WAVE + (L >> 4) * 16;
+            const uint32_t h = heavy_block<MODE>(a.pay, a.vb, dL, JL, mxam & 0xFFFFu, mxam >> 16, a.xd, dst, pdst);
+            if (push) {
+                const int32_t RL = hs->R[e];
+                wave_lds_sync();
+                if (lane < 16) {
+                    const int64_t row = (int64_t)RL * BS + lane;
+                    if ((h >> lane) & 1u) {
+                        if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], (double)sy[lane]);
+                        if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], sp[lane]);
+                    }
+                    if constexpr (valued<MODE>()) sy[lane] = 0.f;
+                    if constexpr (MODE == M_BFS) sp[lane] = INT_MAX;
+                }
+                wave_lds_sync();
+            }
+            if (lane == L) hs->J[e] = (int32_t)h;
+        }
+    }
+    wave_lds_sync();
+}
+
+// Pull (Sec. 3.3.2): a quarter-wave per row-block segment (<= 16 blocks,
+// one block per lane); a quarter takes SLOTS consecutive segments per
+// iteration, consecutive slots of one block row are folded in registers
+// before the commit (Sec. 3.3.3's local aggregation), grid-stride over
+// segment groups.  Blocks that need the whole wave (non-COO formats, long
+// COO blocks) are staged in LDS and processed one by one after the
+// lane-parallel COO work, from a single call site.
+template <int MODE>
+__device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage *hs,
+                          bool spec)
 {
     const int lane = lane_id(), q = lane >> 4, i = lane & 15;
-    const int64_t units = (a.nseg + 3) / 4;
-    for (int64_t u = gw; u < units; u += nw) {
-        const int64_t sid = u * 4 + q;
-        const bool vs = sid < a.nseg;
-        const uint64_t s = vs ? a.seg[sid] : 0ull;
-        const int32_t R = (int32_t)seg_brow(s);
-        const uint32_t nb = seg_nb(s);
-        const bool single = seg_single(s);
-        const uint32_t am = vs ? row_admit<MODE>(a, R) : 0u;
-        bool act = vs && (uint32_t)i < nb && am != 0;
-        const int32_t b = (int32_t)seg_first(s) + i;
-        int32_t J = 0;
-        uint32_t mx = 0;
-        uint64_t d = 0;
-        if (act) {
-            J = a.cb_col[b];
-            mx = mask16(a.xmask, J);
-            act = mx != 0;
+    // segments per quarter and iteration: SLOTS when there is enough work to
+    // keep every wave busy with SLOTS of them, else 1
+    const int spq = a.nseg >= (int64_t)nw * 4 * SLOTS * 2 ? SLOTS : 1;
+    const int64_t groups = (a.nseg + 4 * spq - 1) / (4 * spq);
+    for (int64_t u = gw; u < groups; u += nw) {
+        uint64_t s[SLOTS], d[SLOTS];
+        bool vs[SLOTS], act[SLOTS];
+        int32_t b[SLOTS], J[SLOTS];
+        uint32_t am[SLOTS], mx[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            const int64_t sid = u * 4 * spq + q * spq + k;
+            vs[k] = k < spq && sid < a.nseg;
+            s[k] = vs[k] ? a.seg[sid] : 0ull;
         }
-        if (act) d = a.desc[b];
-        const uint32_t type = desc_type(d);
-        uint32_t hit = 0;
-        if (act && type == T_COO)
-            hit = coo_block<MODE>(a.pay, a.vb, d, J, mx, am, a.xd, sy + q * 16, sp + q * 16);
-        uint64_t hv = ballot(act && type != T_COO);
-        while (hv) {
-            const int L = ctz64(hv);
-            hv &= hv - 1;
-            const uint64_t dL = readlane_u64(d, L);
-            const int32_t JL = (int32_t)readlane_u32((uint32_t)J, L);
-            const uint32_t mxL = readlane_u32(mx, L), amL = readlane_u32(am, L);
-            const int qL = L >> 4;
-            uint32_t h = heavy_block<MODE>(a.pay, dL, JL, mxL, amL, a.xd, sy + qL * 16, sp + qL * 16);
-            if (lane == L) hit |= h;
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            am[k] = vs[k] ? row_admit(a, (int32_t)seg_brow(s[k])) : 0u;
+            act[k] = vs[k] && (uint32_t)i < seg_nb(s[k]) && am[k] != 0;
+            b[k] = (int32_t)seg_first(s[k]) + i;
+            J[k] = act[k] ? a.cb_col[b[k]] : 0;
+            d[k] = (act[k] && spec) ? a.desc[b[k]] : 0ull;
+        }
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            mx[k] = act[k] ? mask16(a.xmask, J[k]) : 0u;
+            act[k] = act[k] && mx[k] != 0;
+        }
+        if (!spec) {
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k) d[k] = act[k] ? a.desc[b[k]] : 0ull;
+        }
+        uint32_t hit[SLOTS];
+        uint64_t hv[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            hit[k] = 0;
+            const bool lanework = act[k] && lane_coo(d[k]);
+            if (lanework)
+                hit[k] = coo_block<MODE>(a.pay, a.vb, d[k], J[k], mx[k], am[k], a.xd,
+                                         sy + k * WAVE + q * 16, sp + k * WAVE + q * 16);
+            const bool wavework = act[k] && !lanework;
+            hv[k] = ballot(wavework);
+            if (wavework) hs->stage(k * WAVE + lane, d[k], J[k], mx[k], am[k], 0);
+        }
+        if (hv[0] | hv[1] | hv[2] | hv[3]) {
+            wave_lds_sync();
+            run_staged<MODE>(a, hs, hv, sy, sp, false);
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k) if ((hv[k] >> lane) & 1u) hit[k] |= hs->hits(k * WAVE + lane);
         }
         wave_lds_sync();
-        const uint32_t hq = or16_in_quarter(hit);
-        if (vs && ((hq >> i) & 1u)) {
-            const int64_t row = (int64_t)R * BS + i;
-            if constexpr (valued<MODE>()) {
-                const float v = sy[lane];
-                if (single) a.yacc[row] = (double)v;
-                else atomicAdd(&a.yacc[row], (double)v);
+        uint32_t hq[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) hq[k] = or16_in_quarter(hit[k]);
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            const int32_t R = (int32_t)seg_brow(s[k]);
+            const float *my = sy + k * WAVE;
+            bool carry = false;
+            if (k + 1 < SLOTS) carry = vs[k] && vs[k + 1] && (int32_t)seg_brow(s[k + 1]) == R;
+            if (carry) {
+                // the next slot continues this block row: fold the partial sums into it
+                if constexpr (valued<MODE>()) sy[(k + 1) * WAVE + lane] += my[lane];
+                if constexpr (MODE == M_BFS) sp[(k + 1) * WAVE + lane] = min(sp[(k + 1) * WAVE + lane], sp[k * WAVE + lane]);
+                if (k + 1 < SLOTS) hq[k + 1] |= hq[k];
+            } else if (vs[k]) {
+                if ((hq[k] >> i) & 1u) {
+                    const int64_t row = (int64_t)R * BS + i;
+                    const bool single = seg_single(s[k]);
+                    if constexpr (valued<MODE>()) {
+                        const float v = my[lane];
+                        if (single) a.yacc[row] = (double)v;
+                        else atomicAdd(&a.yacc[row], (double)v);
+                    }
+                    if constexpr (MODE == M_BFS) {
+                        const int32_t p = sp[k * WAVE + lane];
+                        if (single) a.parent[row] = p;
+                        else atomicMin(&a.parent[row], p);
+                    }
+                }
+                if (i == 0 && hq[k]) or_mask16(a.ybits, R, hq[k]);
             }
-            if constexpr (MODE == M_BFS) {
-                const int32_t p = sp[lane];
-                if (single) a.parent[row] = p;
-                else atomicMin(&a.parent[row], p);
-            }
+            if constexpr (valued<MODE>()) sy[k * WAVE + lane] = 0.f;
+            if constexpr (MODE == M_BFS) sp[k * WAVE + lane] = INT_MAX;
         }
-        if (vs && i == 0 && hq) or_mask16(a.ybits, R, hq);
-        if constexpr (valued<MODE>()) sy[lane] = 0.f;
-        if constexpr (MODE == M_BFS) sp[lane] = INT_MAX;
         wave_lds_sync();
     }
+}
+
+// For each of SLOTS wave-uniform targets, the largest a in [0, n) with
+// arr[a] <= target (arr increasing, arr[0] = 0 <= target): a 64-ary search in
+// which the whole wave probes 64 positions per round (log64 n rounds), the
+// SLOTS searches interleaved so that their loads overlap.
+__device__ __forceinline__ void wave_search(const int32_t *__restrict__ arr, int32_t n,
+                                            const int32_t (&target)[SLOTS], const bool (&valid)[SLOTS],
+                                            int32_t (&res)[SLOTS])
+{
+    const int lane = lane_id();
+    int32_t lo[SLOTS], hi[SLOTS];
+#pragma unroll
+    for (int k = 0; k < SLOTS; ++k) {
+        lo[k] = 0;
+        hi[k] = valid[k] ? n : 1;  // an unused slot needs no search
+    }
+    for (;;) {
+        bool more = false;
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) more |= hi[k] - lo[k] > 1;
+        if (!more) break;
+        int32_t v[SLOTS], step[SLOTS], pi[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            step[k] = (hi[k] - lo[k] + WAVE - 1) / WAVE;
+            pi[k] = lo[k] + lane * step[k];
+            v[k] = (hi[k] - lo[k] > 1 && pi[k] < hi[k]) ? arr[pi[k]] : INT_MAX;
+        }
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            if (hi[k] - lo[k] <= 1) continue;
+            const uint64_t m = ballot(v[k] <= target[k]);  // lane 0 probes lo: always set
+            const int L = 63 - __builtin_clzll(m);
+            lo[k] += L * step[k];
+            hi[k] = min(hi[k], lo[k] + step[k]);
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < SLOTS; ++k) res[k] = lo[k];
 }
 
 // Push (Sec. 3.3.2): block tasks flattened over the block-CSC lists of the
-// active column blocks, 64 tasks per wave, grid-stride.
+// active column blocks; chunks of 64 consecutive tasks, one task per lane,
+// up to SLOTS chunks per wave iteration, grid-stride.  The chunk's first
+// work item comes from a wave search over the item starts; a lane then finds
+// its own item by a 6-step binary search over the next 64 item starts, held
+// one per lane and read by shuffles.
 template <int MODE>
-__device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp)
+__device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage *hs)
 {
     const int lane = lane_id();
     const int32_t T = a.counters[C_TASKS];
-    const int32_t N = a.counters[C_NZBLK];
-    const int64_t units = ((int64_t)T + WAVE - 1) / WAVE;
-    for (int64_t u = gw; u < units; u += nw) {
-        const int64_t t = u * WAVE + lane;
-        const bool vt = t < T;
-        int32_t J = 0, R = 0, b = 0;
-        uint32_t mx = 0, am = 0;
-        uint64_t d = 0;
-        if (vt) {
-            // largest a with task_off[a] <= t
-            int32_t lo = 0, hi = N - 1;
-            while (lo < hi) {
-                int32_t mid = (lo + hi + 1) >> 1;
-                if (a.task_off[mid] <= t) lo = mid;
-                else hi = mid - 1;
-            }
-            J = a.act[lo];
-            const int32_t p = a.cb_ptr[J] + (int32_t)(t - a.task_off[lo]);
-            R = a.csc_row[p];
-            b = a.csc2csr[p];
-            mx = mask16(a.xmask, J);
-            am = row_admit<MODE>(a, R);
+    const int32_t NT = a.counters[C_NTB];
+    const int64_t nchunks = ((int64_t)T + WAVE - 1) / WAVE;
+    const int cpw = nchunks >= (int64_t)nw * SLOTS * 2 ? SLOTS : 1;
+    for (int64_t u = gw; u * cpw < nchunks; u += nw) {
+        int32_t t[SLOTS], a0[SLOTS], B[SLOTS], tgt[SLOTS];
+        bool vt[SLOTS], vc[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            const int64_t c = u * cpw + k;
+            vc[k] = k < cpw && c < nchunks;
+            t[k] = (int32_t)(c * WAVE + lane);
+            vt[k] = vc[k] && t[k] < T;
+            tgt[k] = vc[k] ? (int32_t)(c * WAVE) : 0;
         }
-        const bool act = vt && am != 0;
-        if (act) d = a.desc[b];
-        const uint32_t type = desc_type(d);
-        uint32_t hit = 0;
-        if (act && type == T_COO)
-            hit = coo_block_push<MODE>(a.pay, a.vb, d, J, R, mx, am, a.xd, a.yacc, a.parent);
-        uint64_t hv = ballot(act && type != T_COO);
-        while (hv) {
-            const int L = ctz64(hv);
-            hv &= hv - 1;
-            const uint64_t dL = readlane_u64(d, L);
-            const int32_t JL = (int32_t)readlane_u32((uint32_t)J, L);
-            const int32_t RL = (int32_t)readlane_u32((uint32_t)R, L);
-            const uint32_t mxL = readlane_u32(mx, L), amL = readlane_u32(am, L);
-            uint32_t h = heavy_block<MODE>(a.pay, dL, JL, mxL, amL, a.xd, sy, sp);
-            wave_lds_sync();
-            if (lane < 16) {
-                const int64_t row = (int64_t)RL * BS + lane;
-                if ((h >> lane) & 1u) {
-                    if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], (double)sy[lane]);
-                    if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], sp[lane]);
-                }
-                if constexpr (valued<MODE>()) sy[lane] = 0.f;
-                if constexpr (MODE == M_BFS) sp[lane] = INT_MAX;
-            }
-            wave_lds_sync();
-            if (lane == L) hit |= h;
+        wave_search(a.task_off, NT, tgt, vc, a0);
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            const int32_t w = a0[k] + 1 + lane;
+            B[k] = (vc[k] && w <= NT) ? a.task_off[w] : INT_MAX;
         }
-        if (act && hit) or_mask16(a.ybits, R, hit);
+        int32_t it[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            int lo = 0;
+#pragma unroll
+            for (int st = 32; st > 0; st >>= 1) {
+                const int32_t v = __shfl(B[k], lo + st - 1, WAVE);
+                if (v <= t[k]) lo += st;
+            }
+            it[k] = a0[k] + lo;
+        }
+        int32_t J[SLOTS], p[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            J[k] = vt[k] ? a.act[it[k]] : 0;
+            p[k] = vt[k] ? a.pbase[it[k]] + t[k] : 0;
+        }
+        int32_t R[SLOTS], bb[SLOTS];
+        uint32_t mx[SLOTS], am[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            R[k] = vt[k] ? a.csc_row[p[k]] : 0;
+            bb[k] = vt[k] ? a.csc2csr[p[k]] : 0;
+            mx[k] = vt[k] ? mask16(a.xmask, J[k]) : 0u;
+        }
+        bool act[SLOTS];
+        uint64_t d[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            am[k] = vt[k] ? row_admit(a, R[k]) : 0u;
+            act[k] = vt[k] && am[k] != 0;
+            d[k] = act[k] ? a.desc[bb[k]] : 0ull;
+        }
+        uint32_t hit[SLOTS];
+        uint64_t hv[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            hit[k] = 0;
+            const bool lanework = act[k] && lane_coo(d[k]);
+            if (lanework)
+                hit[k] = coo_block_push<MODE>(a.pay, a.vb, d[k], J[k], R[k], mx[k], am[k], a.xd, a.yacc,
+                                              a.parent);
+            const bool wavework = act[k] && !lanework;
+            hv[k] = ballot(wavework);
+            if (wavework) hs->stage(k * WAVE + lane, d[k], J[k], mx[k], am[k], R[k]);
+        }
+        if (hv[0] | hv[1] | hv[2] | hv[3]) {
+            wave_lds_sync();
+            run_staged<MODE>(a, hs, hv, sy, sp, true);
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k) if ((hv[k] >> lane) & 1u) hit[k] |= hs->hits(k * WAVE + lane);
+            wave_lds_sync();
+        }
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k)
+            if (act[k] && hit[k]) or_mask16(a.ybits, R[k], hit[k]);
     }
 }
 
-template <int MODE>
-__global__ __launch_bounds__(TPB) void k_main(MainArgs a)
+// LDS of one wave: per-slot row accumulators and the staged whole-wave blocks.
+struct WaveLds {
+    float sy[SLOTS * WAVE];
+    int32_t sp[SLOTS * WAVE];
+    HeavyStage hs;
+};
+
+// The traversal kernels (one per path).  Both are launched for an automatic
+// path choice; each reads the choice the scan made on the device and the
+// other one returns at once.
+template <int MODE, int PATH>
+__global__ __launch_bounds__(TPB) void k_traverse(MainArgs a)
 {
-    __shared__ float s_y[TPB / WAVE][WAVE];
-    __shared__ int32_t s_p[TPB / WAVE][WAVE];
+    __shared__ WaveLds lds[TPB / WAVE];
+    // BFS: the host has read the frontier size of this level; restart the count
     if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
-    if (a.counters[C_NZBLK] == 0) return;
+    const int32_t N = a.counters[C_NZBLK];
+    if (N == 0 || a.counters[C_PATH] != PATH) return;
     const int w = threadIdx.x >> 6, lane = lane_id();
-    float *sy = s_y[w];
-    int32_t *sp = s_p[w];
-    sy[lane] = 0.f;
-    sp[lane] = INT_MAX;
+    WaveLds &L = lds[w];
+#pragma unroll
+    for (int k = 0; k < SLOTS; ++k) {
+        L.sy[k * WAVE + lane] = 0.f;
+        L.sp[k * WAVE + lane] = INT_MAX;
+    }
     wave_lds_sync();
     const int gw = blockIdx.x * (TPB / WAVE) + w, nw = gridDim.x * (TPB / WAVE);
-    if (a.counters[C_PATH] == PATH_PUSH) push_loop<MODE>(a, gw, nw, sy, sp);
-    else pull_loop<MODE>(a, gw, nw, sy, sp);
+    if constexpr (PATH == PATH_PUSH) {
+        push_loop<MODE>(a, gw, nw, L.sy, L.sp, &L.hs);
+    } else {
+        // with a quarter or more of the vector blocks active, most visited blocks
+        // are used: load their descriptors together with their block columns
+        const bool spec = (int64_t)N * 4 >= (int64_t)a.nbc;
+        pull_loop<MODE>(a, gw, nw, L.sy, L.sp, &L.hs, spec);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -688,7 +977,8 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
                                                   int32_t *__restrict__ counters, uint64_t *status,
                                                   uint64_t *next_status, int32_t n_status,
                                                   uint32_t *__restrict__ xmask,
-                                                  const int32_t *__restrict__ act)
+                                                  const int32_t *__restrict__ x_idx, int32_t k,
+                                                  int32_t n)
 {
     __shared__ uint64_t lds4[TPB / WAVE];
     __shared__ uint64_t s_prefix;
@@ -696,10 +986,11 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
     __shared__ uint32_t s_wpos[FIN_WORDS];
     for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < n_status; i += gridDim.x * TPB)
         next_status[i] = 0;
-    // clear blk_x_mask of this call's active vector blocks
-    const int32_t N = counters[C_NZBLK];
-    for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < N; i += gridDim.x * TPB)
-        xmask[act[i] >> 1] = 0u;
+    // clear the blk_x_mask words this call's x indices touched
+    for (int32_t t = blockIdx.x * TPB + threadIdx.x; t < k; t += gridDim.x * TPB) {
+        const int32_t j = x_idx[t];
+        if (j >= 0 && j < n) xmask[j >> 5] = 0u;
+    }
     const int tile = blockIdx.x;
     const int32_t w = tile * FIN_WORDS + threadIdx.x;
     const uint32_t word = w < nywords ? ybits[w] : 0u;
@@ -782,7 +1073,8 @@ __global__ __launch_bounds__(TPB) void k_bfs_init(int32_t n, int32_t source, int
                                                   int32_t *__restrict__ parent,
                                                   uint32_t *__restrict__ visited,
                                                   uint32_t *__restrict__ nextm,
-                                                  uint32_t *__restrict__ xmask, int32_t nwords)
+                                                  uint32_t *__restrict__ xmask, int32_t nwords,
+                                                  int32_t *__restrict__ counters)
 {
     const int64_t stride = (int64_t)gridDim.x * TPB;
     for (int64_t v = (int64_t)blockIdx.x * TPB + threadIdx.x; v < n; v += stride) {
@@ -791,6 +1083,7 @@ __global__ __launch_bounds__(TPB) void k_bfs_init(int32_t n, int32_t source, int
     }
     const int32_t sw = source >> 5;
     const uint32_t sb = 1u << (source & 31);
+    if (blockIdx.x == 0 && threadIdx.x == 0) counters[C_NZACC] = 1;  // the source's vector block
     for (int64_t w = (int64_t)blockIdx.x * TPB + threadIdx.x; w < nwords; w += stride) {
         visited[w] = w == sw ? sb : 0u;
         xmask[w] = w == sw ? sb : 0u;
@@ -808,7 +1101,7 @@ __global__ __launch_bounds__(TPB) void k_bfs_update(int32_t nwords, int32_t next
                                                     int32_t *__restrict__ counters)
 {
     int32_t w = blockIdx.x * TPB + threadIdx.x;
-    uint32_t cnt = 0;
+    uint32_t cnt = 0, blocks = 0;
     if (w < nwords) {
         uint32_t nm = nextm[w];
         xmask[w] = nm;
@@ -816,6 +1109,7 @@ __global__ __launch_bounds__(TPB) void k_bfs_update(int32_t nwords, int32_t next
             visited[w] |= nm;
             nextm[w] = 0u;
             cnt = __popc(nm);
+            blocks = ((nm & 0xFFFFu) != 0) + ((nm >> 16) != 0);
             while (nm) {
                 int b = ctz32(nm);
                 nm &= nm - 1;
@@ -823,8 +1117,11 @@ __global__ __launch_bounds__(TPB) void k_bfs_update(int32_t nwords, int32_t next
             }
         }
     }
-    uint32_t tot = wave_sum(cnt);
-    if (lane_id() == 0 && tot) atomicAdd(&counters[C_FRONTIER], (int32_t)tot);
+    const uint32_t tot = wave_sum(cnt), totb = wave_sum(blocks);
+    if (lane_id() == 0 && tot) {
+        atomicAdd(&counters[C_FRONTIER], (int32_t)tot);
+        atomicAdd(&counters[C_NZACC], (int32_t)totb);
+    }
 }
 
 __global__ __launch_bounds__(TPB) void k_bfs_finish(int32_t n, int32_t *__restrict__ parent)
@@ -845,12 +1142,45 @@ static inline int grid_for(int64_t items, int per_block, int cap)
     return (int)g;
 }
 
-int main_grid(const DevMatrix &A)
+// Resident workgroups of a traversal kernel on the whole device (compute
+// units x workgroups per compute unit at its register and LDS use), so that
+// the persistent grid is exactly one round of residency.
+template <int MODE, int PATH>
+static int resident_grid()
 {
-    int64_t pull_waves = (A.nseg + 3) / 4;
-    int64_t push_waves = (A.nblk + WAVE - 1) / WAVE;
-    int64_t waves = pull_waves > push_waves ? pull_waves : push_waves;
-    return grid_for(waves, TPB / WAVE, MAX_MAIN_GRID);
+    static int cached = 0;
+    if (!cached) {
+        int dev = 0, cus = 0, per_cu = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_traverse<MODE, PATH>, TPB, 0) != hipSuccess ||
+            cus <= 0 || per_cu <= 0) {
+            cached = MAX_MAIN_GRID;
+        } else {
+            cached = cus * per_cu;
+        }
+    }
+    return cached;
+}
+
+template <int MODE, int PATH>
+static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStream_t s)
+{
+    const int64_t waves = PATH == PATH_PULL ? (A.nseg + 3) / 4 : (A.nblk + WAVE - 1) / WAVE;
+    int g = grid_for(waves, TPB / WAVE, MAX_MAIN_GRID);
+    const int cap = resident_grid<MODE, PATH>();
+    if (g > cap) g = cap;
+    hipLaunchKernelGGL((k_traverse<MODE, PATH>), dim3(g), dim3(TPB), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int MODE>
+static hipError_t launch_paths(const DevMatrix &A, const MainArgs &a, int forced, hipStream_t s)
+{
+    hipError_t e = hipSuccess;
+    if (forced != PATH_PULL) e = launch_traverse<MODE, PATH_PUSH>(A, a, s);
+    if (e == hipSuccess && forced != PATH_PUSH) e = launch_traverse<MODE, PATH_PULL>(A, a, s);
+    return e;
 }
 
 hipError_t launch_scatter(const DevMatrix &A, const DevCtx &C, int mode, int32_t k,
@@ -871,8 +1201,8 @@ hipError_t launch_ballot(const DevMatrix &A, const DevCtx &C, int mode, const vo
 {
     int64_t lanes = ((int64_t)A.n + WAVE - 1) / WAVE * WAVE;
     dim3 g(grid_for(lanes, TPB, INT_MAX)), b(TPB);
-    if (mode == M_F16) hipLaunchKernelGGL(k_ballot<M_F16>, g, b, 0, s, x_dense, A.n, C.xd, C.xmask, C.nxwords);
-    else hipLaunchKernelGGL(k_ballot<M_F32>, g, b, 0, s, x_dense, A.n, C.xd, C.xmask, C.nxwords);
+    if (mode == M_F16) hipLaunchKernelGGL(k_ballot<M_F16>, g, b, 0, s, x_dense, A.n, C.xd, C.xmask, C.nxwords, C.counters);
+    else hipLaunchKernelGGL(k_ballot<M_F32>, g, b, 0, s, x_dense, A.n, C.xd, C.xmask, C.nxwords, C.counters);
     return hipGetLastError();
 }
 
@@ -880,22 +1210,23 @@ hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th
 {
     dim3 g(grid_for(A.nbc, SCAN_TILE, INT_MAX)), b(TPB);
     const int p = C.scan_parity;
-    hipLaunchKernelGGL(k_scan, g, b, 0, s, C.xmask, A.cb_ptr, A.nbc, C.act, C.task_off, C.counters,
-                       C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3);
+    hipLaunchKernelGGL(k_scan, g, b, 0, s, C.xmask, A.cb_ptr, A.nbc, C.act, C.task_off, C.pbase,
+                       C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) C.scan_parity = 1 - p;
     return e;
 }
 
 hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
-                       const uint32_t *omask, int complement, int32_t *parent, hipStream_t s)
+                       const uint32_t *omask, int complement, int32_t *parent, int forced_path,
+                       hipStream_t s)
 {
     MainArgs a;
     a.cb_col = A.cb_col;
     a.desc = A.desc;
     a.pay = A.pay;
     a.vb = A.dtype == 0 ? 4u : (A.dtype == 1 ? 2u : 0u);
-    a.cb_ptr = A.cb_ptr;
+    a.nbc = A.nbc;
     a.csc_row = A.csc_row;
     a.csc2csr = A.csc2csr;
     a.seg = A.seg;
@@ -904,24 +1235,23 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
     a.xmask = C.xmask;
     a.act = C.act;
     a.task_off = C.task_off;
+    a.pbase = C.pbase;
     a.counters = C.counters;
     a.omask = omask;
     a.complement = complement;
     a.yacc = C.yacc;
     a.ybits = mode == M_BFS ? C.nextm : C.ybits;
     a.parent = parent;
-    dim3 g(main_grid(A)), b(TPB);
     switch (mode) {
-    case M_F32: hipLaunchKernelGGL(k_main<M_F32>, g, b, 0, s, a); break;
-    case M_F16: hipLaunchKernelGGL(k_main<M_F16>, g, b, 0, s, a); break;
-    case M_BOOL: hipLaunchKernelGGL(k_main<M_BOOL>, g, b, 0, s, a); break;
-    default: hipLaunchKernelGGL(k_main<M_BFS>, g, b, 0, s, a); break;
+    case M_F32: return launch_paths<M_F32>(A, a, forced_path, s);
+    case M_F16: return launch_paths<M_F16>(A, a, forced_path, s);
+    case M_BOOL: return launch_paths<M_BOOL>(A, a, forced_path, s);
+    default: return launch_paths<M_BFS>(A, a, forced_path, s);
     }
-    return hipGetLastError();
 }
 
 hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_idx, void *y_val,
-                           int32_t *y_nnz, hipStream_t s)
+                           int32_t *y_nnz, const int32_t *x_idx, int32_t k, hipStream_t s)
 {
     int32_t nyw = (A.nbr + 1) / 2;
     dim3 g(grid_for(nyw, FIN_WORDS, INT_MAX)), b(TPB);
@@ -929,9 +1259,9 @@ hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_i
     uint64_t *st = C.st_fin[p], *nx = C.st_fin[1 - p];
     const int32_t ns = C.n_st_fin;
     switch (mode) {
-    case M_F32: hipLaunchKernelGGL(k_finalize<M_F32>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, C.act); break;
-    case M_F16: hipLaunchKernelGGL(k_finalize<M_F16>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, C.act); break;
-    default: hipLaunchKernelGGL(k_finalize<M_BOOL>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, C.act); break;
+    case M_F32: hipLaunchKernelGGL(k_finalize<M_F32>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, x_idx, k, A.n); break;
+    case M_F16: hipLaunchKernelGGL(k_finalize<M_F16>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, x_idx, k, A.n); break;
+    default: hipLaunchKernelGGL(k_finalize<M_BOOL>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, x_idx, k, A.n); break;
     }
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) C.fin_parity = 1 - p;
@@ -956,7 +1286,8 @@ hipError_t launch_bfs_init(const DevMatrix &A, const DevCtx &C, int32_t source, 
 {
     int32_t nwords = (A.nbr + 1) / 2;
     dim3 g(grid_for(A.n, TPB, 4096)), b(TPB);
-    hipLaunchKernelGGL(k_bfs_init, g, b, 0, s, A.n, source, level, parent, C.visited, C.nextm, C.xmask, nwords);
+    hipLaunchKernelGGL(k_bfs_init, g, b, 0, s, A.n, source, level, parent, C.visited, C.nextm, C.xmask, nwords,
+                       C.counters);
     return hipGetLastError();
 }
 

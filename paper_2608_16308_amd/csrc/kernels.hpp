@@ -26,7 +26,9 @@ enum Counter : int {
     C_ERR = 4,       // error bits raised by the blocker during this call
     C_ERR_LAST = 5,  // error bits of the last completed call
     C_FRONTIER = 6,  // BFS: vertices in the next frontier
-    C_COUNT = 8
+    C_NZACC = 7,     // nonzero vector blocks counted by the blocker (consumed by the scan)
+    C_NTB = 8,       // push work items (nonzero vector blocks with a nonempty block column)
+    C_COUNT = 12
 };
 constexpr int PATH_PUSH = 1, PATH_PULL = 2;
 
@@ -37,8 +39,9 @@ struct DevCtx {
     void *xd = nullptr;           // dense x values, 16 * nbc entries (fp32 or fp16)
     uint32_t *xmask = nullptr;    // blk_x_mask, two 16-bit masks per word
     int32_t nxwords = 0;
-    int32_t *act = nullptr;       // active vector blocks, ascending (nbc)
-    int32_t *task_off = nullptr;  // exclusive scan of their block-CSC lengths (nbc + 1)
+    int32_t *act = nullptr;       // push work items: active vector blocks with blocks, ascending (nbc)
+    int32_t *task_off = nullptr;  // their first task (exclusive scan of block-CSC lengths) (nbc + 1)
+    int32_t *pbase = nullptr;     // block-CSC position of task t of item a = pbase[a] + t (nbc)
     double *yacc = nullptr;       // y accumulators (16 * nbr)
     uint32_t *ybits = nullptr;    // y structure, two 16-bit row-block masks per word
     int32_t nywords = 0;
@@ -63,10 +66,14 @@ hipError_t launch_ballot(const DevMatrix &A, const DevCtx &C, int mode, const vo
                          hipStream_t s);
 hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th3,
                        hipStream_t s);
+// Launches the traversal: the push and the pull kernel for an automatic path
+// (each returns at once unless the scan chose it), or only the forced one.
 hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
-                       const uint32_t *omask, int complement, int32_t *parent, hipStream_t s);
+                       const uint32_t *omask, int complement, int32_t *parent, int forced_path,
+                       hipStream_t s);
 hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_idx,
-                           void *y_val, int32_t *y_nnz, hipStream_t s);
+                           void *y_val, int32_t *y_nnz, const int32_t *x_idx, int32_t k,
+                           hipStream_t s);
 hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, void *y,
                                  float *y32, hipStream_t s);
 hipError_t launch_bfs_init(const DevMatrix &A, const DevCtx &C, int32_t source, int32_t *level,
@@ -75,6 +82,5 @@ hipError_t launch_bfs_update(const DevMatrix &A, const DevCtx &C, int32_t next_l
                              int32_t *level, hipStream_t s);
 hipError_t launch_bfs_finish(const DevMatrix &A, int32_t *parent, hipStream_t s);
 
-int main_grid(const DevMatrix &A);
 
 }  // namespace dbs

@@ -17,6 +17,14 @@ def desc_fields(d):
     return d >> 16, ((d >> 8) & 0xFF) + 1, d & 7
 
 
+def desc_inline(d):
+    return (int(d) >> 3) & 1 == 1
+
+
+def inline_capacity(vb):
+    return 48 // (8 + 8 * vb)
+
+
 def seg_fields(s):
     s = int(s)
     return s & 0xFFFFFFFF, (s >> 32) & 0x7FFFFFF, ((s >> 59) & 0xF) + 1, (s >> 63) & 1
@@ -37,6 +45,19 @@ def decode_block(pay, d, vb):
     """Returns a list of (local row, local col, value or None) in row-major order."""
     off, nnz, t = desc_fields(d)
     out = []
+    if desc_inline(d):
+        assert t == COO and nnz <= inline_capacity(vb)
+        d = int(d)
+        for e in range(nnz):
+            sh = 16 + e * (8 + 8 * vb)
+            cd = (d >> sh) & 0xFF
+            v = None
+            if vb == 4:
+                v = np.uint32((d >> (sh + 8)) & 0xFFFFFFFF).view(np.float32)
+            elif vb == 2:
+                v = np.uint16((d >> (sh + 8)) & 0xFFFF)
+            out.append((cd >> 4, cd & 15, v))
+        return out
     if t == COO:
         vals = _vals(pay, off, nnz, vb)
         for k in range(nnz):

@@ -124,11 +124,26 @@ def test_crafted_covers_every_format_and_boundary():
 
 @pytest.mark.parametrize("force", [0, 1, 2, 3, 4])
 @pytest.mark.parametrize("dtype", [np.float32, np.float16, None])
-def test_forced_formats_roundtrip(force, dtype):
+@pytest.mark.parametrize("inline", [1, 0])
+def test_forced_formats_roundtrip(force, dtype, inline):
     a = wl.crafted(dtype, key=3)
-    opts = dbs.default_opts(force_type=force)
+    opts = dbs.default_opts(force_type=force, inline_small=inline)
     hm, info, arrs = _check_roundtrip(a, opts)
     assert info["blocks_by_type"][_lib.BLOCK_TYPE_NAMES[force]] == info["nblk"]
+    n_inline = sum(dbf.desc_inline(d) for d in arrs["desc"])
+    if not inline or force != 0:
+        assert n_inline == 0
+    else:
+        cap = dbf.inline_capacity(_vb(a.vals))
+        small = sum(dbf.desc_fields(d)[1] <= cap for d in arrs["desc"])
+        assert n_inline == small > 0
+
+
+def test_inline_blocks_take_no_payload():
+    a = wl.random_csr(300, 300, 0.004, key=(1, 9))  # almost only 1-entry blocks
+    on = dbs.HostMatrix.from_csr(a.m, a.n, a.row_ptr, a.col_idx, a.vals).info()
+    off = dbs.HostMatrix.from_csr(a.m, a.n, a.row_ptr, a.col_idx, a.vals, dbs.default_opts(inline_small=0)).info()
+    assert on["payload_bytes"] < off["payload_bytes"]
 
 
 @pytest.mark.parametrize("seg_close", [1, 4, 16, 64])

@@ -73,15 +73,15 @@ def test_crafted_all_formats(torch, dtype):
                              label=label)
 
 
-@pytest.mark.parametrize("force", [0, 1, 2, 3, 4])
-def test_forced_single_format(torch, force):
+@pytest.mark.parametrize("force,inline", [(0, 1), (0, 0), (1, 1), (2, 1), (3, 1), (4, 1)])
+def test_forced_single_format(torch, force, inline):
     a = wl.crafted(np.float32, key=12)
-    A = gpu_matrix(a, dbs.default_opts(force_type=force))
+    A = gpu_matrix(a, dbs.default_opts(force_type=force, inline_small=inline))
     om = oracle_matrix(a)
     ctx = dbs.Context(A)
     for kind, (xi, xv) in x_kinds(a.n, 2).items():
         for p in ("push", "pull"):
-            label = f"force_type={force} x={kind} path={p}"
+            label = f"force_type={force} inline={inline} x={kind} path={p}"
             log(label)
             check_spmspv(ctx, A, om, a, xi, xv, path=p, label=label)
 
