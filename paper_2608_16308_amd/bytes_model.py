@@ -11,13 +11,14 @@ distinct element once per kernel that needs it:
   scan      2 B mask per vector block, and per active vector block 8 B of
             block-CSC pointers read + 8 B (list entry, task offset) written
   push      per active vector block 8 B list entry + task offset; per
-            visited block 4 B csc_row + 4 B csc2csr + 8 B descriptor +
+            visited block 4 B csc_row + 4 B slot + 8 B descriptor +
             the record bytes its microkernel reads; 8 B per (block, row) fp64
             accumulator update; 4 B structure-mask update per block with hits
-  pull      8 B per segment + 4 B cb_col + 2 B x-mask per scanned block;
-            per block with an active vector block 8 B descriptor + record
-            bytes; 8 B per (segment, row) accumulator write; 4 B mask update
-            per segment with hits
+  pull      4 B per segment + 4 B block column per segment slot (16 per
+            segment, padding included) + 2 B x-mask per scanned block; per
+            block with an active vector block 8 B descriptor + record bytes;
+            8 B per (segment, row) accumulator write; 4 B mask update per
+            segment with hits
   x values  V bytes per nonzero of x (read once from the dense x)
   finalize  2 B structure mask per block row; per y entry 8 B accumulator
             read + 8 B reset + 4 B index + V value written; 4 B mask reset
@@ -113,7 +114,8 @@ class BytesModel:
         if path == "push":
             main = 16 * N + nact_blocks * (4 + 4 + 8) + rec_bytes + 8 * blk_rows + 4 * blks_hit
         else:
-            main = 8 * self.nseg + 6 * self.nblk + 8 * nact_blocks + rec_bytes + 8 * seg_rows + 4 * segs_hit
+            main = 4 * self.nseg + 64 * self.nseg + 2 * self.nblk + 8 * nact_blocks + rec_bytes \
+                + 8 * seg_rows + 4 * segs_hit
         main += V * k
         finalize = 2 * self.nbr + y_nnz * (8 + 8 + 4 + V) + 4 * N
         total = blocker + scan + main + finalize

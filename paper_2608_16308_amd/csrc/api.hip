@@ -186,14 +186,44 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
     d.nblk = h->nblk;
     d.nseg = h->nseg;
     d.dtype = h->dtype;
+    // primary order -> pull-segment slots (see DevMatrix)
+    std::vector<int32_t> sl_col, csc_slot;
+    std::vector<uint64_t> sl_desc;
+    std::vector<uint32_t> seg_rs;
+    try {
+        const size_t nslots = (size_t)16 * (size_t)h->nseg;
+        sl_col.assign(nslots, -1);
+        sl_desc.assign(nslots, 0ull);
+        seg_rs.resize((size_t)h->nseg);
+        std::vector<int32_t> slot_of((size_t)h->nblk);
+        for (int64_t s = 0; s < h->nseg; ++s) {
+            const uint64_t sg = h->seg[s];
+            seg_rs[s] = seg_brow(sg) | (seg_single(sg) ? 0x80000000u : 0u);
+            const uint32_t first = seg_first(sg), nb = seg_nb(sg);
+            for (uint32_t i = 0; i < nb; ++i) {
+                const size_t slot = (size_t)16 * s + i;
+                sl_col[slot] = h->cb_col[first + i];
+                sl_desc[slot] = h->desc[first + i];
+                slot_of[first + i] = (int32_t)slot;
+            }
+        }
+        csc_slot.resize((size_t)h->nblk);
+        for (int64_t q = 0; q < h->nblk; ++q) csc_slot[q] = slot_of[h->csc2csr[q]];
+    } catch (const std::bad_alloc &) {
+        delete A;
+        return dbs_fail(DBS_ERR_ALLOC, "host allocation failed during upload");
+    }
+    if ((int64_t)16 * h->nseg >= ((int64_t)1 << 31)) {
+        delete A;
+        return dbs_fail(DBS_ERR_UNSUPPORTED, "%lld pull segments exceed the 2^31 slot limit", (long long)h->nseg);
+    }
     dbs_status s2 = DBS_OK;
-    if ((s2 = dev_upload(A->allocs, h->rb_ptr, &d.rb_ptr)) != DBS_OK ||
-        (s2 = dev_upload(A->allocs, h->cb_col, &d.cb_col)) != DBS_OK ||
+    if ((s2 = dev_upload(A->allocs, sl_col, &d.sl_col)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, sl_desc, &d.sl_desc)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, seg_rs, &d.seg_rs)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->cb_ptr, &d.cb_ptr)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->csc_row, &d.csc_row)) != DBS_OK ||
-        (s2 = dev_upload(A->allocs, h->csc2csr, &d.csc2csr)) != DBS_OK ||
-        (s2 = dev_upload(A->allocs, h->desc, &d.desc)) != DBS_OK ||
-        (s2 = dev_upload(A->allocs, h->seg, &d.seg)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, csc_slot, &d.csc_slot)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->payload, &d.pay)) != DBS_OK) {
         free_all(A->allocs);
         delete A;
@@ -260,6 +290,7 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
     float *xd = nullptr;
     if ((st = dev_zeros(ctx->allocs, (size_t)16 * nb, &xd)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &xmask)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)(nb + 31) / 32 + 64, &c.xbits)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)nbc + 1, &c.act)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)nbc + 2, &c.task_off)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)nbc + 1, &c.pbase)) != DBS_OK ||

@@ -208,6 +208,7 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
                                               const int32_t *__restrict__ cb_ptr, int32_t nbc,
                                               int32_t *__restrict__ act, int32_t *__restrict__ task_off,
                                               int32_t *__restrict__ pbase,
+                                              uint32_t *__restrict__ xbits,
                                               int32_t *__restrict__ counters, uint64_t *status,
                                               uint64_t *next_status, int32_t n_status,
                                               int32_t forced_path, double th3)
@@ -222,13 +223,24 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
     int32_t start[SCAN_ITEMS];
     uint32_t len[SCAN_ITEMS];
     uint64_t mine = 0;
+    uint32_t nib = 0;  // activity of this thread's 4 vector blocks
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
         const int32_t J = base + k;
         const uint32_t am = J < nbc ? mask16(xmask, J) : 0u;
+        nib |= (am ? 1u : 0u) << k;
         start[k] = am ? cb_ptr[J] : 0;
         len[k] = am ? (uint32_t)(cb_ptr[J + 1] - start[k]) : 0u;
         if (len[k]) mine += (1ull << 34) + len[k];
+    }
+    // one activity bit per vector block: 8 threads x 4 blocks form a word
+    {
+        uint32_t word = nib << (4 * (lane_id() & 7));
+        word |= __shfl_xor(word, 1, WAVE);
+        word |= __shfl_xor(word, 2, WAVE);
+        word |= __shfl_xor(word, 4, WAVE);
+        const int32_t wi = base >> 5;
+        if ((lane_id() & 7) == 0 && base < nbc) xbits[wi] = word;
     }
     uint64_t total;
     uint64_t excl = block_exclusive_scan(mine, &total, lds4);
@@ -282,7 +294,7 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
 // held inline, else with at most three aligned dword loads covering the
 // record's coordinate bytes (the payload is padded to 16 bytes, so the last
 // covering dword is inside it).
-__device__ __forceinline__ uint64_t coo_coords(uint64_t d, const uint8_t *rec, uint32_t vb, uint32_t nnz)
+__device__ __forceinline__ uint64_t coo_coords(uint64_t d, const uint8_t *pay, uint32_t vb, uint32_t nnz)
 {
     if (desc_inline(d)) {
         if (nnz == 1) return (d >> 16) & 0xFFull;  // the common hypersparse case
@@ -290,9 +302,12 @@ __device__ __forceinline__ uint64_t coo_coords(uint64_t d, const uint8_t *rec, u
         for (uint32_t e = 0; e < nnz; ++e) c |= ((d >> inline_shift(e, vb)) & 0xFFull) << (8 * e);
         return c;
     }
-    const uintptr_t a = (uintptr_t)(rec + vb * nnz);  // coordinates follow the values
-    const uint32_t mis = (uint32_t)(a & 3u);
-    const uint32_t *w = (const uint32_t *)(a - mis);
+    // the coordinates follow the values; read them as aligned words of the
+    // (256-byte aligned) payload, indexed from its base so that the loads
+    // stay global loads
+    const uint64_t at = desc_off(d) + (uint64_t)vb * nnz;
+    const uint32_t mis = (uint32_t)(at & 3u);
+    const uint32_t *w = (const uint32_t *)pay + (at >> 2);
     const uint32_t nw = (mis + nnz + 3) / 4;
     const uint32_t w0 = w[0], w1 = nw > 1 ? w[1] : 0u, w2 = nw > 2 ? w[2] : 0u;
     const uint64_t lo = ((uint64_t)w1 << 32) | w0;
@@ -337,8 +352,8 @@ __device__ __forceinline__ uint32_t coo_block(const uint8_t *__restrict__ pay, u
                                               int32_t *pdst16)
 {
     const uint32_t nnz = desc_nnz(d);
-    const uint8_t *rec = desc_inline(d) ? nullptr : pay + desc_off(d);
-    const uint64_t cds = coo_coords(d, rec, vb, nnz);
+    const uint8_t *rec = pay + (desc_inline(d) ? 0 : desc_off(d));
+    const uint64_t cds = coo_coords(d, pay, vb, nnz);
     uint32_t mm = coo_matches(cds, nnz, mx, am);
     uint32_t hit = 0;
     int cur = -1;
@@ -376,8 +391,8 @@ __device__ __forceinline__ uint32_t coo_block_push(const uint8_t *__restrict__ p
                                                    double *yacc, int32_t *parent)
 {
     const uint32_t nnz = desc_nnz(d);
-    const uint8_t *rec = desc_inline(d) ? nullptr : pay + desc_off(d);
-    const uint64_t cds = coo_coords(d, rec, vb, nnz);
+    const uint8_t *rec = pay + (desc_inline(d) ? 0 : desc_off(d));
+    const uint64_t cds = coo_coords(d, pay, vb, nnz);
     uint32_t mm = coo_matches(cds, nnz, mx, am);
     uint32_t hit = 0;
     int cur = -1;
@@ -407,14 +422,12 @@ __device__ __forceinline__ uint32_t coo_block_push(const uint8_t *__restrict__ p
     return hit;
 }
 
-// COO blocks with at most this many entries are processed by one lane;
-// longer ones by the whole wave.
-constexpr uint32_t COO_LANE_MAX = 8;
-static_assert(COO_LANE_MAX <= 8, "coo_coords gathers at most 8 coordinate bytes");
-__device__ __forceinline__ bool lane_coo(uint64_t d)
-{
-    return desc_type(d) == T_COO && desc_nnz(d) <= COO_LANE_MAX;
-}
+// COO blocks whose entries sit in the descriptor are processed by one lane
+// (no payload loads); COO blocks with a payload record are processed
+// entry-parallel by the whole wave (coo_flat); the other formats by the
+// whole wave, one block at a time (heavy_block).
+__device__ __forceinline__ bool lane_coo(uint64_t d) { return desc_inline(d); }
+__device__ __forceinline__ bool flat_coo(uint64_t d) { return !desc_inline(d) && desc_type(d) == T_COO; }
 
 // i-th set bit of v (i >= 0), or -1.
 __device__ __forceinline__ int nth_set_bit(uint32_t v, int i)
@@ -599,17 +612,18 @@ __device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint32_t vb, ui
 // main traversal kernel
 // ---------------------------------------------------------------------------
 struct MainArgs {
-    const int32_t *cb_col;
-    const uint64_t *desc;
+    const int32_t *sl_col;   // pull-segment slots: block column (-1 padding)
+    const uint64_t *sl_desc; // pull-segment slots: descriptor
+    const uint32_t *seg_rs;  // per segment: block row | single-segment flag << 31
     const uint8_t *pay;
     uint32_t vb;            // value bytes of the matrix (4, 2 or 0)
     int32_t nbc;
     const int32_t *csc_row;
-    const int32_t *csc2csr;
-    const uint64_t *seg;
+    const int32_t *csc_slot;
     int64_t nseg;
     const void *xd;
     const uint32_t *xmask;
+    const uint32_t *xbits;       // one activity bit per vector block (global copy)
     const int32_t *act;          // push work items (see k_scan)
     const int32_t *task_off;
     const int32_t *pbase;
@@ -631,20 +645,101 @@ __device__ __forceinline__ uint32_t row_admit(const MainArgs &a, int32_t R)
     return allowed16(a.omask, a.complement, R);
 }
 
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int l)
+{
+    const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, l, WAVE);
+    const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), l, WAVE);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Entry-parallel COO (Sec. 3.3.3's COO microkernel, re-mapped to wave64):
+// the entries of the stored COO blocks owned by the lanes with own set are
+// numbered by a wave prefix sum, and the wave walks them 64 at a time, one
+// entry per lane.  A lane finds the block of its entry by a 6-step binary
+// search over the owners' inclusive prefix sums (read by shuffles) and
+// fetches that block's descriptor, column block and masks from the owner's
+// registers.  The coordinate and value loads of all lanes go out together,
+// then the x gathers.
+//   pull (PUSH false): products are added to the owner's quarter of the
+//   slot's LDS rows (dst + 16 (owner / 16) + row); BFS keeps the smallest
+//   active column per row there.
+//   push (PUSH true): products go straight to the fp64 accumulators of
+//   block row R of the owner.
+// Rows hit are collected per owner in hits (64 words of LDS) and returned to
+// the owner lane.
+template <int MODE, bool PUSH>
+__device__ uint32_t coo_flat(const MainArgs &a, bool own, uint64_t d, int32_t J, uint32_t mx, uint32_t am,
+                             int32_t R, float *dst, int32_t *pdst, uint32_t *hits)
+{
+    const int lane = lane_id();
+    if (!ballot(own)) return 0;
+    const int32_t cnt = own ? (int32_t)desc_nnz(d) : 0;
+    int32_t incl = cnt;
+#pragma unroll
+    for (int o = 1; o < WAVE; o <<= 1) {
+        const int32_t v = __shfl_up(incl, o, WAVE);
+        if (lane >= o) incl += v;
+    }
+    const int32_t E = __shfl(incl, WAVE - 1, WAVE);
+    hits[lane] = 0;
+    wave_lds_sync();
+    const uint32_t vb = a.vb;
+    for (int32_t base = 0; base < E; base += WAVE) {
+        const int32_t g = base + lane;
+        int lo = 0;
+#pragma unroll
+        for (int st = 32; st > 0; st >>= 1) {
+            const int32_t v = __shfl(incl, lo + st - 1, WAVE);
+            if (v <= g) lo += st;
+        }
+        const int L = lo < WAVE ? lo : WAVE - 1;
+        const uint64_t dO = shfl_u64(d, L);
+        const int32_t JO = __shfl(J, L, WAVE);
+        const uint32_t mxam = (uint32_t)__shfl((int)(mx | (am << 16)), L, WAVE);
+        const int32_t first = __shfl(incl - cnt, L, WAVE);
+        const int32_t RO = PUSH ? __shfl(R, L, WAVE) : 0;
+        const bool valid = g < E;
+        const uint32_t e = (uint32_t)(g - first), nnz = desc_nnz(dO);
+        const uint64_t off = desc_off(dO);
+        const uint32_t cd = valid ? a.pay[off + (uint64_t)vb * nnz + e] : 0u;
+        float val = 0.f;
+        if constexpr (valued<MODE>()) val = valid ? VT<MODE>::load(a.pay + off, e) : 0.f;
+        const uint32_t r = cd >> 4, c = cd & 15u;
+        const bool m = valid && ((mxam >> c) & (mxam >> (16 + r)) & 1u);
+        if (m) {
+            if constexpr (valued<MODE>()) {
+                const float prod = val * VT<MODE>::x(a.xd, (int64_t)JO * BS + c);
+                if constexpr (PUSH) atomicAdd(&a.yacc[(int64_t)RO * BS + r], (double)prod);
+                else atomicAdd(&dst[(L >> 4) * 16 + r], prod);
+            }
+            if constexpr (MODE == M_BFS) {
+                if constexpr (PUSH) atomicMin(&a.parent[(int64_t)RO * BS + r], JO * BS + (int32_t)c);
+                else atomicMin(&pdst[(L >> 4) * 16 + r], JO * BS + (int32_t)c);
+            }
+            atomicOr(&hits[L], 1u << r);
+        }
+    }
+    wave_lds_sync();
+    return own ? hits[lane] : 0u;
+}
+
 // Blocks staged for whole-wave processing: slot-major, one entry per lane.
 // After an entry is processed its J word carries the rows hit back to the
-// lane that staged it (5 KB per wave, so that the traversal kernels' LDS
-// stays well inside the compute unit's 160 KB at full occupancy).
+// lane that staged it.  4 KB per wave (5 KB with the block rows push needs),
+// so that the traversal kernels' LDS, with the pull kernel's activity
+// bitmap, stays inside the compute unit's 160 KB at five workgroups.
+template <bool PUSH>
 struct HeavyStage {
     uint64_t d[SLOTS * WAVE];
     int32_t J[SLOTS * WAVE];      // block column; rows hit once processed
-    int32_t R[SLOTS * WAVE];
     uint32_t mxam[SLOTS * WAVE];  // vector-block mask | admitted rows << 16
+    uint32_t hitw[WAVE];          // rows hit per owner lane (coo_flat)
+    int32_t R[PUSH ? SLOTS * WAVE : 1];
     __device__ __forceinline__ void stage(int e, uint64_t dd, int32_t j, uint32_t mx, uint32_t am, int32_t r)
     {
         d[e] = dd;
         J[e] = j;
-        R[e] = r;
+        if constexpr (PUSH) R[e] = r;
         mxam[e] = mx | (am << 16);
     }
     __device__ __forceinline__ uint32_t hits(int e) const { return (uint32_t)J[e]; }
@@ -654,9 +749,9 @@ struct HeavyStage {
 // Pull: the partial row sums go to the owning quarter's LDS accumulators of
 // that slot.  Push: each block's row sums are committed to HBM at once.  The
 // rows hit are handed back through hs->hits to the lane that staged the block.
-template <int MODE>
-__device__ void run_staged(const MainArgs &a, HeavyStage *hs, const uint64_t (&hv)[SLOTS], float *sy,
-                           int32_t *sp, bool push)
+template <int MODE, bool PUSH>
+__device__ void run_staged(const MainArgs &a, HeavyStage<PUSH> *hs, const uint64_t (&hv)[SLOTS], float *sy,
+                           int32_t *sp)
 {
     const int lane = lane_id();
     for (int k = 0; k < SLOTS; ++k) {
@@ -668,10 +763,10 @@ __device__ void run_staged(const MainArgs &a, HeavyStage *hs, const uint64_t (&h
             const uint64_t dL = hs->d[e];
             const int32_t JL = hs->J[e];
             const uint32_t mxam = hs->mxam[e];
-            float *dst = push ? sy : sy + k * WAVE + (L >> 4) * 16;
-            int32_t *pdst = push ? sp : sp + k * WAVE + (L >> 4) * 16;
+            float *dst = PUSH ? sy : sy + k * WAVE + (L >> 4) * 16;
+            int32_t *pdst = PUSH ? sp : sp + k * WAVE + (L >> 4) * 16;
             const uint32_t h = heavy_block<MODE>(a.pay, a.vb, dL, JL, mxam & 0xFFFFu, mxam >> 16, a.xd, dst, pdst);
-            if (push) {
+            if constexpr (PUSH) {
                 const int32_t RL = hs->R[e];
                 wave_lds_sync();
                 if (lane < 16) {
@@ -698,8 +793,18 @@ __device__ void run_staged(const MainArgs &a, HeavyStage *hs, const uint64_t (&h
 // segment groups.  Blocks that need the whole wave (non-COO formats, long
 // COO blocks) are staged in LDS and processed one by one after the
 // lane-parallel COO work, from a single call site.
-template <int MODE>
-__device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage *hs,
+// Activity bitmap of the pull kernel (one bit per vector block), written by
+// the scan: up to 16 KB (131072 vector blocks) it is copied into the LDS of
+// every workgroup and tested before the vector-block mask is gathered.  A
+// larger bitmap is not used (a global lookup would add a dependent load in
+// front of the mask gather).
+constexpr int32_t LDS_BITMAP_WORDS = 4096;
+extern __shared__ uint32_t lds_bits[];
+
+__device__ __forceinline__ bool block_active(int32_t J) { return (lds_bits[J >> 5] >> (J & 31)) & 1u; }
+
+template <int MODE, bool LDSBITS>
+__device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<false> *hs,
                           bool spec)
 {
     const int lane = lane_id(), q = lane >> 4, i = lane & 15;
@@ -708,23 +813,27 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
     const int spq = a.nseg >= (int64_t)nw * 4 * SLOTS * 2 ? SLOTS : 1;
     const int64_t groups = (a.nseg + 4 * spq - 1) / (4 * spq);
     for (int64_t u = gw; u < groups; u += nw) {
-        uint64_t s[SLOTS], d[SLOTS];
+        uint32_t s[SLOTS];
+        uint64_t d[SLOTS];
         bool vs[SLOTS], act[SLOTS];
         int32_t b[SLOTS], J[SLOTS];
         uint32_t am[SLOTS], mx[SLOTS];
+        // segment word, block column and (spec) descriptor: independent loads
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
             const int64_t sid = u * 4 * spq + q * spq + k;
             vs[k] = k < spq && sid < a.nseg;
-            s[k] = vs[k] ? a.seg[sid] : 0ull;
+            s[k] = vs[k] ? a.seg_rs[sid] : 0u;
+            b[k] = (int32_t)(sid * 16 + i);
+            J[k] = vs[k] ? a.sl_col[b[k]] : -1;
+            d[k] = (vs[k] && spec) ? a.sl_desc[b[k]] : 0ull;
         }
+        // activity bit first (when the bitmap is in LDS), then the 16-bit mask
+        // only for the blocks whose vector block is nonzero
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
-            am[k] = vs[k] ? row_admit(a, (int32_t)seg_brow(s[k])) : 0u;
-            act[k] = vs[k] && (uint32_t)i < seg_nb(s[k]) && am[k] != 0;
-            b[k] = (int32_t)seg_first(s[k]) + i;
-            J[k] = act[k] ? a.cb_col[b[k]] : 0;
-            d[k] = (act[k] && spec) ? a.desc[b[k]] : 0ull;
+            am[k] = vs[k] ? row_admit(a, (int32_t)(s[k] & 0x7FFFFFFFu)) : 0u;
+            act[k] = J[k] >= 0 && am[k] != 0 && (!LDSBITS || block_active(J[k]));
         }
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
@@ -733,8 +842,10 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
         }
         if (!spec) {
 #pragma unroll
-            for (int k = 0; k < SLOTS; ++k) d[k] = act[k] ? a.desc[b[k]] : 0ull;
+            for (int k = 0; k < SLOTS; ++k) d[k] = act[k] ? a.sl_desc[b[k]] : 0ull;
         }
+        // nothing to multiply anywhere in the wave: the LDS rows are untouched
+        if (!ballot(act[0] || act[1] || act[2] || act[3])) continue;
         uint32_t hit[SLOTS];
         uint64_t hv[SLOTS];
 #pragma unroll
@@ -744,13 +855,15 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             if (lanework)
                 hit[k] = coo_block<MODE>(a.pay, a.vb, d[k], J[k], mx[k], am[k], a.xd,
                                          sy + k * WAVE + q * 16, sp + k * WAVE + q * 16);
-            const bool wavework = act[k] && !lanework;
+            hit[k] |= coo_flat<MODE, false>(a, act[k] && flat_coo(d[k]), d[k], J[k], mx[k], am[k], 0,
+                                            sy + k * WAVE, sp + k * WAVE, hs->hitw);
+            const bool wavework = act[k] && desc_type(d[k]) != T_COO;
             hv[k] = ballot(wavework);
             if (wavework) hs->stage(k * WAVE + lane, d[k], J[k], mx[k], am[k], 0);
         }
         if (hv[0] | hv[1] | hv[2] | hv[3]) {
             wave_lds_sync();
-            run_staged<MODE>(a, hs, hv, sy, sp, false);
+            run_staged<MODE, false>(a, hs, hv, sy, sp);
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k) if ((hv[k] >> lane) & 1u) hit[k] |= hs->hits(k * WAVE + lane);
         }
@@ -760,10 +873,10 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
         for (int k = 0; k < SLOTS; ++k) hq[k] = or16_in_quarter(hit[k]);
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
-            const int32_t R = (int32_t)seg_brow(s[k]);
+            const int32_t R = (int32_t)(s[k] & 0x7FFFFFFFu);
             const float *my = sy + k * WAVE;
             bool carry = false;
-            if (k + 1 < SLOTS) carry = vs[k] && vs[k + 1] && (int32_t)seg_brow(s[k + 1]) == R;
+            if (k + 1 < SLOTS) carry = vs[k] && vs[k + 1] && (int32_t)(s[k + 1] & 0x7FFFFFFFu) == R;
             if (carry) {
                 // the next slot continues this block row: fold the partial sums into it
                 if constexpr (valued<MODE>()) sy[(k + 1) * WAVE + lane] += my[lane];
@@ -772,7 +885,7 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             } else if (vs[k]) {
                 if ((hq[k] >> i) & 1u) {
                     const int64_t row = (int64_t)R * BS + i;
-                    const bool single = seg_single(s[k]);
+                    const bool single = (s[k] >> 31) != 0;
                     if constexpr (valued<MODE>()) {
                         const float v = my[lane];
                         if (single) a.yacc[row] = (double)v;
@@ -840,7 +953,7 @@ __device__ __forceinline__ void wave_search(const int32_t *__restrict__ arr, int
 // its own item by a 6-step binary search over the next 64 item starts, held
 // one per lane and read by shuffles.
 template <int MODE>
-__device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage *hs)
+__device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<true> *hs)
 {
     const int lane = lane_id();
     const int32_t T = a.counters[C_TASKS];
@@ -886,7 +999,7 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
             R[k] = vt[k] ? a.csc_row[p[k]] : 0;
-            bb[k] = vt[k] ? a.csc2csr[p[k]] : 0;
+            bb[k] = vt[k] ? a.csc_slot[p[k]] : 0;
             mx[k] = vt[k] ? mask16(a.xmask, J[k]) : 0u;
         }
         bool act[SLOTS];
@@ -895,7 +1008,7 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
         for (int k = 0; k < SLOTS; ++k) {
             am[k] = vt[k] ? row_admit(a, R[k]) : 0u;
             act[k] = vt[k] && am[k] != 0;
-            d[k] = act[k] ? a.desc[bb[k]] : 0ull;
+            d[k] = act[k] ? a.sl_desc[bb[k]] : 0ull;
         }
         uint32_t hit[SLOTS];
         uint64_t hv[SLOTS];
@@ -906,13 +1019,15 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             if (lanework)
                 hit[k] = coo_block_push<MODE>(a.pay, a.vb, d[k], J[k], R[k], mx[k], am[k], a.xd, a.yacc,
                                               a.parent);
-            const bool wavework = act[k] && !lanework;
+            hit[k] |= coo_flat<MODE, true>(a, act[k] && flat_coo(d[k]), d[k], J[k], mx[k], am[k], R[k],
+                                           nullptr, nullptr, hs->hitw);
+            const bool wavework = act[k] && desc_type(d[k]) != T_COO;
             hv[k] = ballot(wavework);
             if (wavework) hs->stage(k * WAVE + lane, d[k], J[k], mx[k], am[k], R[k]);
         }
         if (hv[0] | hv[1] | hv[2] | hv[3]) {
             wave_lds_sync();
-            run_staged<MODE>(a, hs, hv, sy, sp, true);
+            run_staged<MODE, true>(a, hs, hv, sy, sp);
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k) if ((hv[k] >> lane) & 1u) hit[k] |= hs->hits(k * WAVE + lane);
             wave_lds_sync();
@@ -924,11 +1039,12 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
 }
 
 // LDS of one wave: per-slot row accumulators and the staged whole-wave blocks.
+template <bool PUSH>
 struct WaveLds {
-    float sy[SLOTS * WAVE];
-    int32_t sp[SLOTS * WAVE];
-    HeavyStage hs;
+    uint32_t acc[SLOTS * WAVE];  // row accumulators: fp32 sums, or BFS minimum parents
+    HeavyStage<PUSH> hs;
 };
+
 
 // The traversal kernels (one per path).  Both are launched for an automatic
 // path choice; each reads the choice the scan made on the device and the
@@ -936,27 +1052,34 @@ struct WaveLds {
 template <int MODE, int PATH>
 __global__ __launch_bounds__(TPB) void k_traverse(MainArgs a)
 {
-    __shared__ WaveLds lds[TPB / WAVE];
+    __shared__ WaveLds<PATH == PATH_PUSH> lds[TPB / WAVE];
     // BFS: the host has read the frontier size of this level; restart the count
     if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
     const int32_t N = a.counters[C_NZBLK];
     if (N == 0 || a.counters[C_PATH] != PATH) return;
     const int w = threadIdx.x >> 6, lane = lane_id();
-    WaveLds &L = lds[w];
+    WaveLds<PATH == PATH_PUSH> &L = lds[w];
+    float *sy = (float *)L.acc;
+    int32_t *sp = (int32_t *)L.acc;
 #pragma unroll
-    for (int k = 0; k < SLOTS; ++k) {
-        L.sy[k * WAVE + lane] = 0.f;
-        L.sp[k * WAVE + lane] = INT_MAX;
-    }
-    wave_lds_sync();
+    for (int k = 0; k < SLOTS; ++k) L.acc[k * WAVE + lane] = MODE == M_BFS ? (uint32_t)INT_MAX : 0u;
     const int gw = blockIdx.x * (TPB / WAVE) + w, nw = gridDim.x * (TPB / WAVE);
     if constexpr (PATH == PATH_PUSH) {
-        push_loop<MODE>(a, gw, nw, L.sy, L.sp, &L.hs);
+        wave_lds_sync();
+        push_loop<MODE>(a, gw, nw, sy, sp, &L.hs);
     } else {
         // with a quarter or more of the vector blocks active, most visited blocks
         // are used: load their descriptors together with their block columns
         const bool spec = (int64_t)N * 4 >= (int64_t)a.nbc;
-        pull_loop<MODE>(a, gw, nw, L.sy, L.sp, &L.hs, spec);
+        const int32_t nwords = (a.nbc + 31) >> 5;
+        if (nwords <= LDS_BITMAP_WORDS) {
+            for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
+            __syncthreads();
+            pull_loop<MODE, true>(a, gw, nw, sy, sp, &L.hs, spec);
+        } else {
+            wave_lds_sync();
+            pull_loop<MODE, false>(a, gw, nw, sy, sp, &L.hs, spec);
+        }
     }
 }
 
@@ -1146,31 +1269,38 @@ static inline int grid_for(int64_t items, int per_block, int cap)
 // units x workgroups per compute unit at its register and LDS use), so that
 // the persistent grid is exactly one round of residency.
 template <int MODE, int PATH>
-static int resident_grid()
+static int resident_grid(size_t dyn_lds)
 {
-    static int cached = 0;
-    if (!cached) {
-        int dev = 0, cus = 0, per_cu = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_traverse<MODE, PATH>, TPB, 0) != hipSuccess ||
-            cus <= 0 || per_cu <= 0) {
-            cached = MAX_MAIN_GRID;
-        } else {
-            cached = cus * per_cu;
-        }
+    // cached per dynamic LDS size (a handful of distinct sizes occur)
+    static size_t cached_lds[8];
+    static int cached_grid[8];
+    static int ncached = 0;
+    for (int i = 0; i < ncached; ++i)
+        if (cached_lds[i] == dyn_lds) return cached_grid[i];
+    int dev = 0, cus = 0, per_cu = 0, grid = MAX_MAIN_GRID;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_traverse<MODE, PATH>, TPB, dyn_lds) == hipSuccess &&
+        cus > 0 && per_cu > 0)
+        grid = cus * per_cu;
+    if (ncached < 8) {
+        cached_lds[ncached] = dyn_lds;
+        cached_grid[ncached] = grid;
+        ++ncached;
     }
-    return cached;
+    return grid;
 }
 
 template <int MODE, int PATH>
 static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStream_t s)
 {
     const int64_t waves = PATH == PATH_PULL ? (A.nseg + 3) / 4 : (A.nblk + WAVE - 1) / WAVE;
+    const int32_t nwords = (A.nbc + 31) >> 5;
+    const size_t dyn = (PATH == PATH_PULL && nwords <= LDS_BITMAP_WORDS) ? (size_t)nwords * 4 : 0;
     int g = grid_for(waves, TPB / WAVE, MAX_MAIN_GRID);
-    const int cap = resident_grid<MODE, PATH>();
+    const int cap = resident_grid<MODE, PATH>(dyn);
     if (g > cap) g = cap;
-    hipLaunchKernelGGL((k_traverse<MODE, PATH>), dim3(g), dim3(TPB), 0, s, a);
+    hipLaunchKernelGGL((k_traverse<MODE, PATH>), dim3(g), dim3(TPB), dyn, s, a);
     return hipGetLastError();
 }
 
@@ -1211,7 +1341,7 @@ hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th
     dim3 g(grid_for(A.nbc, SCAN_TILE, INT_MAX)), b(TPB);
     const int p = C.scan_parity;
     hipLaunchKernelGGL(k_scan, g, b, 0, s, C.xmask, A.cb_ptr, A.nbc, C.act, C.task_off, C.pbase,
-                       C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3);
+                       C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) C.scan_parity = 1 - p;
     return e;
@@ -1222,17 +1352,18 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
                        hipStream_t s)
 {
     MainArgs a;
-    a.cb_col = A.cb_col;
-    a.desc = A.desc;
+    a.sl_col = A.sl_col;
+    a.sl_desc = A.sl_desc;
+    a.seg_rs = A.seg_rs;
     a.pay = A.pay;
     a.vb = A.dtype == 0 ? 4u : (A.dtype == 1 ? 2u : 0u);
     a.nbc = A.nbc;
     a.csc_row = A.csc_row;
-    a.csc2csr = A.csc2csr;
-    a.seg = A.seg;
+    a.csc_slot = A.csc_slot;
     a.nseg = A.nseg;
     a.xd = xd;
     a.xmask = C.xmask;
+    a.xbits = C.xbits;
     a.act = C.act;
     a.task_off = C.task_off;
     a.pbase = C.pbase;

@@ -7,13 +7,23 @@
 namespace dbs {
 
 // Device-resident DB matrix (Sec. 3.2.1): dual block views over one payload.
+//
+// On the device the primary (block-CSR) order is laid out in pull-segment
+// slots: segment s owns slots [16 s, 16 s + 16), its blocks in block-CSR
+// order followed by padding (block column -1).  A pull lane thus finds its
+// block column and descriptor at 16 s + lane without first reading the
+// segment, and the block-CSC view maps to slots (csc_slot) instead of
+// primary ids.  The payload records are unchanged.
 struct DevMatrix {
     int32_t m = 0, n = 0, nbr = 0, nbc = 0;
     int64_t nblk = 0, nseg = 0;
     int32_t dtype = 0;  // dbs_dtype
-    const int32_t *rb_ptr = nullptr, *cb_col = nullptr;
-    const int32_t *cb_ptr = nullptr, *csc_row = nullptr, *csc2csr = nullptr;
-    const uint64_t *desc = nullptr, *seg = nullptr;
+    const int32_t *sl_col = nullptr;    // 16 nseg: block column, -1 = padding
+    const uint64_t *sl_desc = nullptr;  // 16 nseg: descriptor
+    const uint32_t *seg_rs = nullptr;   // nseg: block row | 1 << 31 if the row has one segment
+    const int32_t *cb_ptr = nullptr;    // block-CSC view: column pointer (nbc + 1)
+    const int32_t *csc_row = nullptr;   // block row per CSC position
+    const int32_t *csc_slot = nullptr;  // slot per CSC position
     const uint8_t *pay = nullptr;
 };
 
@@ -39,6 +49,7 @@ struct DevCtx {
     void *xd = nullptr;           // dense x values, 16 * nbc entries (fp32 or fp16)
     uint32_t *xmask = nullptr;    // blk_x_mask, two 16-bit masks per word
     int32_t nxwords = 0;
+    uint32_t *xbits = nullptr;    // one activity bit per vector block, written by the scan
     int32_t *act = nullptr;       // push work items: active vector blocks with blocks, ascending (nbc)
     int32_t *task_off = nullptr;  // their first task (exclusive scan of block-CSC lengths) (nbc + 1)
     int32_t *pbase = nullptr;     // block-CSC position of task t of item a = pbase[a] + t (nbc)
