@@ -54,13 +54,13 @@ dbs_status dev_upload(std::vector<void *> &allocs, const std::vector<T> &h, cons
 }
 
 template <class T>
-dbs_status dev_zeros(std::vector<void *> &allocs, size_t count, T **out)
+dbs_status dev_zeros(std::vector<void *> &allocs, size_t count, T **out, int byte = 0)
 {
     size_t bytes = std::max<size_t>(count * sizeof(T), 16);
     void *p = nullptr;
     HIP_TRY(hipMalloc(&p, bytes), "hipMalloc (context)");
     allocs.push_back(p);
-    HIP_TRY(hipMemset(p, 0, bytes), "hipMemset (context)");
+    HIP_TRY(hipMemset(p, byte, bytes), "hipMemset (context)");
     *out = (T *)p;
     return DBS_OK;
 }
@@ -187,7 +187,7 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
     d.nseg = h->nseg;
     d.dtype = h->dtype;
     // primary order -> pull-segment slots (see DevMatrix)
-    std::vector<int32_t> sl_col, csc_slot;
+    std::vector<int32_t> sl_col, csc_slot, hv_slot;
     std::vector<uint64_t> sl_desc;
     std::vector<uint32_t> seg_rs;
     try {
@@ -198,14 +198,25 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
         std::vector<int32_t> slot_of((size_t)h->nblk);
         for (int64_t s = 0; s < h->nseg; ++s) {
             const uint64_t sg = h->seg[s];
-            seg_rs[s] = seg_brow(sg) | (seg_single(sg) ? 0x80000000u : 0u);
             const uint32_t first = seg_first(sg), nb = seg_nb(sg);
+            bool heavy = false;
             for (uint32_t i = 0; i < nb; ++i) {
                 const size_t slot = (size_t)16 * s + i;
+                const uint64_t dd = h->desc[first + i];
                 sl_col[slot] = h->cb_col[first + i];
-                sl_desc[slot] = h->desc[first + i];
+                sl_desc[slot] = dd;
                 slot_of[first + i] = (int32_t)slot;
+                if (desc_type(dd) != T_COO) {
+                    // whole-wave block: pulled from the heavy list, flagged in
+                    // the slot by the sign bit of its block column
+                    sl_col[slot] |= (int32_t)0x80000000u;
+                    hv_slot.push_back((int32_t)slot);
+                    heavy = true;
+                }
             }
+            // a row block with a listed block gets contributions from two
+            // places: its segments commit with atomics then
+            seg_rs[s] = seg_brow(sg) | (seg_single(sg) && !heavy ? 0x80000000u : 0u);
         }
         csc_slot.resize((size_t)h->nblk);
         for (int64_t q = 0; q < h->nblk; ++q) csc_slot[q] = slot_of[h->csc2csr[q]];
@@ -224,11 +235,13 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
         (s2 = dev_upload(A->allocs, h->cb_ptr, &d.cb_ptr)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->csc_row, &d.csc_row)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, csc_slot, &d.csc_slot)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, hv_slot, &d.hv_slot)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->payload, &d.pay)) != DBS_OK) {
         free_all(A->allocs);
         delete A;
         return s2;
     }
+    d.nheavy = (int64_t)hv_slot.size();
     fill_info(*h, &A->info);
     *out = A;
     return DBS_OK;
@@ -288,7 +301,8 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
     c.n_st_fin = ((nbr + 1) / 2 + 255) / 256 + 1;
     uint32_t *xmask = nullptr, *ybits = nullptr, *visited = nullptr, *nextm = nullptr;
     float *xd = nullptr;
-    if ((st = dev_zeros(ctx->allocs, (size_t)16 * nb, &xd)) != DBS_OK ||
+    // densified x: all-ones bits mark absent entries (fp32 and fp16 views)
+    if ((st = dev_zeros(ctx->allocs, (size_t)16 * nb, &xd, 0xFF)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &xmask)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)(nb + 31) / 32 + 64, &c.xbits)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)nbc + 1, &c.act)) != DBS_OK ||

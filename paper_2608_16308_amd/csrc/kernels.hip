@@ -145,8 +145,15 @@ __global__ __launch_bounds__(TPB) void k_scatter(const int32_t *__restrict__ xi,
         if (j < 0 || j >= n) {
             bad = true;
         } else {
-            if constexpr (MODE == M_F32) ((float *)xd)[j] = ((const float *)xv)[t];
-            if constexpr (MODE == M_F16) ((uint16_t *)xd)[j] = ((const uint16_t *)xv)[t];
+            // an input equal to the absent-entry marker becomes the canonical NaN
+            if constexpr (MODE == M_F32) {
+                const uint32_t v = ((const uint32_t *)xv)[t];
+                ((uint32_t *)xd)[j] = v == 0xFFFFFFFFu ? 0x7FC00000u : v;
+            }
+            if constexpr (MODE == M_F16) {
+                const uint16_t v = ((const uint16_t *)xv)[t];
+                ((uint16_t *)xd)[j] = v == 0xFFFFu ? (uint16_t)0x7E00u : v;
+            }
             const uint32_t J = (uint32_t)j >> 4;
             const uint32_t half = (J & 1) * 16;
             const uint32_t bit = 1u << (half + (j & 15));
@@ -176,14 +183,15 @@ __global__ __launch_bounds__(TPB) void k_ballot(const void *__restrict__ x, int3
     int64_t j = (int64_t)blockIdx.x * TPB + threadIdx.x;
     bool nz = false;
     if (j < n) {
+        // zero entries are not stored: they keep the absent-entry marker
         if constexpr (MODE == M_F16) {
             uint16_t v = ((const uint16_t *)x)[j];
-            ((uint16_t *)xd)[j] = v;
             nz = (v & 0x7FFFu) != 0;
+            ((uint16_t *)xd)[j] = !nz ? (uint16_t)0xFFFFu : v == 0xFFFFu ? (uint16_t)0x7E00u : v;
         } else {
             uint32_t v = ((const uint32_t *)x)[j];
-            ((uint32_t *)xd)[j] = v;
             nz = (v & 0x7FFFFFFFu) != 0;
+            ((uint32_t *)xd)[j] = !nz ? 0xFFFFFFFFu : v == 0xFFFFFFFFu ? 0x7FC00000u : v;
         }
     }
     uint64_t b = ballot(nz);
@@ -341,49 +349,12 @@ __device__ __forceinline__ uint32_t coo_matches(uint64_t cds, uint32_t nnz, uint
     return mm;
 }
 
-// One lane, one COO block of at most 8 entries (entries in row-major order).
-// Adds the products of the matching entries into dst16[row] (LDS), merging
-// runs of one row first; for BFS records the smallest active column per row
-// (the first match met, columns ascend within a row).  Returns the rows hit.
-template <int MODE>
-__device__ __forceinline__ uint32_t coo_block(const uint8_t *__restrict__ pay, uint32_t vb, uint64_t d,
-                                              int32_t J, uint32_t mx, uint32_t am,
-                                              const void *__restrict__ xd, float *dst16,
-                                              int32_t *pdst16)
-{
-    const uint32_t nnz = desc_nnz(d);
-    const uint8_t *rec = pay + (desc_inline(d) ? 0 : desc_off(d));
-    const uint64_t cds = coo_coords(d, pay, vb, nnz);
-    uint32_t mm = coo_matches(cds, nnz, mx, am);
-    uint32_t hit = 0;
-    int cur = -1;
-    float acc = 0.f;
-    while (mm) {
-        const uint32_t e = ctz32(mm);
-        mm &= mm - 1;
-        const uint32_t cd = (uint32_t)(cds >> (8 * e)) & 0xFFu, r = cd >> 4, c = cd & 15u;
-        if constexpr (valued<MODE>()) {
-            const float prod = coo_value<MODE>(d, rec, vb, e) * VT<MODE>::x(xd, (int64_t)J * BS + c);
-            if ((int)r != cur) {
-                if (cur >= 0) atomicAdd(&dst16[cur], acc);
-                cur = (int)r;
-                acc = prod;
-            } else {
-                acc += prod;
-            }
-        }
-        if constexpr (MODE == M_BFS) {
-            if (!((hit >> r) & 1u)) atomicMin(&pdst16[r], J * BS + (int32_t)c);
-        }
-        hit |= 1u << r;
-    }
-    if constexpr (valued<MODE>()) {
-        if (cur >= 0) atomicAdd(&dst16[cur], acc);
-    }
-    return hit;
-}
-
-// Same COO block, committing straight to global memory (push path).
+// One lane, one COO block whose entries sit in its descriptor (entries in
+// row-major order), committing straight to global memory (push path): the
+// products of the matching entries are added to the row accumulators,
+// merging runs of one row first; for BFS the smallest active column per row
+// is kept (the first match met, columns ascend within a row).  Returns the
+// rows hit.
 template <int MODE>
 __device__ __forceinline__ uint32_t coo_block_push(const uint8_t *__restrict__ pay, uint32_t vb,
                                                    uint64_t d, int32_t J, int32_t R, uint32_t mx,
@@ -424,10 +395,40 @@ __device__ __forceinline__ uint32_t coo_block_push(const uint8_t *__restrict__ p
 
 // COO blocks whose entries sit in the descriptor are processed by one lane
 // (no payload loads); COO blocks with a payload record are processed
-// entry-parallel by the whole wave (coo_flat); the other formats by the
+// entry-parallel by the whole wave (flat_pass); the other formats by the
 // whole wave, one block at a time (heavy_block).
 __device__ __forceinline__ bool lane_coo(uint64_t d) { return desc_inline(d); }
 __device__ __forceinline__ bool flat_coo(uint64_t d) { return !desc_inline(d) && desc_type(d) == T_COO; }
+
+// Densified x (valued modes): absent entries hold all-ones bits in either
+// element width, so the gather of x_j also tells whether x_j is stored.  The
+// scatter kernel maps an input whose bits equal the marker to the canonical
+// NaN.  Boolean modes test the vector-block mask instead.
+constexpr uint32_t X_ABSENT32 = 0xFFFFFFFFu;
+constexpr uint32_t X_ABSENT16 = 0xFFFFu;
+
+template <int MODE>
+__device__ __forceinline__ bool x_present(uint32_t raw, int32_t J, uint32_t c)
+{
+    if constexpr (MODE == M_F32) return raw != X_ABSENT32;
+    else if constexpr (MODE == M_F16) return raw != X_ABSENT16;
+    else return (raw >> ((J & 1) * 16 + c)) & 1u;
+}
+template <int MODE>
+__device__ __forceinline__ float x_value(uint32_t raw)
+{
+    if constexpr (MODE == M_F32) return __uint_as_float(raw);
+    else if constexpr (MODE == M_F16) return h2f((uint16_t)raw);
+    else return 0.f;
+}
+
+// Gathered x words held per inline COO block: one per entry for valued
+// modes (capacity 1 fp32 / 2 fp16 entries), the block's mask word otherwise.
+template <int MODE> constexpr int inline_max() { return MODE == M_F32 ? 1 : MODE == M_F16 ? 2 : 1; }
+__device__ __forceinline__ uint32_t inline_cd(uint64_t d, int e, uint32_t vb)
+{
+    return (uint32_t)(d >> inline_shift((uint32_t)e, vb)) & 0xFFu;
+}
 
 // i-th set bit of v (i >= 0), or -1.
 __device__ __forceinline__ int nth_set_bit(uint32_t v, int i)
@@ -450,21 +451,6 @@ __device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint32_t vb, ui
     const uint16_t *msk = (const uint16_t *)(rec + HDR_MASK);
     const uint8_t *st = rec + HDR_START;
     const int64_t xb = (int64_t)J * BS;
-
-    if (type == T_COO) {
-        // A COO block too long for one lane: one entry per lane (Sec. 3.3.3:
-        // COO blocks scan their packed coordinates and accumulate in LDS).
-        const uint8_t *crd = rec + vb * nnz;
-        uint32_t hl = 0;
-        for (uint32_t e = lane; e < nnz; e += WAVE) {
-            const uint32_t cd = crd[e], r = cd >> 4, c = cd & 15u;
-            if (!((mx >> c) & (am >> r) & 1u)) continue;
-            if constexpr (valued<MODE>()) atomicAdd(&dst16[r], VT<MODE>::load(rec, e) * VT<MODE>::x(xd, xb + c));
-            if constexpr (MODE == M_BFS) atomicMin(&pdst16[r], (int32_t)xb + (int32_t)c);
-            hl |= 1u << r;
-        }
-        return wave_or(hl);
-    }
 
     if constexpr (!valued<MODE>()) {
         // Boolean propagation (Alg. 5): per row lane, the active columns with a
@@ -612,7 +598,7 @@ __device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint32_t vb, ui
 // main traversal kernel
 // ---------------------------------------------------------------------------
 struct MainArgs {
-    const int32_t *sl_col;   // pull-segment slots: block column (-1 padding)
+    const int32_t *sl_col;   // pull-segment slots: block column (-1 padding, sign bit: listed)
     const uint64_t *sl_desc; // pull-segment slots: descriptor
     const uint32_t *seg_rs;  // per segment: block row | single-segment flag << 31
     const uint8_t *pay;
@@ -620,6 +606,8 @@ struct MainArgs {
     int32_t nbc;
     const int32_t *csc_row;
     const int32_t *csc_slot;
+    const int32_t *hv_slot;  // slots of the non-COO blocks (pull: whole-wave list)
+    int64_t nheavy;
     int64_t nseg;
     const void *xd;
     const uint32_t *xmask;
@@ -645,6 +633,61 @@ __device__ __forceinline__ uint32_t row_admit(const MainArgs &a, int32_t R)
     return allowed16(a.omask, a.complement, R);
 }
 
+// Gathers the word that holds x_j for j = 16 J + c: the value bits (valued
+// modes) or the vector-block mask word (boolean modes).
+template <int MODE>
+__device__ __forceinline__ uint32_t x_gather(const MainArgs &a, int32_t J, uint32_t c)
+{
+    const int64_t j = (int64_t)J * BS + c;
+    if constexpr (MODE == M_F32) return ((const uint32_t *)a.xd)[j];
+    else if constexpr (MODE == M_F16) return ((const uint16_t *)a.xd)[j];
+    else return a.xmask[J >> 1];
+}
+
+// One lane, one COO block whose entries sit in its descriptor, with the x
+// words already gathered (pull path): the products of the entries whose x is
+// stored and whose row is admitted are added to dst16[row] (LDS), merging
+// runs of one row first; for BFS the smallest active column per row is kept
+// in pdst16 (the first match met, columns ascend within a row).  Returns the
+// rows hit.
+template <int MODE>
+__device__ __forceinline__ uint32_t inline_block(const MainArgs &a, uint64_t d, int32_t J, uint32_t am,
+                                                 const uint32_t (&xr)[inline_max<MODE>()], float *dst16,
+                                                 int32_t *pdst16)
+{
+    constexpr int CAP = valued<MODE>() ? inline_max<MODE>() : 6;
+    const uint32_t nnz = desc_nnz(d), vb = a.vb;
+    uint32_t hit = 0;
+    int cur = -1;
+    float acc = 0.f;
+#pragma unroll
+    for (int e = 0; e < CAP; ++e) {
+        if ((uint32_t)e >= nnz) break;
+        const uint32_t cd = inline_cd(d, e, vb), r = cd >> 4, c = cd & 15u;
+        const uint32_t raw = xr[valued<MODE>() ? e : 0];
+        if (!x_present<MODE>(raw, J, c) || !((am >> r) & 1u)) continue;
+        if constexpr (valued<MODE>()) {
+            const uint32_t vbits = (uint32_t)(d >> (inline_shift((uint32_t)e, vb) + 8));
+            const float prod = (MODE == M_F32 ? __uint_as_float(vbits) : h2f((uint16_t)vbits)) * x_value<MODE>(raw);
+            if ((int)r != cur) {
+                if (cur >= 0) atomicAdd(&dst16[cur], acc);
+                cur = (int)r;
+                acc = prod;
+            } else {
+                acc += prod;
+            }
+        }
+        if constexpr (MODE == M_BFS) {
+            if (!((hit >> r) & 1u)) atomicMin(&pdst16[r], J * BS + (int32_t)c);
+        }
+        hit |= 1u << r;
+    }
+    if constexpr (valued<MODE>()) {
+        if (cur >= 0) atomicAdd(&dst16[cur], acc);
+    }
+    return hit;
+}
+
 __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int l)
 {
     const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, l, WAVE);
@@ -652,88 +695,21 @@ __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int l)
     return ((uint64_t)hi << 32) | lo;
 }
 
-// Entry-parallel COO (Sec. 3.3.3's COO microkernel, re-mapped to wave64):
-// the entries of the stored COO blocks owned by the lanes with own set are
-// numbered by a wave prefix sum, and the wave walks them 64 at a time, one
-// entry per lane.  A lane finds the block of its entry by a 6-step binary
-// search over the owners' inclusive prefix sums (read by shuffles) and
-// fetches that block's descriptor, column block and masks from the owner's
-// registers.  The coordinate and value loads of all lanes go out together,
-// then the x gathers.
-//   pull (PUSH false): products are added to the owner's quarter of the
-//   slot's LDS rows (dst + 16 (owner / 16) + row); BFS keeps the smallest
-//   active column per row there.
-//   push (PUSH true): products go straight to the fp64 accumulators of
-//   block row R of the owner.
-// Rows hit are collected per owner in hits (64 words of LDS) and returned to
-// the owner lane.
-template <int MODE, bool PUSH>
-__device__ uint32_t coo_flat(const MainArgs &a, bool own, uint64_t d, int32_t J, uint32_t mx, uint32_t am,
-                             int32_t R, float *dst, int32_t *pdst, uint32_t *hits)
-{
-    const int lane = lane_id();
-    if (!ballot(own)) return 0;
-    const int32_t cnt = own ? (int32_t)desc_nnz(d) : 0;
-    int32_t incl = cnt;
-#pragma unroll
-    for (int o = 1; o < WAVE; o <<= 1) {
-        const int32_t v = __shfl_up(incl, o, WAVE);
-        if (lane >= o) incl += v;
-    }
-    const int32_t E = __shfl(incl, WAVE - 1, WAVE);
-    hits[lane] = 0;
-    wave_lds_sync();
-    const uint32_t vb = a.vb;
-    for (int32_t base = 0; base < E; base += WAVE) {
-        const int32_t g = base + lane;
-        int lo = 0;
-#pragma unroll
-        for (int st = 32; st > 0; st >>= 1) {
-            const int32_t v = __shfl(incl, lo + st - 1, WAVE);
-            if (v <= g) lo += st;
-        }
-        const int L = lo < WAVE ? lo : WAVE - 1;
-        const uint64_t dO = shfl_u64(d, L);
-        const int32_t JO = __shfl(J, L, WAVE);
-        const uint32_t mxam = (uint32_t)__shfl((int)(mx | (am << 16)), L, WAVE);
-        const int32_t first = __shfl(incl - cnt, L, WAVE);
-        const int32_t RO = PUSH ? __shfl(R, L, WAVE) : 0;
-        const bool valid = g < E;
-        const uint32_t e = (uint32_t)(g - first), nnz = desc_nnz(dO);
-        const uint64_t off = desc_off(dO);
-        const uint32_t cd = valid ? a.pay[off + (uint64_t)vb * nnz + e] : 0u;
-        float val = 0.f;
-        if constexpr (valued<MODE>()) val = valid ? VT<MODE>::load(a.pay + off, e) : 0.f;
-        const uint32_t r = cd >> 4, c = cd & 15u;
-        const bool m = valid && ((mxam >> c) & (mxam >> (16 + r)) & 1u);
-        if (m) {
-            if constexpr (valued<MODE>()) {
-                const float prod = val * VT<MODE>::x(a.xd, (int64_t)JO * BS + c);
-                if constexpr (PUSH) atomicAdd(&a.yacc[(int64_t)RO * BS + r], (double)prod);
-                else atomicAdd(&dst[(L >> 4) * 16 + r], prod);
-            }
-            if constexpr (MODE == M_BFS) {
-                if constexpr (PUSH) atomicMin(&a.parent[(int64_t)RO * BS + r], JO * BS + (int32_t)c);
-                else atomicMin(&pdst[(L >> 4) * 16 + r], JO * BS + (int32_t)c);
-            }
-            atomicOr(&hits[L], 1u << r);
-        }
-    }
-    wave_lds_sync();
-    return own ? hits[lane] : 0u;
-}
-
-// Blocks staged for whole-wave processing: slot-major, one entry per lane.
-// After an entry is processed its J word carries the rows hit back to the
-// lane that staged it.  4 KB per wave (5 KB with the block rows push needs),
-// so that the traversal kernels' LDS, with the pull kernel's activity
-// bitmap, stays inside the compute unit's 160 KB at five workgroups.
+// Blocks staged for whole-wave processing: slot-major, one entry per lane
+// (entry k * 64 + lane for slot k).  After an entry is processed its J word
+// carries the rows hit back to the lane that staged it.  Stored COO blocks
+// for the entry-parallel pass use the same entries, with the descriptor
+// replaced by flat_word.  About 4.4 KB per wave (5.3 KB with the block rows
+// and per-block hits push needs), so that the traversal kernels' LDS, with
+// the pull kernel's activity bitmap, allows five workgroups per compute unit.
 template <bool PUSH>
 struct HeavyStage {
     uint64_t d[SLOTS * WAVE];
     int32_t J[SLOTS * WAVE];      // block column; rows hit once processed
     uint32_t mxam[SLOTS * WAVE];  // vector-block mask | admitted rows << 16
-    uint32_t hitw[WAVE];          // rows hit per owner lane (coo_flat)
+    int32_t mark[WAVE];           // entry-parallel pass: owner starting at each lane's entry
+    uint32_t hitw[PUSH ? SLOTS * WAVE : SLOTS * 4];  // entry-parallel pass: rows hit per block
+                                                     // (push) or per slot quarter (pull)
     int32_t R[PUSH ? SLOTS * WAVE : 1];
     __device__ __forceinline__ void stage(int e, uint64_t dd, int32_t j, uint32_t mx, uint32_t am, int32_t r)
     {
@@ -744,6 +720,143 @@ struct HeavyStage {
     }
     __device__ __forceinline__ uint32_t hits(int e) const { return (uint32_t)J[e]; }
 };
+
+// Staged word of a stored COO block in the entry-parallel pass: payload
+// offset, entry count and the number of entries before the block.  The
+// payload offset keeps 39 bits (512 GB), the count 8 and the start 17
+// (at most SLOTS * 64 blocks of at most 256 entries).
+__device__ __forceinline__ uint64_t flat_word(uint64_t d, uint32_t excl)
+{
+    return (desc_off(d) << 25) | ((uint64_t)(desc_nnz(d) - 1) << 17) | excl;
+}
+
+// One lane's entry of a window of the entry-parallel pass.
+struct FlatEntry {
+    int32_t o;      // staging entry (slot * 64 + lane) of the block
+    int32_t J;      // its block column
+    uint32_t mxam;  // its vector-block mask (when staged) | admitted rows << 16
+    uint32_t cd;    // coordinate byte (row << 4 | column)
+    float val;      // value (valued modes)
+    bool valid;
+};
+
+// Finds the block of entry base + lane and issues its coordinate and value
+// loads.
+template <int MODE, bool PUSH>
+__device__ __forceinline__ FlatEntry flat_issue(const MainArgs &a, HeavyStage<PUSH> *hs,
+                                                const uint32_t (&cnt)[SLOTS], const uint32_t (&excl)[SLOTS],
+                                                uint32_t tot, uint32_t base, int32_t &carry)
+{
+    const int lane = lane_id();
+    hs->mark[lane] = -1;
+    wave_lds_sync();
+#pragma unroll
+    for (int k = 0; k < SLOTS; ++k)
+        if (cnt[k] && excl[k] >= base && excl[k] < base + WAVE) hs->mark[excl[k] - base] = k * WAVE + lane;
+    wave_lds_sync();
+    int32_t o = hs->mark[lane];
+#pragma unroll
+    for (int st = 1; st < WAVE; st <<= 1) {
+        const int32_t v = __shfl_up(o, st, WAVE);
+        if (lane >= st) o = max(o, v);
+    }
+    if (o < 0) o = carry;
+    carry = __shfl(o, WAVE - 1, WAVE);
+    FlatEntry f;
+    const uint32_t g = base + (uint32_t)lane;
+    f.valid = g < tot;
+    f.o = o;
+    const uint64_t w = hs->d[o];
+    f.J = hs->J[o];
+    f.mxam = hs->mxam[o];
+    const uint64_t off = w >> 25;
+    const uint32_t nnz = (uint32_t)((w >> 17) & 0xFFu) + 1u, e = g - (uint32_t)(w & 0x1FFFFu);
+    f.cd = f.valid ? a.pay[off + (uint64_t)a.vb * nnz + e] : 0u;
+    f.val = 0.f;
+    if constexpr (valued<MODE>()) f.val = f.valid ? VT<MODE>::load(a.pay + off, e) : 0.f;
+    return f;
+}
+
+// Gathers x for the entry and adds its product (see flat_pass).  MXK: the
+// staged word holds the block's vector-block mask, which then answers the
+// boolean modes' presence test without a gather.
+template <int MODE, bool PUSH, bool MXK>
+__device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> *hs, const FlatEntry &f,
+                                            float *sy, int32_t *sp)
+{
+    const uint32_t r = f.cd >> 4, c = f.cd & 15u;
+    const bool adm = f.valid && ((f.mxam >> (16 + r)) & 1u);
+    constexpr bool known = MXK && !valued<MODE>();
+    const uint32_t raw = (adm && !known) ? x_gather<MODE>(a, f.J, c) : 0u;
+    const bool present = known ? ((f.mxam >> c) & 1u) != 0 : x_present<MODE>(raw, f.J, c);
+    if (adm && present) {
+        const int o = f.o, ko = o >> 6, lo = o & (WAVE - 1);
+        if constexpr (PUSH) {
+            const int64_t row = (int64_t)hs->R[o] * BS + r;
+            if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], (double)(f.val * x_value<MODE>(raw)));
+            if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], f.J * BS + (int32_t)c);
+            atomicOr(&hs->hitw[o], 1u << r);
+        } else {
+            const int at = ko * WAVE + (lo >> 4) * 16 + (int)r;
+            if constexpr (valued<MODE>()) atomicAdd(&sy[at], f.val * x_value<MODE>(raw));
+            if constexpr (MODE == M_BFS) atomicMin(&sp[at], f.J * BS + (int32_t)c);
+            atomicOr(&hs->hitw[ko * 4 + (lo >> 4)], 1u << r);
+        }
+    }
+}
+
+// Entry-parallel pass over the stored COO blocks of one wave iteration
+// (Sec. 3.3.3's COO microkernel, re-mapped to wave64).  The entries of the
+// blocks staged with cnt[k] > 0 are numbered in slot-major order by wave
+// prefix sums; the wave walks them 64 at a time, one entry per lane.  Each
+// round, the blocks that start inside the window mark their first entry;
+// a max-scan over the lanes then gives every lane the block of its entry
+// (blocks start in ascending entry order).  The coordinate and value loads
+// of all lanes go out together, then the x gathers.
+//   pull: products are added to the owner's quarter of its slot's LDS rows;
+//         BFS keeps the smallest active column per row there; rows hit are
+//         collected per slot quarter in hitw[slot * 4 + quarter].
+//   push: products go straight to the fp64 accumulators of the owner's
+//         block row; rows hit are collected per block in hitw[entry].
+template <int MODE, bool PUSH, bool MXK, class Between>
+__device__ void flat_pass(const MainArgs &a, HeavyStage<PUSH> *hs, const uint32_t (&cnt)[SLOTS],
+                          const uint64_t (&d)[SLOTS], float *sy, int32_t *sp, Between &&between)
+{
+    const int lane = lane_id();
+    uint32_t excl[SLOTS];
+    uint32_t tot = 0;
+#pragma unroll
+    for (int k = 0; k < SLOTS; ++k) {
+        uint32_t incl = cnt[k];
+#pragma unroll
+        for (int o = 1; o < WAVE; o <<= 1) {
+            const uint32_t v = (uint32_t)__shfl_up((int)incl, o, WAVE);
+            if (lane >= o) incl += v;
+        }
+        excl[k] = tot + incl - cnt[k];
+        tot += (uint32_t)__shfl((int)incl, WAVE - 1, WAVE);
+    }
+#pragma unroll
+    for (int k = 0; k < SLOTS; ++k)
+        if (cnt[k]) hs->d[k * WAVE + lane] = flat_word(d[k], excl[k]);
+    if constexpr (PUSH) {
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) hs->hitw[k * WAVE + lane] = 0u;
+    } else {
+        if (lane < SLOTS * 4) hs->hitw[lane] = 0u;
+    }
+    int32_t carry = 0;
+    // the first window is peeled: its record loads are in flight while the
+    // caller's inline products are formed
+    FlatEntry f = flat_issue<MODE, PUSH>(a, hs, cnt, excl, tot, 0u, carry);
+    between();
+    flat_finish<MODE, PUSH, MXK>(a, hs, f, sy, sp);
+    for (uint32_t base = WAVE; base < tot; base += WAVE) {
+        f = flat_issue<MODE, PUSH>(a, hs, cnt, excl, tot, base, carry);
+        flat_finish<MODE, PUSH, MXK>(a, hs, f, sy, sp);
+    }
+    wave_lds_sync();
+}
 
 // Processes the staged blocks of the wave one at a time with the whole wave.
 // Pull: the partial row sums go to the owning quarter's LDS accumulators of
@@ -803,11 +916,59 @@ extern __shared__ uint32_t lds_bits[];
 
 __device__ __forceinline__ bool block_active(int32_t J) { return (lds_bits[J >> 5] >> (J & 31)) & 1u; }
 
+// Pull: the non-COO blocks, listed at upload, spread over all waves ahead of
+// the segment loop.  Lane t of a wave loads the metadata of the wave's t-th
+// listed block (block column, block row, admitted rows, vector-block mask,
+// descriptor: all independent of each other, so they are in flight
+// together); the active blocks are then processed one at a time by the
+// whole wave (heavy_block) and committed with atomics (the segments of such
+// a block row commit with atomics as well).
+template <int MODE, bool LDSBITS>
+__device__ void pull_heavy(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp)
+{
+    const int lane = lane_id();
+    for (int64_t h0 = gw; h0 < a.nheavy; h0 += (int64_t)nw * WAVE) {
+        const int64_t h = h0 + (int64_t)lane * nw;
+        const bool valid = h < a.nheavy;
+        const int32_t b = valid ? a.hv_slot[h] : 0;
+        const int32_t J = valid ? (a.sl_col[b] & 0x7FFFFFFF) : 0;
+        const int32_t R = valid ? (int32_t)(a.seg_rs[b >> 4] & 0x7FFFFFFFu) : 0;
+        const uint32_t am = valid ? row_admit(a, R) : 0u;
+        bool act = am != 0;
+        if constexpr (LDSBITS) act = act && block_active(J);
+        const uint32_t mx = act ? mask16(a.xmask, J) : 0u;
+        act = act && mx != 0;
+        const uint64_t d = act ? a.sl_desc[b] : 0ull;
+        uint64_t m = ballot(act);
+        while (m) {
+            const int L = ctz64(m);
+            m &= m - 1;
+            const int32_t JL = (int32_t)readlane_u32((uint32_t)J, L), RL = (int32_t)readlane_u32((uint32_t)R, L);
+            const uint32_t mxL = readlane_u32(mx, L), amL = readlane_u32(am, L);
+            const uint64_t dL = readlane_u64(d, L);
+            const uint32_t hit = heavy_block<MODE>(a.pay, a.vb, dL, JL, mxL, amL, a.xd, sy, sp);
+            wave_lds_sync();
+            if (lane < 16) {
+                if ((hit >> lane) & 1u) {
+                    const int64_t row = (int64_t)RL * BS + lane;
+                    if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], (double)sy[lane]);
+                    if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], sp[lane]);
+                }
+                if constexpr (valued<MODE>()) sy[lane] = 0.f;
+                if constexpr (MODE == M_BFS) sp[lane] = INT_MAX;
+            }
+            if (lane == 0 && hit) or_mask16(a.ybits, RL, hit);
+            wave_lds_sync();
+        }
+    }
+}
+
 template <int MODE, bool LDSBITS>
 __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<false> *hs,
                           bool spec)
 {
     const int lane = lane_id(), q = lane >> 4, i = lane & 15;
+    constexpr int IM = inline_max<MODE>();
     // segments per quarter and iteration: SLOTS when there is enough work to
     // keep every wave busy with SLOTS of them, else 1
     const int spq = a.nseg >= (int64_t)nw * 4 * SLOTS * 2 ? SLOTS : 1;
@@ -828,17 +989,20 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             J[k] = vs[k] ? a.sl_col[b[k]] : -1;
             d[k] = (vs[k] && spec) ? a.sl_desc[b[k]] : 0ull;
         }
-        // activity bit first (when the bitmap is in LDS), then the 16-bit mask
-        // only for the blocks whose vector block is nonzero
+        // block activity: the LDS bitmap when it fits, else the vector-block
+        // mask (gathered here then, and kept for the whole-wave blocks)
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
             am[k] = vs[k] ? row_admit(a, (int32_t)(s[k] & 0x7FFFFFFFu)) : 0u;
-            act[k] = J[k] >= 0 && am[k] != 0 && (!LDSBITS || block_active(J[k]));
+            act[k] = J[k] >= 0 && am[k] != 0;
+            if constexpr (LDSBITS) act[k] = act[k] && block_active(J[k]);
         }
+        if constexpr (!LDSBITS) {
 #pragma unroll
-        for (int k = 0; k < SLOTS; ++k) {
-            mx[k] = act[k] ? mask16(a.xmask, J[k]) : 0u;
-            act[k] = act[k] && mx[k] != 0;
+            for (int k = 0; k < SLOTS; ++k) {
+                mx[k] = act[k] ? mask16(a.xmask, J[k]) : 0u;
+                act[k] = act[k] && mx[k] != 0;
+            }
         }
         if (!spec) {
 #pragma unroll
@@ -846,26 +1010,47 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
         }
         // nothing to multiply anywhere in the wave: the LDS rows are untouched
         if (!ballot(act[0] || act[1] || act[2] || act[3])) continue;
-        uint32_t hit[SLOTS];
-        uint64_t hv[SLOTS];
+        // Issue every gather that depends only on the descriptors at once:
+        // x of the entries of the inline COO blocks (one lane each) and (in
+        // flat_pass) the records of the stored COO blocks; the inline products
+        // are formed while the record loads are in flight.  Blocks of the
+        // other formats are not in the slots' work (negative block column):
+        // pull_heavy takes them.
+        uint32_t hit[SLOTS], cnt[SLOTS];
+        uint32_t xr[SLOTS][IM];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
-            hit[k] = 0;
-            const bool lanework = act[k] && lane_coo(d[k]);
-            if (lanework)
-                hit[k] = coo_block<MODE>(a.pay, a.vb, d[k], J[k], mx[k], am[k], a.xd,
-                                         sy + k * WAVE + q * 16, sp + k * WAVE + q * 16);
-            hit[k] |= coo_flat<MODE, false>(a, act[k] && flat_coo(d[k]), d[k], J[k], mx[k], am[k], 0,
-                                            sy + k * WAVE, sp + k * WAVE, hs->hitw);
-            const bool wavework = act[k] && desc_type(d[k]) != T_COO;
-            hv[k] = ballot(wavework);
-            if (wavework) hs->stage(k * WAVE + lane, d[k], J[k], mx[k], am[k], 0);
-        }
-        if (hv[0] | hv[1] | hv[2] | hv[3]) {
-            wave_lds_sync();
-            run_staged<MODE, false>(a, hs, hv, sy, sp);
+            const bool inl = act[k] && desc_inline(d[k]);
+            const uint32_t nnz = desc_nnz(d[k]);
+            if constexpr (!LDSBITS && !valued<MODE>()) {
+                // the vector-block mask is already here: it is the x word
+                xr[k][0] = mx[k] << ((J[k] & 1) * 16);
+            } else {
 #pragma unroll
-            for (int k = 0; k < SLOTS; ++k) if ((hv[k] >> lane) & 1u) hit[k] |= hs->hits(k * WAVE + lane);
+                for (int e = 0; e < IM; ++e)
+                    xr[k][e] = (inl && (uint32_t)e < nnz) ? x_gather<MODE>(a, J[k], inline_cd(d[k], e, a.vb) & 15u)
+                                                          : 0u;
+            }
+            const bool flat = act[k] && flat_coo(d[k]);
+            cnt[k] = flat ? nnz : 0u;
+            if (flat) hs->stage(k * WAVE + lane, d[k], J[k], LDSBITS ? 0u : mx[k], am[k], 0);
+        }
+        auto inline_products = [&]() {
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k) {
+                hit[k] = 0;
+                if (act[k] && desc_inline(d[k]))
+                    hit[k] = inline_block<MODE>(a, d[k], J[k], am[k], xr[k], sy + k * WAVE + q * 16,
+                                                sp + k * WAVE + q * 16);
+            }
+        };
+        if (ballot(cnt[0] | cnt[1] | cnt[2] | cnt[3])) {
+            wave_lds_sync();
+            flat_pass<MODE, false, !LDSBITS>(a, hs, cnt, d, sy, sp, inline_products);
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k) hit[k] |= hs->hitw[k * 4 + q];
+        } else {
+            inline_products();
         }
         wave_lds_sync();
         uint32_t hq[SLOTS];
@@ -1010,7 +1195,7 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             act[k] = vt[k] && am[k] != 0;
             d[k] = act[k] ? a.sl_desc[bb[k]] : 0ull;
         }
-        uint32_t hit[SLOTS];
+        uint32_t hit[SLOTS], cnt[SLOTS];
         uint64_t hv[SLOTS];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
@@ -1019,11 +1204,18 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             if (lanework)
                 hit[k] = coo_block_push<MODE>(a.pay, a.vb, d[k], J[k], R[k], mx[k], am[k], a.xd, a.yacc,
                                               a.parent);
-            hit[k] |= coo_flat<MODE, true>(a, act[k] && flat_coo(d[k]), d[k], J[k], mx[k], am[k], R[k],
-                                           nullptr, nullptr, hs->hitw);
+            const bool flat = act[k] && flat_coo(d[k]);
+            cnt[k] = flat ? desc_nnz(d[k]) : 0u;
             const bool wavework = act[k] && desc_type(d[k]) != T_COO;
             hv[k] = ballot(wavework);
-            if (wavework) hs->stage(k * WAVE + lane, d[k], J[k], mx[k], am[k], R[k]);
+            if (wavework || flat) hs->stage(k * WAVE + lane, d[k], J[k], mx[k], am[k], R[k]);
+        }
+        if (ballot(cnt[0] | cnt[1] | cnt[2] | cnt[3])) {
+            wave_lds_sync();
+            flat_pass<MODE, true, true>(a, hs, cnt, d, sy, sp, [] {});
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k) if (cnt[k]) hit[k] |= hs->hitw[k * WAVE + lane];
+            wave_lds_sync();
         }
         if (hv[0] | hv[1] | hv[2] | hv[3]) {
             wave_lds_sync();
@@ -1049,8 +1241,10 @@ struct WaveLds {
 // The traversal kernels (one per path).  Both are launched for an automatic
 // path choice; each reads the choice the scan made on the device and the
 // other one returns at once.
+// Pull is held to 96 registers (five waves per SIMD; a few spill), which
+// measured faster than four waves without spills; push keeps its registers.
 template <int MODE, int PATH>
-__global__ __launch_bounds__(TPB) void k_traverse(MainArgs a)
+__global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(MainArgs a)
 {
     __shared__ WaveLds<PATH == PATH_PUSH> lds[TPB / WAVE];
     // BFS: the host has read the frontier size of this level; restart the count
@@ -1075,9 +1269,11 @@ __global__ __launch_bounds__(TPB) void k_traverse(MainArgs a)
         if (nwords <= LDS_BITMAP_WORDS) {
             for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
             __syncthreads();
+            pull_heavy<MODE, true>(a, gw, nw, sy, sp);
             pull_loop<MODE, true>(a, gw, nw, sy, sp, &L.hs, spec);
         } else {
             wave_lds_sync();
+            pull_heavy<MODE, false>(a, gw, nw, sy, sp);
             pull_loop<MODE, false>(a, gw, nw, sy, sp, &L.hs, spec);
         }
     }
@@ -1099,7 +1295,7 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
                                                   int32_t *__restrict__ y_nnz,
                                                   int32_t *__restrict__ counters, uint64_t *status,
                                                   uint64_t *next_status, int32_t n_status,
-                                                  uint32_t *__restrict__ xmask,
+                                                  uint32_t *__restrict__ xmask, void *__restrict__ xd,
                                                   const int32_t *__restrict__ x_idx, int32_t k,
                                                   int32_t n)
 {
@@ -1109,10 +1305,15 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
     __shared__ uint32_t s_wpos[FIN_WORDS];
     for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < n_status; i += gridDim.x * TPB)
         next_status[i] = 0;
-    // clear the blk_x_mask words this call's x indices touched
+    // clear the blk_x_mask words this call's x indices touched, and put the
+    // absent-entry marker back into the densified x
     for (int32_t t = blockIdx.x * TPB + threadIdx.x; t < k; t += gridDim.x * TPB) {
         const int32_t j = x_idx[t];
-        if (j >= 0 && j < n) xmask[j >> 5] = 0u;
+        if (j >= 0 && j < n) {
+            xmask[j >> 5] = 0u;
+            if constexpr (MODE == M_F32) ((uint32_t *)xd)[j] = 0xFFFFFFFFu;
+            if constexpr (MODE == M_F16) ((uint16_t *)xd)[j] = (uint16_t)0xFFFFu;
+        }
     }
     const int tile = blockIdx.x;
     const int32_t w = tile * FIN_WORDS + threadIdx.x;
@@ -1170,6 +1371,7 @@ __global__ __launch_bounds__(TPB) void k_finalize_dense(double *__restrict__ yac
                                                         void *__restrict__ y, float *__restrict__ y32,
                                                         uint32_t *__restrict__ ybits, int32_t nywords,
                                                         uint32_t *__restrict__ xmask, int32_t nxwords,
+                                                        void *__restrict__ xd, int32_t n,
                                                         int32_t *__restrict__ counters)
 {
     const int64_t stride = (int64_t)gridDim.x * TPB;
@@ -1182,6 +1384,11 @@ __global__ __launch_bounds__(TPB) void k_finalize_dense(double *__restrict__ yac
     }
     for (int64_t i = (int64_t)blockIdx.x * TPB + threadIdx.x; i < nywords; i += stride) ybits[i] = 0u;
     for (int64_t i = (int64_t)blockIdx.x * TPB + threadIdx.x; i < nxwords; i += stride) xmask[i] = 0u;
+    // every x_j went through the densified x: restore the absent-entry marker
+    for (int64_t i = (int64_t)blockIdx.x * TPB + threadIdx.x; i < n; i += stride) {
+        if constexpr (MODE == M_F32) ((uint32_t *)xd)[i] = 0xFFFFFFFFu;
+        else ((uint16_t *)xd)[i] = (uint16_t)0xFFFFu;
+    }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         counters[C_YNNZ] = m;
         counters[C_ERR_LAST] = counters[C_ERR];
@@ -1353,6 +1560,8 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
 {
     MainArgs a;
     a.sl_col = A.sl_col;
+    a.hv_slot = A.hv_slot;
+    a.nheavy = A.nheavy;
     a.sl_desc = A.sl_desc;
     a.seg_rs = A.seg_rs;
     a.pay = A.pay;
@@ -1390,9 +1599,9 @@ hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_i
     uint64_t *st = C.st_fin[p], *nx = C.st_fin[1 - p];
     const int32_t ns = C.n_st_fin;
     switch (mode) {
-    case M_F32: hipLaunchKernelGGL(k_finalize<M_F32>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, x_idx, k, A.n); break;
-    case M_F16: hipLaunchKernelGGL(k_finalize<M_F16>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, x_idx, k, A.n); break;
-    default: hipLaunchKernelGGL(k_finalize<M_BOOL>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, x_idx, k, A.n); break;
+    case M_F32: hipLaunchKernelGGL(k_finalize<M_F32>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, C.xd, x_idx, k, A.n); break;
+    case M_F16: hipLaunchKernelGGL(k_finalize<M_F16>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, C.xd, x_idx, k, A.n); break;
+    default: hipLaunchKernelGGL(k_finalize<M_BOOL>, g, b, 0, s, C.ybits, nyw, C.yacc, A.m, y_idx, y_val, y_nnz, C.counters, st, nx, ns, C.xmask, C.xd, x_idx, k, A.n); break;
     }
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) C.fin_parity = 1 - p;
@@ -1406,9 +1615,9 @@ hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, 
     int64_t items = A.m > C.nxwords ? A.m : C.nxwords;
     dim3 g(grid_for(items, TPB, 4096)), b(TPB);
     if (mode == M_F16)
-        hipLaunchKernelGGL(k_finalize_dense<M_F16>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, C.nxwords, C.counters);
+        hipLaunchKernelGGL(k_finalize_dense<M_F16>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, C.nxwords, C.xd, A.n, C.counters);
     else
-        hipLaunchKernelGGL(k_finalize_dense<M_F32>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, C.nxwords, C.counters);
+        hipLaunchKernelGGL(k_finalize_dense<M_F32>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, C.nxwords, C.xd, A.n, C.counters);
     return hipGetLastError();
 }
 

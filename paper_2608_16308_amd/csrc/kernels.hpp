@@ -18,12 +18,14 @@ struct DevMatrix {
     int32_t m = 0, n = 0, nbr = 0, nbc = 0;
     int64_t nblk = 0, nseg = 0;
     int32_t dtype = 0;  // dbs_dtype
-    const int32_t *sl_col = nullptr;    // 16 nseg: block column, -1 = padding
+    const int32_t *sl_col = nullptr;    // 16 nseg: block column, -1 = padding, sign bit = listed in hv_slot
     const uint64_t *sl_desc = nullptr;  // 16 nseg: descriptor
     const uint32_t *seg_rs = nullptr;   // nseg: block row | 1 << 31 if the row has one segment
     const int32_t *cb_ptr = nullptr;    // block-CSC view: column pointer (nbc + 1)
     const int32_t *csc_row = nullptr;   // block row per CSC position
     const int32_t *csc_slot = nullptr;  // slot per CSC position
+    const int32_t *hv_slot = nullptr;   // slots of the non-COO blocks (pull: whole-wave list)
+    int64_t nheavy = 0;
     const uint8_t *pay = nullptr;
 };
 
