@@ -297,8 +297,8 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
     const int32_t nb = std::max(nbr, nbc);
     c.nxwords = (nb + 1) / 2 + 2;
     c.nywords = (nbr + 1) / 2 + 2;
-    c.n_st_scan = (nbc + 1023) / 1024 + 1;
-    c.n_st_fin = ((nbr + 1) / 2 + 255) / 256 + 1;
+    c.n_st_scan = scan_tiles(nbc) + 1;
+    c.n_st_fin = finalize_tiles(nbr) + 1;
     uint32_t *xmask = nullptr, *ybits = nullptr, *visited = nullptr, *nextm = nullptr;
     float *xd = nullptr;
     // densified x: all-ones bits mark absent entries (fp32 and fp16 views)
@@ -416,10 +416,22 @@ extern "C" dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring
         mode = A->d.dtype == DBS_F16 ? M_F16 : M_F32;
     }
     const hipStream_t s = ctx->stream;
+    // The automatic choice (push iff N_nzblk < th3 N_blk) is made on the
+    // device, so both traversal kernels are launched and one returns at once.
+    // Often k alone settles it: N_nzblk <= k, and N_nzblk >= ceil(k / 16)
+    // when the k indices are distinct and in range (with invalid x, which is
+    // flagged, the other path may be taken; y is the same).  Then only that
+    // kernel is launched.
+    int launch_path = (int)path;
+    if (path == DBS_PATH_AUTO) {
+        const double lim = (double)norm_th3(th3) * (double)A->d.nbc;
+        if ((double)x_nnz < lim) launch_path = DBS_PATH_PUSH;
+        else if ((double)((x_nnz + 15) / 16) >= lim) launch_path = DBS_PATH_PULL;
+    }
     LAUNCH(ctx, DBS_K_SCATTER, launch_scatter(A->d, ctx->c, mode, x_nnz, d_x_idx, d_x_val, s));
-    LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, (int)path, (double)norm_th3(th3), s));
+    LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, launch_path, (double)norm_th3(th3), s));
     LAUNCH(ctx, DBS_K_MAIN,
-           launch_main(A->d, ctx->c, mode, ctx->c.xd, d_mask, complement_mask ? 1 : 0, nullptr, (int)path, s));
+           launch_main(A->d, ctx->c, mode, ctx->c.xd, d_mask, complement_mask ? 1 : 0, nullptr, launch_path, s));
     LAUNCH(ctx, DBS_K_FINALIZE,
            launch_finalize(A->d, ctx->c, mode, d_y_idx, sr == DBS_OR_AND ? nullptr : d_y_val, d_y_nnz,
                            d_x_idx, x_nnz, s));
@@ -498,8 +510,9 @@ extern "C" dbs_status dbs_bfs(dbs_ctx *ctx, const dbs_matrix *A, int32_t source,
             stats->path[level] = h[C_PATH];
             stats->frontier[level] = frontier;
         }
+        // the scan's choice is on the host already: launch that kernel only
         LAUNCH(ctx, DBS_K_MAIN,
-               launch_main(A->d, ctx->c, M_BFS, nullptr, ctx->c.visited, 1, d_parent, (int)policy, s));
+               launch_main(A->d, ctx->c, M_BFS, nullptr, ctx->c.visited, 1, d_parent, h[C_PATH], s));
         LAUNCH(ctx, DBS_K_BFS_UPDATE, launch_bfs_update(A->d, ctx->c, level + 1, d_level, s));
         ++level;
     }

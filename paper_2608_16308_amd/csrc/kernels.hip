@@ -34,8 +34,9 @@
 namespace dbs {
 
 constexpr int TPB = 256;            // threads per workgroup (4 waves)
-constexpr int SCAN_ITEMS = 4;       // items per thread in the look-back scans
+constexpr int SCAN_ITEMS = SCAN_ITEMS_PER_THREAD;  // vector blocks per thread in the scan
 constexpr int SCAN_TILE = TPB * SCAN_ITEMS;
+static_assert(SCAN_ITEMS == 1 || SCAN_ITEMS == 2 || SCAN_ITEMS == 4, "scan items");
 constexpr int MAX_MAIN_GRID = 4096; // upper bound: 256 CUs x 16 workgroups
 
 constexpr uint64_t ST_AGG = 1ull << 62, ST_INC = 2ull << 62, ST_PAYLOAD = (1ull << 62) - 1;
@@ -129,9 +130,10 @@ __device__ uint64_t block_exclusive_scan(uint64_t v, uint64_t *total, uint64_t *
 // ---------------------------------------------------------------------------
 // vector blocker
 // ---------------------------------------------------------------------------
-// Sparse x: scatter the values into the dense scratch and set the mask bits.
-// The first index that lands in a vector block counts it (N_nzblk, Sec. 3.3.1);
-// an index whose bit is already set is a duplicate and is flagged.
+// Sparse x: scatter the values into the dense scratch and set the mask bits
+// (Sec. 3.2.2).  Out-of-range indices are counted and skipped.  N_nzblk
+// (Sec. 3.3.1) and the number of distinct indices (which exposes duplicates)
+// are counted afterwards by the scan from the masks.
 template <int MODE>
 __global__ __launch_bounds__(TPB) void k_scatter(const int32_t *__restrict__ xi,
                                                  const void *__restrict__ xv, int32_t k, int32_t n,
@@ -139,7 +141,10 @@ __global__ __launch_bounds__(TPB) void k_scatter(const int32_t *__restrict__ xi,
                                                  int32_t *__restrict__ counters)
 {
     const int32_t t = blockIdx.x * TPB + threadIdx.x;
-    bool first = false, bad = false, dup = false;
+    const int lane = lane_id();
+    bool bad = false;
+    int32_t w = -1;     // mask word of the entry (-1: none)
+    uint32_t bits = 0;  // its bit in that word
     if (t < k) {
         const int32_t j = xi[t];
         if (j < 0 || j >= n) {
@@ -154,20 +159,23 @@ __global__ __launch_bounds__(TPB) void k_scatter(const int32_t *__restrict__ xi,
                 const uint16_t v = ((const uint16_t *)xv)[t];
                 ((uint16_t *)xd)[j] = v == 0xFFFFu ? (uint16_t)0x7E00u : v;
             }
-            const uint32_t J = (uint32_t)j >> 4;
-            const uint32_t half = (J & 1) * 16;
-            const uint32_t bit = 1u << (half + (j & 15));
-            const uint32_t old = atomicOr(&xmask[J >> 1], bit);
-            dup = (old & bit) != 0;
-            first = !dup && ((old >> half) & 0xFFFFu) == 0;
+            w = j >> 5;
+            bits = 1u << (j & 31);
         }
     }
-    // one counter update per wave
-    const uint64_t fm = ballot(first), bm = ballot(bad), dm = ballot(dup);
-    if (lane_id() == 0) {
-        if (fm) atomicAdd(&counters[C_NZACC], (int32_t)__popcll(fm));
-        if (bm | dm) atomicOr(&counters[C_ERR], (bm ? 1 : 0) | (dm ? 2 : 0));
+    // Segmented OR over runs of lanes with the same mask word (sorted or
+    // clustered indices form long runs), then one non-returning atomic per
+    // run.  Duplicates and the nonzero vector blocks are counted by the scan.
+#pragma unroll
+    for (int o = 1; o < WAVE; o <<= 1) {
+        const uint32_t vb = (uint32_t)__shfl_up((int)bits, o, WAVE);
+        const int32_t vw = __shfl_up(w, o, WAVE);
+        if (lane >= o && vw == w) bits |= vb;
     }
+    const int32_t nextw = __shfl_down(w, 1, WAVE);
+    if (w >= 0 && (lane == WAVE - 1 || nextw != w)) atomicOr(&xmask[w], bits);
+    const uint64_t bm = ballot(bad);
+    if (lane == 0 && bm) atomicAdd(&counters[C_XBAD], (int32_t)__popcll(bm));
 }
 
 // Dense activation (Sec. 4.1): each wave reads 64 consecutive entries and
@@ -199,10 +207,7 @@ __global__ __launch_bounds__(TPB) void k_ballot(const void *__restrict__ x, int3
         int64_t w = (j - lane_id()) >> 5;
         if (w < nwords) xmask[w] = (uint32_t)b;
         if (w + 1 < nwords) xmask[w + 1] = (uint32_t)(b >> 32);
-        int cnt = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) cnt += ((b >> (16 * q)) & 0xFFFFull) != 0;
-        if (cnt) atomicAdd(&counters[C_NZACC], cnt);
+        (void)counters;
     }
 }
 
@@ -222,6 +227,7 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
                                               int32_t forced_path, double th3)
 {
     __shared__ uint64_t lds4[TPB / WAVE];
+    __shared__ uint64_t s_cnt[TPB / WAVE];
     __shared__ uint64_t s_prefix;
     // clear the other copy of the status words for the next scan
     for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < n_status; i += gridDim.x * TPB)
@@ -232,28 +238,45 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
     uint32_t len[SCAN_ITEMS];
     uint64_t mine = 0;
     uint32_t nib = 0;  // activity of this thread's 4 vector blocks
+    uint32_t pop = 0;  // stored x entries in them
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
         const int32_t J = base + k;
         const uint32_t am = J < nbc ? mask16(xmask, J) : 0u;
         nib |= (am ? 1u : 0u) << k;
+        pop += __popc(am);
         start[k] = am ? cb_ptr[J] : 0;
         len[k] = am ? (uint32_t)(cb_ptr[J + 1] - start[k]) : 0u;
         if (len[k]) mine += (1ull << 34) + len[k];
     }
-    // one activity bit per vector block: 8 threads x 4 blocks form a word
+    // one activity bit per vector block: 32 / SCAN_ITEMS threads form a word
     {
-        uint32_t word = nib << (4 * (lane_id() & 7));
-        word |= __shfl_xor(word, 1, WAVE);
-        word |= __shfl_xor(word, 2, WAVE);
-        word |= __shfl_xor(word, 4, WAVE);
+        constexpr int LPW = 32 / SCAN_ITEMS;
+        uint32_t word = nib << (SCAN_ITEMS * (lane_id() & (LPW - 1)));
+#pragma unroll
+        for (int o = 1; o < LPW; o <<= 1) word |= __shfl_xor(word, o, WAVE);
         const int32_t wi = base >> 5;
-        if ((lane_id() & 7) == 0 && base < nbc) xbits[wi] = word;
+        if ((lane_id() & (LPW - 1)) == 0 && base < nbc) xbits[wi] = word;
     }
+    // nonzero vector blocks and stored x entries of the tile (low / high
+    // 32 bits), reduced alongside the scan
+    uint64_t cnt2 = wave_sum(((uint64_t)pop << 32) | (uint64_t)__popc(nib));
+    if (lane_id() == 0) s_cnt[threadIdx.x >> 6] = cnt2;
     uint64_t total;
     uint64_t excl = block_exclusive_scan(mine, &total, lds4);
     if (threadIdx.x < WAVE) {
         uint64_t prefix = 0;
+        if (threadIdx.x == 0) {
+            // counted before the tile's status is published: a tile that has
+            // seen every earlier status (directly or through an inclusive
+            // one) also sees their counts
+            uint64_t c = 0;
+#pragma unroll
+            for (int i = 0; i < TPB / WAVE; ++i) c += s_cnt[i];
+            if ((uint32_t)c) atomicAdd(&counters[C_NZACC], (int32_t)(uint32_t)c);
+            if (c >> 32) atomicAdd(&counters[C_XPOP], (int32_t)(c >> 32));
+            __threadfence();
+        }
         if (tile == 0) {
             if (threadIdx.x == 0) st_store(&status[0], ST_INC | total);
         } else {
@@ -281,7 +304,8 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
         const uint64_t all = s_prefix + total;
         const int32_t NT = (int32_t)(all >> 34);
         const int32_t T = (int32_t)(all & ((1ull << 34) - 1));
-        const int32_t N = counters[C_NZACC];
+        __threadfence();
+        const int32_t N = __hip_atomic_load(&counters[C_NZACC], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         counters[C_NZACC] = 0;
         counters[C_NZBLK] = N;
         counters[C_NTB] = NT;
@@ -430,16 +454,77 @@ __device__ __forceinline__ uint32_t inline_cd(uint64_t d, int e, uint32_t vb)
     return (uint32_t)(d >> inline_shift((uint32_t)e, vb)) & 0xFFu;
 }
 
-// i-th set bit of v (i >= 0), or -1.
-__device__ __forceinline__ int nth_set_bit(uint32_t v, int i)
+
+// Header of a 16-group record (the 16-bit row masks, or column masks for
+// ForceCSC, then the 8-bit group starts), read by every lane with three
+// 16-byte loads (records of these formats are 16-byte aligned).
+struct Hdr16 {
+    uint32_t m[8];
+    uint32_t s[4];
+};
+__device__ __forceinline__ Hdr16 load_hdr(const uint8_t *rec)
 {
-    for (int k = 0; k < i && v; ++k) v &= v - 1;
-    return v ? ctz32(v) : -1;
+    const uint4 a = ((const uint4 *)(rec + HDR_MASK))[0], b = ((const uint4 *)(rec + HDR_MASK))[1];
+    const uint4 c = *(const uint4 *)(rec + HDR_START);
+    return Hdr16{{a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w}, {c.x, c.y, c.z, c.w}};
+}
+// (t is a constant after unrolling: no dynamic register indexing)
+__device__ __forceinline__ uint32_t hdr_mask(const Hdr16 &h, int t) { return (h.m[t >> 1] >> ((t & 1) * 16)) & 0xFFFFu; }
+__device__ __forceinline__ uint32_t hdr_start(const Hdr16 &h, int t) { return (h.s[t >> 2] >> ((t & 3) * 8)) & 0xFFu; }
+
+// Position of the k-th (0-based) set bit of a 16-bit v, by halving.
+__device__ __forceinline__ uint32_t nth_bit16(uint32_t v, uint32_t k)
+{
+    uint32_t pos = 0;
+#pragma unroll
+    for (int step = 8; step > 0; step >>= 1) {
+        const uint32_t c = __popc(v & ((1u << step) - 1u));
+        if (k >= c) {
+            k -= c;
+            v >>= step;
+            pos += (uint32_t)step;
+        }
+    }
+    return pos;
+}
+
+// Entry e of a 16-group record: its group (the last group starting at or
+// before e; empty groups start where the next one does) and its position
+// inside the group's mask.
+__device__ __forceinline__ void hdr_locate(const Hdr16 &h, uint32_t e, uint32_t &g, uint32_t &other)
+{
+    uint32_t gg = 0, gs = 0, gm = 0;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+        const uint32_t st = hdr_start(h, t);
+        if (st <= e) {
+            gg = (uint32_t)t;
+            gs = st;
+            gm = hdr_mask(h, t);
+        }
+    }
+    g = gg;
+    other = nth_bit16(gm, e - gs);
+}
+
+template <int MODE>
+__device__ __forceinline__ uint32_t xd_raw(const void *xd, int64_t j)
+{
+    if constexpr (MODE == M_F32) return ((const uint32_t *)xd)[j];
+    else return ((const uint16_t *)xd)[j];
 }
 
 // Whole wave, one block of a non-COO format.  Adds the row sums of the
 // admitted rows into dst16 (LDS); for BFS records the smallest active
 // column per row in pdst16.  Returns the rows hit (uniform).
+//   ForceCSR, patched CSR (row view) and ForceCSC (column view) are taken
+//   entry-parallel (Alg. 2 and 3 re-mapped to wave64): lane t takes entries
+//   t, t + 64, ...; it locates its entry's row and column from the record
+//   header, which every lane loads together with its values, then gathers
+//   x (value and presence in one word) -- two dependent loads in all,
+//   whatever the vector-block mask.
+//   Dense (Alg. 4): 4 lanes per row, 4 consecutive columns each.
+//   Boolean modes need only the masks (Alg. 5).
 template <int MODE>
 __device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint32_t vb, uint64_t d, int32_t J,
                                 uint32_t mx, uint32_t am, const void *__restrict__ xd, float *dst16,
@@ -449,30 +534,25 @@ __device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint32_t vb, ui
     const uint32_t type = desc_type(d), nnz = desc_nnz(d);
     const uint8_t *rec = pay + desc_off(d);
     const uint16_t *msk = (const uint16_t *)(rec + HDR_MASK);
-    const uint8_t *st = rec + HDR_START;
     const int64_t xb = (int64_t)J * BS;
 
     if constexpr (!valued<MODE>()) {
         // Boolean propagation (Alg. 5): per row lane, the active columns with a
         // stored entry; the first one is the smallest candidate parent.
-        const int r = lane & 15;
-        uint32_t cand = 0;
-        if (lane < 16) {
-            if (type == T_FCSC) {
-                uint32_t a = mx;
-                while (a) {
-                    int c = ctz32(a);
-                    if ((msk[c] >> r) & 1u) { cand = 1u << c; break; }  // first hit ends the scan
-                    a &= a - 1;
-                }
-            } else {
-                cand = msk[r] & mx;
-            }
+        const Hdr16 h = load_hdr(rec);
+        const uint32_t r = (uint32_t)lane & 15u;
+        uint32_t cand = 0, rm = 0;
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+            const uint32_t mt = hdr_mask(h, t);
+            cand |= (((mx >> t) & (mt >> r)) & 1u) << t;  // ForceCSC: column masks
+            rm = (uint32_t)t == r ? mt : rm;             // the others: row masks
         }
-        bool h = lane < 16 && cand != 0 && ((am >> r) & 1u);
-        uint32_t hits = (uint32_t)ballot(h) & 0xFFFFu;
+        if (type != T_FCSC) cand = rm & mx;
+        bool hl = lane < 16 && cand != 0 && ((am >> r) & 1u);
+        uint32_t hits = (uint32_t)ballot(hl) & 0xFFFFu;
         if constexpr (MODE == M_BFS) {
-            if (h) atomicMin(&pdst16[r], (int32_t)xb + ctz32(cand));
+            if (hl) atomicMin(&pdst16[r], (int32_t)xb + ctz32(cand));
         }
         return hits;
     } else {
@@ -508,91 +588,39 @@ __device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint32_t vb, ui
             if (h) atomicAdd(&dst16[rr], srow);
             return hits;
         }
-        const bool rowwise = type == T_FCSR || (type == T_CSR && __popc(mx) >= 8);
-        if (rowwise) {
-            // Alg. 2 on wave64: 4 lanes per row take every 4th active column.
-            const uint8_t *vals = rec + values_at(type, nnz);
-            const int r = lane >> 2, sub = lane & 3;
-            const uint32_t rm = msk[r];
-            uint32_t a = rm & mx;
-            const uint32_t start = st[r];
-            float s = 0.f;
-            int k = 0;
-            while (a) {
-                int c = ctz32(a);
-                if ((k & 3) == sub) {
-                    uint32_t p = start + __popc(rm & ((1u << c) - 1u));
-                    s = fmaf(VT<MODE>::load(vals, p), VT<MODE>::x(xd, xb + c), s);
-                }
-                a &= a - 1;
-                ++k;
+        // entry-parallel ForceCSR / patched CSR / ForceCSC
+        const bool colview = type == T_FCSC;
+        const uint8_t *vals = rec + values_at(type, nnz);
+        const Hdr16 h = load_hdr(rec);
+        uint32_t hl = 0;
+        for (uint32_t e0 = 0; e0 < nnz; e0 += 2 * WAVE) {
+            // two entries per lane per pass, loads issued together
+            const uint32_t e[2] = {e0 + (uint32_t)lane, e0 + WAVE + (uint32_t)lane};
+            float v[2];
+            uint32_t r[2], c[2], raw[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) v[u] = e[u] < nnz ? VT<MODE>::load(vals, e[u]) : 0.f;
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                uint32_t g, o;
+                hdr_locate(h, e[u], g, o);
+                r[u] = colview ? o : g;
+                c[u] = colview ? g : o;
+                const bool adm = e[u] < nnz && ((am >> r[u]) & 1u);
+                raw[u] = adm ? xd_raw<MODE>(xd, xb + c[u]) : (MODE == M_F32 ? X_ABSENT32 : X_ABSENT16);
             }
-            s += __shfl_xor(s, 1, WAVE);
-            s += __shfl_xor(s, 2, WAVE);
-            const int rr = lane & 15;
-            float srow = __shfl(s, rr * 4, WAVE);
-            bool h = lane < 16 && (msk[rr] & mx) != 0 && ((am >> rr) & 1u);
-            uint32_t hits = (uint32_t)ballot(h) & 0xFFFFu;
-            if (h) atomicAdd(&dst16[rr], srow);
-            return hits;
-        }
-        if (type == T_FCSC) {
-            // Alg. 3 on wave64: lane = row, 4 column quarters per wave.
-            const uint8_t *vals = rec + HDR_START2;
-            const int r = lane & 15, part = lane >> 4;
-            uint32_t a = mx & (0xFu << (4 * part));
-            float s = 0.f;
-            uint32_t found = 0;
-            while (a) {
-                int c = ctz32(a);
-                uint32_t cm = msk[c];
-                if ((cm >> r) & 1u) {
-                    uint32_t p = st[c] + __popc(cm & ((1u << r) - 1u));
-                    s = fmaf(VT<MODE>::load(vals, p), VT<MODE>::x(xd, xb + c), s);
-                    found = 1;
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                if (raw[u] != (MODE == M_F32 ? X_ABSENT32 : X_ABSENT16)) {
+                    atomicAdd(&dst16[r[u]], v[u] * x_value<MODE>(raw[u]));
+                    hl |= 1u << r[u];
                 }
-                a &= a - 1;
             }
-            s += __shfl_xor(s, 16, WAVE);
-            s += __shfl_xor(s, 32, WAVE);
-            found |= __shfl_xor(found, 16, WAVE);
-            found |= __shfl_xor(found, 32, WAVE);
-            bool h = lane < 16 && found && ((am >> r) & 1u);
-            uint32_t hits = (uint32_t)ballot(h) & 0xFFFFu;
-            if (h) atomicAdd(&dst16[r], s);
-            return hits;
         }
-        // Patched CSR with a sparse vector block: push by columns through
-        // col_start and row_idx_csc2csr (row << 4 | rank in row), reading only
-        // the entries of the active columns; 4 columns x 16 entries per pass.
-        {
-            const uint8_t *cs = rec + HDR_START2;
-            const uint8_t *rcsc = rec + HDR_RCSC;
-            const uint8_t *vals = rec + values_at(type, nnz);
-            const int slot = lane >> 4, k = lane & 15;
-            uint32_t cols = mx;
-            uint32_t hl = 0;
-            while (cols) {
-                int c = nth_set_bit(cols, slot);
-                if (c >= 0) {
-                    uint32_t b0 = cs[c], b1 = c == 15 ? nnz : cs[c + 1];
-                    if ((uint32_t)k < b1 - b0) {
-                        uint32_t rc = rcsc[b0 + k];
-                        uint32_t row = rc >> 4, rank = rc & 15u;
-                        if ((am >> row) & 1u) {
-                            uint32_t p = st[row] + rank;
-                            atomicAdd(&dst16[row], VT<MODE>::load(vals, p) * VT<MODE>::x(xd, xb + c));
-                            hl |= 1u << row;
-                        }
-                    }
-                }
-                for (int q = 0; q < 4 && cols; ++q) cols &= cols - 1;
-            }
-            return wave_or(hl);
-        }
+        (void)VB;
+        return wave_or(hl);
     }
 }
-
 
 // ---------------------------------------------------------------------------
 // main traversal kernel
@@ -1286,7 +1314,9 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(Mai
 // (its popcount enters the tile scan and the look-back); the rows are then
 // written in 32 rounds where thread t handles row t + 256 r of the tile, so
 // consecutive lanes touch consecutive accumulators and output slots.
-constexpr int FIN_WORDS = TPB;
+constexpr int FIN_WORDS = FINALIZE_WORDS;
+constexpr int FIN_ROUNDS = FIN_WORDS * 32 / TPB;  // rows per thread
+static_assert(FIN_WORDS <= TPB && FIN_ROUNDS >= 1, "finalize tile");
 
 template <int MODE>
 __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, int32_t nywords,
@@ -1317,11 +1347,13 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
     }
     const int tile = blockIdx.x;
     const int32_t w = tile * FIN_WORDS + threadIdx.x;
-    const uint32_t word = w < nywords ? ybits[w] : 0u;
+    const uint32_t word = ((int)threadIdx.x < FIN_WORDS && w < nywords) ? ybits[w] : 0u;
     uint64_t total;
     const uint64_t excl = block_exclusive_scan((uint64_t)__popc(word), &total, lds4);
-    s_word[threadIdx.x] = word;
-    s_wpos[threadIdx.x] = (uint32_t)excl;
+    if ((int)threadIdx.x < FIN_WORDS) {
+        s_word[threadIdx.x] = word;
+        s_wpos[threadIdx.x] = (uint32_t)excl;
+    }
     if (threadIdx.x < WAVE) {
         uint64_t prefix = 0;
         if (tile == 0) {
@@ -1337,30 +1369,43 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
     if (word) ybits[w] = 0u;
     const int64_t base_pos = (int64_t)s_prefix;
     const int64_t row0 = (int64_t)tile * FIN_WORDS * 32;
-#pragma unroll 4
-    for (int r = 0; r < 32; ++r) {
-        const int lr = r * TPB + threadIdx.x;  // row within the tile
-        const uint32_t wd = s_word[lr >> 5];
-        const uint32_t bit = lr & 31;
-        if (!((wd >> bit) & 1u)) continue;
-        const int64_t pos = base_pos + s_wpos[lr >> 5] + __popc(wd & ((1u << bit) - 1u));
-        const int64_t i = row0 + lr;
-        y_idx[pos] = (int32_t)i;
-        if constexpr (MODE == M_F32) {
-            ((float *)y_val)[pos] = (float)yacc[i];
-            yacc[i] = 0.0;
+    // up to 16 rounds at a time: the accumulator loads of all go out together
+    constexpr int FB = FIN_ROUNDS < 16 ? FIN_ROUNDS : 16;
+    for (int r0 = 0; r0 < FIN_ROUNDS; r0 += FB) {
+        double v[FB];
+        uint32_t hm = 0;
+#pragma unroll
+        for (int u = 0; u < FB; ++u) {
+            const int lr = (r0 + u) * TPB + threadIdx.x;  // row within the tile
+            const uint32_t wd = s_word[lr >> 5];
+            const bool h = (wd >> (lr & 31)) & 1u;
+            hm |= (h ? 1u : 0u) << u;
+            v[u] = (valued<MODE>() && h) ? yacc[row0 + lr] : 0.0;
         }
-        if constexpr (MODE == M_F16) {
-            ((uint16_t *)y_val)[pos] = f64_to_f16_rne(yacc[i]);
-            yacc[i] = 0.0;
+#pragma unroll
+        for (int u = 0; u < FB; ++u) {
+            if (!((hm >> u) & 1u)) continue;
+            const int lr = (r0 + u) * TPB + threadIdx.x;
+            const uint32_t wd = s_word[lr >> 5];
+            const uint32_t bit = lr & 31;
+            const int64_t pos = base_pos + s_wpos[lr >> 5] + __popc(wd & ((1u << bit) - 1u));
+            const int64_t i = row0 + lr;
+            y_idx[pos] = (int32_t)i;
+            if constexpr (MODE == M_F32) ((float *)y_val)[pos] = (float)v[u];
+            if constexpr (MODE == M_F16) ((uint16_t *)y_val)[pos] = f64_to_f16_rne(v[u]);
+            if constexpr (valued<MODE>()) yacc[i] = 0.0;
         }
     }
     if (tile == (int)gridDim.x - 1 && threadIdx.x == 0) {
         int32_t tot = (int32_t)(s_prefix + total);
         *y_nnz = tot;
         counters[C_YNNZ] = tot;
-        counters[C_ERR_LAST] = counters[C_ERR];
-        counters[C_ERR] = 0;
+        // out-of-range indices were counted by the blocker; fewer stored
+        // entries than valid indices means a duplicate
+        const int32_t bad = counters[C_XBAD], pop = counters[C_XPOP];
+        counters[C_ERR_LAST] = (bad ? 1 : 0) | (pop < k - bad ? 2 : 0);
+        counters[C_XBAD] = 0;
+        counters[C_XPOP] = 0;
     }
     (void)m;
 }
@@ -1391,8 +1436,9 @@ __global__ __launch_bounds__(TPB) void k_finalize_dense(double *__restrict__ yac
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         counters[C_YNNZ] = m;
-        counters[C_ERR_LAST] = counters[C_ERR];
-        counters[C_ERR] = 0;
+        counters[C_ERR_LAST] = 0;
+        counters[C_XBAD] = 0;
+        counters[C_XPOP] = 0;
     }
 }
 
@@ -1413,7 +1459,6 @@ __global__ __launch_bounds__(TPB) void k_bfs_init(int32_t n, int32_t source, int
     }
     const int32_t sw = source >> 5;
     const uint32_t sb = 1u << (source & 31);
-    if (blockIdx.x == 0 && threadIdx.x == 0) counters[C_NZACC] = 1;  // the source's vector block
     for (int64_t w = (int64_t)blockIdx.x * TPB + threadIdx.x; w < nwords; w += stride) {
         visited[w] = w == sw ? sb : 0u;
         xmask[w] = w == sw ? sb : 0u;
@@ -1431,7 +1476,9 @@ __global__ __launch_bounds__(TPB) void k_bfs_update(int32_t nwords, int32_t next
                                                     int32_t *__restrict__ counters)
 {
     int32_t w = blockIdx.x * TPB + threadIdx.x;
-    uint32_t cnt = 0, blocks = 0;
+    uint32_t cnt = 0;
+    // the scan's entry count is not used by BFS
+    if (w == 0) counters[C_XPOP] = 0;
     if (w < nwords) {
         uint32_t nm = nextm[w];
         xmask[w] = nm;
@@ -1439,7 +1486,6 @@ __global__ __launch_bounds__(TPB) void k_bfs_update(int32_t nwords, int32_t next
             visited[w] |= nm;
             nextm[w] = 0u;
             cnt = __popc(nm);
-            blocks = ((nm & 0xFFFFu) != 0) + ((nm >> 16) != 0);
             while (nm) {
                 int b = ctz32(nm);
                 nm &= nm - 1;
@@ -1447,11 +1493,8 @@ __global__ __launch_bounds__(TPB) void k_bfs_update(int32_t nwords, int32_t next
             }
         }
     }
-    const uint32_t tot = wave_sum(cnt), totb = wave_sum(blocks);
-    if (lane_id() == 0 && tot) {
-        atomicAdd(&counters[C_FRONTIER], (int32_t)tot);
-        atomicAdd(&counters[C_NZACC], (int32_t)totb);
-    }
+    const uint32_t tot = wave_sum(cnt);
+    if (lane_id() == 0 && tot) atomicAdd(&counters[C_FRONTIER], (int32_t)tot);
 }
 
 __global__ __launch_bounds__(TPB) void k_bfs_finish(int32_t n, int32_t *__restrict__ parent)
@@ -1589,6 +1632,9 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
     default: return launch_paths<M_BFS>(A, a, forced_path, s);
     }
 }
+
+int32_t scan_tiles(int32_t nbc) { return (nbc + SCAN_TILE - 1) / SCAN_TILE; }
+int32_t finalize_tiles(int32_t nbr) { return ((nbr + 1) / 2 + FIN_WORDS - 1) / FIN_WORDS; }
 
 hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_idx, void *y_val,
                            int32_t *y_nnz, const int32_t *x_idx, int32_t k, hipStream_t s)

@@ -35,14 +35,26 @@ enum Counter : int {
     C_TASKS = 1,     // push block tasks (sum of block-CSC lengths of active columns)
     C_PATH = 2,      // 1 push, 2 pull
     C_YNNZ = 3,      // entries written to y
-    C_ERR = 4,       // error bits raised by the blocker during this call
+    C_XBAD = 4,      // x indices out of range, counted by the blocker during this call
     C_ERR_LAST = 5,  // error bits of the last completed call
     C_FRONTIER = 6,  // BFS: vertices in the next frontier
-    C_NZACC = 7,     // nonzero vector blocks counted by the blocker (consumed by the scan)
+    C_NZACC = 7,     // nonzero vector blocks, summed by the scan tiles (consumed by its last tile)
     C_NTB = 8,       // push work items (nonzero vector blocks with a nonempty block column)
+    C_XPOP = 9,      // distinct x indices (mask popcounts), summed by the scan tiles
     C_COUNT = 12
 };
 constexpr int PATH_PUSH = 1, PATH_PULL = 2;
+
+// Tile sizes of the look-back scans (vector blocks per thread of the active
+// block scan; 32-row structure words per workgroup of the y compaction).
+#ifndef SCAN_ITEMS_PER_THREAD
+#define SCAN_ITEMS_PER_THREAD 4
+#endif
+#ifndef FINALIZE_WORDS
+#define FINALIZE_WORDS 64
+#endif
+int32_t scan_tiles(int32_t nbc);      // workgroups (and status words) of the scan
+int32_t finalize_tiles(int32_t nbr);  // workgroups (and status words) of the compaction
 
 // Per-context scratch.  Every buffer is sized for the largest matrix the
 // context was created for and is all-zero between calls (each call clears
