@@ -34,7 +34,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 DENSITIES = [1e-4, 1e-3, 1e-2, 1e-1]
 KINDS = ["uniform", "clustered"]
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "main_rmat20_sweep_traffic.md")
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traverse_rmat20_sweep_traffic.md")
 
 
 def log(*a):
