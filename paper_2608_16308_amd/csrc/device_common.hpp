@@ -51,13 +51,56 @@ __device__ __forceinline__ uint32_t wave_or(uint32_t v)
     return v;
 }
 
+// Cross-lane moves by DPP (data-parallel primitives of the GFX9 vector ALU):
+// no LDS round trip and no per-pattern address register, unlike shuffles.
+// A lane whose source is outside its row (or the wave) receives `old`.
+namespace dppc {
+constexpr int ROW_SHR = 0x110;    // + n: lane i of a 16-lane row reads lane i - n of the row
+constexpr int ROW_ROR = 0x120;    // + n: rotate right within the row
+constexpr int WF_SR1 = 0x138;     // lane i reads lane i - 1 of the wave
+constexpr int ROW_BCAST15 = 0x142;  // lane 15 of each row feeds the next row
+constexpr int ROW_BCAST31 = 0x143;  // lane 31 feeds rows 2 and 3
+}  // namespace dppc
+
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t old, uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROW_MASK, 0xF, false);
+}
+
+// Inclusive scans over the 64 lanes (Hillis-Steele inside each row, then the
+// two row broadcasts).
+__device__ __forceinline__ uint32_t wave_incl_add(uint32_t v)
+{
+    v += dpp_mov<dppc::ROW_SHR + 1>(0u, v);
+    v += dpp_mov<dppc::ROW_SHR + 2>(0u, v);
+    v += dpp_mov<dppc::ROW_SHR + 4>(0u, v);
+    v += dpp_mov<dppc::ROW_SHR + 8>(0u, v);
+    v += dpp_mov<dppc::ROW_BCAST15, 0xA>(0u, v);
+    v += dpp_mov<dppc::ROW_BCAST31, 0xC>(0u, v);
+    return v;
+}
+__device__ __forceinline__ uint32_t wave_incl_max(uint32_t v)
+{
+    v = max(v, dpp_mov<dppc::ROW_SHR + 1>(0u, v));
+    v = max(v, dpp_mov<dppc::ROW_SHR + 2>(0u, v));
+    v = max(v, dpp_mov<dppc::ROW_SHR + 4>(0u, v));
+    v = max(v, dpp_mov<dppc::ROW_SHR + 8>(0u, v));
+    v = max(v, dpp_mov<dppc::ROW_BCAST15, 0xA>(0u, v));
+    v = max(v, dpp_mov<dppc::ROW_BCAST31, 0xC>(0u, v));
+    return v;
+}
+// The value of lane i - 1 (0 for lane 0).
+__device__ __forceinline__ uint32_t wave_shr1(uint32_t v) { return dpp_mov<dppc::WF_SR1>(0u, v); }
+
 __device__ __forceinline__ uint32_t or16_in_quarter(uint32_t v)
 {
-    // OR over the 16 lanes of this lane's quarter-wave.
-    v |= __shfl_xor(v, 1, WAVE);
-    v |= __shfl_xor(v, 2, WAVE);
-    v |= __shfl_xor(v, 4, WAVE);
-    v |= __shfl_xor(v, 8, WAVE);
+    // OR over the 16 lanes of this lane's quarter-wave (a DPP row): rotations
+    // by 1, 2, 4 and 8 leave the OR of the whole row in every lane.
+    v |= dpp_mov<dppc::ROW_ROR + 1>(0u, v);
+    v |= dpp_mov<dppc::ROW_ROR + 2>(0u, v);
+    v |= dpp_mov<dppc::ROW_ROR + 4>(0u, v);
+    v |= dpp_mov<dppc::ROW_ROR + 8>(0u, v);
     return v;
 }
 

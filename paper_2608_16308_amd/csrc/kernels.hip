@@ -723,6 +723,14 @@ __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int l)
     return ((uint64_t)hi << 32) | lo;
 }
 
+// Entries per lane in one window of the entry-parallel pass (a window is
+// FLAT_E * 64 consecutive entries; lane l takes entries FLAT_E l .. FLAT_E l
+// + FLAT_E - 1), so that FLAT_E record loads, then FLAT_E x gathers, are in
+// flight per lane.
+constexpr int FLAT_E = 4;
+constexpr int FLAT_W = FLAT_E * WAVE;
+static_assert(FLAT_E == 4, "the mark reads below take 4 marks per lane");
+
 // Blocks staged for whole-wave processing: slot-major, one entry per lane
 // (entry k * 64 + lane for slot k).  After an entry is processed its J word
 // carries the rows hit back to the lane that staged it.  Stored COO blocks
@@ -735,7 +743,7 @@ struct HeavyStage {
     uint64_t d[SLOTS * WAVE];
     int32_t J[SLOTS * WAVE];      // block column; rows hit once processed
     uint32_t mxam[SLOTS * WAVE];  // vector-block mask | admitted rows << 16
-    int32_t mark[WAVE];           // entry-parallel pass: owner starting at each lane's entry
+    alignas(8) uint16_t mark[FLAT_W];  // entry-parallel pass: 1 + block starting at each window entry
     uint32_t hitw[PUSH ? SLOTS * WAVE : SLOTS * 4];  // entry-parallel pass: rows hit per block
                                                      // (push) or per slot quarter (pull)
     int32_t R[PUSH ? SLOTS * WAVE : 1];
@@ -758,77 +766,95 @@ __device__ __forceinline__ uint64_t flat_word(uint64_t d, uint32_t excl)
     return (desc_off(d) << 25) | ((uint64_t)(desc_nnz(d) - 1) << 17) | excl;
 }
 
-// One lane's entry of a window of the entry-parallel pass.
-struct FlatEntry {
-    int32_t o;      // staging entry (slot * 64 + lane) of the block
-    int32_t J;      // its block column
-    uint32_t mxam;  // its vector-block mask (when staged) | admitted rows << 16
-    uint32_t cd;    // coordinate byte (row << 4 | column)
-    float val;      // value (valued modes)
-    bool valid;
+
+// One lane's entries of a window (the block's column and masks are read
+// again from the staging area when the entry is finished).
+struct FlatEntries {
+    uint32_t ocd[FLAT_E];   // staging entry of the block (slot * 64 + lane) << 8 | coordinate byte;
+                            // bit 31: valid
+    float val[FLAT_E];      // value (valued modes)
 };
 
-// Finds the block of entry base + lane and issues its coordinate and value
-// loads.
+// Finds the blocks of this lane's entries of the window starting at base
+// and issues their coordinate and value loads.  carry: 1 + the block of the
+// last entry of the previous window.
 template <int MODE, bool PUSH>
-__device__ __forceinline__ FlatEntry flat_issue(const MainArgs &a, HeavyStage<PUSH> *hs,
-                                                const uint32_t (&cnt)[SLOTS], const uint32_t (&excl)[SLOTS],
-                                                uint32_t tot, uint32_t base, int32_t &carry)
+__device__ __forceinline__ FlatEntries flat_issue(const MainArgs &a, HeavyStage<PUSH> *hs,
+                                                  const uint32_t (&cnt)[SLOTS], const uint32_t (&excl)[SLOTS],
+                                                  uint32_t tot, uint32_t base, uint32_t &carry)
 {
     const int lane = lane_id();
-    hs->mark[lane] = -1;
+    // marks: 1 + block index at the window position of each block's first entry
+    *(uint64_t *)&hs->mark[lane * FLAT_E] = 0ull;
     wave_lds_sync();
 #pragma unroll
     for (int k = 0; k < SLOTS; ++k)
-        if (cnt[k] && excl[k] >= base && excl[k] < base + WAVE) hs->mark[excl[k] - base] = k * WAVE + lane;
+        if (cnt[k] && excl[k] >= base && excl[k] < base + FLAT_W)
+            hs->mark[excl[k] - base] = (uint16_t)(k * WAVE + lane + 1);
     wave_lds_sync();
-    int32_t o = hs->mark[lane];
+    const uint64_t mw = *(const uint64_t *)&hs->mark[lane * FLAT_E];
+    uint32_t m[FLAT_E];
 #pragma unroll
-    for (int st = 1; st < WAVE; st <<= 1) {
-        const int32_t v = __shfl_up(o, st, WAVE);
-        if (lane >= st) o = max(o, v);
+    for (int j = 0; j < FLAT_E; ++j) m[j] = (uint32_t)(mw >> (16 * j)) & 0xFFFFu;
+#pragma unroll
+    for (int j = 1; j < FLAT_E; ++j) m[j] = max(m[j], m[j - 1]);
+    // blocks start in ascending entry order: the block of an entry is the
+    // largest mark at or before it (max-scan over the lanes, then carry)
+    const uint32_t inc = wave_incl_max(m[FLAT_E - 1]);
+    const uint32_t cin = max(wave_shr1(inc), carry);
+    carry = max(carry, readlane_u32(inc, WAVE - 1));
+    FlatEntries f;
+#pragma unroll
+    for (int j = 0; j < FLAT_E; ++j) {
+        const uint32_t g = base + (uint32_t)(lane * FLAT_E + j);
+        const bool valid = g < tot;
+        const uint32_t own = max(cin, m[j]);
+        const uint32_t o = own ? own - 1 : 0u;
+        const uint64_t w = hs->d[o];
+        const uint64_t off = w >> 25;
+        const uint32_t nnz = (uint32_t)((w >> 17) & 0xFFu) + 1u, e = g - (uint32_t)(w & 0x1FFFFu);
+        const uint32_t cd = valid ? a.pay[off + (uint64_t)a.vb * nnz + e] : 0u;
+        f.ocd[j] = (valid ? 0x80000000u : 0u) | (o << 8) | cd;
+        f.val[j] = 0.f;
+        if constexpr (valued<MODE>()) f.val[j] = valid ? VT<MODE>::load(a.pay + off, e) : 0.f;
     }
-    if (o < 0) o = carry;
-    carry = __shfl(o, WAVE - 1, WAVE);
-    FlatEntry f;
-    const uint32_t g = base + (uint32_t)lane;
-    f.valid = g < tot;
-    f.o = o;
-    const uint64_t w = hs->d[o];
-    f.J = hs->J[o];
-    f.mxam = hs->mxam[o];
-    const uint64_t off = w >> 25;
-    const uint32_t nnz = (uint32_t)((w >> 17) & 0xFFu) + 1u, e = g - (uint32_t)(w & 0x1FFFFu);
-    f.cd = f.valid ? a.pay[off + (uint64_t)a.vb * nnz + e] : 0u;
-    f.val = 0.f;
-    if constexpr (valued<MODE>()) f.val = f.valid ? VT<MODE>::load(a.pay + off, e) : 0.f;
     return f;
 }
 
-// Gathers x for the entry and adds its product (see flat_pass).  MXK: the
-// staged word holds the block's vector-block mask, which then answers the
-// boolean modes' presence test without a gather.
+// Gathers x for the entries and adds their products (see flat_pass).  MXK:
+// the staged word holds the block's vector-block mask, which then answers
+// the boolean modes' presence test without a gather.
 template <int MODE, bool PUSH, bool MXK>
-__device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> *hs, const FlatEntry &f,
+__device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> *hs, FlatEntries f,
                                             float *sy, int32_t *sp)
 {
-    const uint32_t r = f.cd >> 4, c = f.cd & 15u;
-    const bool adm = f.valid && ((f.mxam >> (16 + r)) & 1u);
     constexpr bool known = MXK && !valued<MODE>();
-    const uint32_t raw = (adm && !known) ? x_gather<MODE>(a, f.J, c) : 0u;
-    const bool present = known ? ((f.mxam >> c) & 1u) != 0 : x_present<MODE>(raw, f.J, c);
-    if (adm && present) {
-        const int o = f.o, ko = o >> 6, lo = o & (WAVE - 1);
-        if constexpr (PUSH) {
-            const int64_t row = (int64_t)hs->R[o] * BS + r;
-            if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], (double)(f.val * x_value<MODE>(raw)));
-            if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], f.J * BS + (int32_t)c);
-            atomicOr(&hs->hitw[o], 1u << r);
-        } else {
-            const int at = ko * WAVE + (lo >> 4) * 16 + (int)r;
-            if constexpr (valued<MODE>()) atomicAdd(&sy[at], f.val * x_value<MODE>(raw));
-            if constexpr (MODE == M_BFS) atomicMin(&sp[at], f.J * BS + (int32_t)c);
-            atomicOr(&hs->hitw[ko * 4 + (lo >> 4)], 1u << r);
+    uint32_t raw[FLAT_E];
+#pragma unroll
+    for (int j = 0; j < FLAT_E; ++j) {
+        const uint32_t o = (f.ocd[j] >> 8) & 0xFFu, r = (f.ocd[j] >> 4) & 15u, c = f.ocd[j] & 15u;
+        const bool adm = (f.ocd[j] >> 31) && ((hs->mxam[o] >> (16 + r)) & 1u);
+        raw[j] = (adm && !known) ? x_gather<MODE>(a, hs->J[o], c) : 0u;
+        if (!adm) f.ocd[j] = 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < FLAT_E; ++j) {
+        const uint32_t o = (f.ocd[j] >> 8) & 0xFFu, r = (f.ocd[j] >> 4) & 15u, c = f.ocd[j] & 15u;
+        const int32_t J = hs->J[o];
+        const bool present = known ? ((hs->mxam[o] >> c) & 1u) != 0 : x_present<MODE>(raw[j], J, c);
+        if ((f.ocd[j] >> 31) && present) {
+            const int ko = (int)(o >> 6), lo = (int)(o & (WAVE - 1));
+            if constexpr (PUSH) {
+                const int64_t row = (int64_t)hs->R[o] * BS + r;
+                if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], (double)(f.val[j] * x_value<MODE>(raw[j])));
+                if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], J * BS + (int32_t)c);
+                atomicOr(&hs->hitw[o], 1u << r);
+            } else {
+                const int at = ko * WAVE + (lo >> 4) * 16 + (int)r;
+                if constexpr (valued<MODE>()) atomicAdd(&sy[at], f.val[j] * x_value<MODE>(raw[j]));
+                if constexpr (MODE == M_BFS) atomicMin(&sp[at], J * BS + (int32_t)c);
+                atomicOr(&hs->hitw[ko * 4 + (lo >> 4)], 1u << r);
+            }
         }
     }
 }
@@ -836,11 +862,11 @@ __device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> 
 // Entry-parallel pass over the stored COO blocks of one wave iteration
 // (Sec. 3.3.3's COO microkernel, re-mapped to wave64).  The entries of the
 // blocks staged with cnt[k] > 0 are numbered in slot-major order by wave
-// prefix sums; the wave walks them 64 at a time, one entry per lane.  Each
-// round, the blocks that start inside the window mark their first entry;
-// a max-scan over the lanes then gives every lane the block of its entry
-// (blocks start in ascending entry order).  The coordinate and value loads
-// of all lanes go out together, then the x gathers.
+// prefix sums; the wave walks them FLAT_W at a time, FLAT_E consecutive
+// entries per lane.  Each window, the blocks that start inside it mark their
+// first entry; a max-scan over the marks then gives every lane the blocks of
+// its entries (blocks start in ascending entry order).  The coordinate and
+// value loads of all lanes go out together, then the x gathers.
 //   pull: products are added to the owner's quarter of its slot's LDS rows;
 //         BFS keeps the smallest active column per row there; rows hit are
 //         collected per slot quarter in hitw[slot * 4 + quarter].
@@ -855,14 +881,9 @@ __device__ void flat_pass(const MainArgs &a, HeavyStage<PUSH> *hs, const uint32_
     uint32_t tot = 0;
 #pragma unroll
     for (int k = 0; k < SLOTS; ++k) {
-        uint32_t incl = cnt[k];
-#pragma unroll
-        for (int o = 1; o < WAVE; o <<= 1) {
-            const uint32_t v = (uint32_t)__shfl_up((int)incl, o, WAVE);
-            if (lane >= o) incl += v;
-        }
+        const uint32_t incl = wave_incl_add(cnt[k]);
         excl[k] = tot + incl - cnt[k];
-        tot += (uint32_t)__shfl((int)incl, WAVE - 1, WAVE);
+        tot += readlane_u32(incl, WAVE - 1);
     }
 #pragma unroll
     for (int k = 0; k < SLOTS; ++k)
@@ -873,13 +894,13 @@ __device__ void flat_pass(const MainArgs &a, HeavyStage<PUSH> *hs, const uint32_
     } else {
         if (lane < SLOTS * 4) hs->hitw[lane] = 0u;
     }
-    int32_t carry = 0;
+    uint32_t carry = 0;
     // the first window is peeled: its record loads are in flight while the
     // caller's inline products are formed
-    FlatEntry f = flat_issue<MODE, PUSH>(a, hs, cnt, excl, tot, 0u, carry);
+    FlatEntries f = flat_issue<MODE, PUSH>(a, hs, cnt, excl, tot, 0u, carry);
     between();
     flat_finish<MODE, PUSH, MXK>(a, hs, f, sy, sp);
-    for (uint32_t base = WAVE; base < tot; base += WAVE) {
+    for (uint32_t base = FLAT_W; base < tot; base += FLAT_W) {
         f = flat_issue<MODE, PUSH>(a, hs, cnt, excl, tot, base, carry);
         flat_finish<MODE, PUSH, MXK>(a, hs, f, sy, sp);
     }
