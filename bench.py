@@ -63,6 +63,107 @@ def read_traffic(digest: str):
     return None
 
 
+def _time_call(torch, fn, reps):
+    """Mean microseconds of fn() over reps back-to-back calls (HIP events on
+    torch's current stream, which the library's context uses)."""
+    for _ in range(3):
+        fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / reps
+
+
+def run_ablation(args, torch, dbs, wl, dev):
+    """Paper Sec. 5 style ablations on the synthetic R-MAT matrices: (1) the
+    push / pull crossover over a finer density grid, as a function of
+    s_b = N_nzblk / N_blk (the quantity the global selector thresholds,
+    Sec. 3.3.1); (2) forced block formats (all COO, all patched CSR) against
+    the classifier's choice (Sec. 3.2.1); (3) BFS with candidate th3."""
+    out = {"ablation": True, "scale": args.scale}
+    a = wl.rmat(args.scale)
+    log(f"[ablation] R-MAT {args.scale}: n={a.n} nnz={a.nnz}")
+    m = a.m
+    y_idx = torch.empty(m, dtype=torch.int32, device=dev)
+    y_val = torch.empty(m, dtype=torch.float32, device=dev)
+    y_nnz = torch.zeros(1, dtype=torch.int32, device=dev)
+    dens = [1e-4, 2e-4, 5e-4, 1e-3, 2e-3, 5e-3, 1e-2, 2e-2, 5e-2, 1e-1]
+
+    def sweep(A, ctx, densities, kinds, paths):
+        rows = []
+        for di, d in enumerate(densities):
+            for kind in kinds:
+                xi, xv = wl.sparse_x(a.n, d, kind, key=(21, di, KINDS.index(kind)))
+                dxi, dxv = torch.from_numpy(xi).to(dev), torch.from_numpy(xv).to(dev)
+                st = ctx.spmspv_raw(A, dxi, dxv, y_idx, y_val, y_nnz, path="push", stats=True)
+                row = {"density": d, "x": kind, "k": int(xi.size), "n_nzblk": st["n_nzblk"],
+                       "s_b": round(st["n_nzblk"] / st["n_blk"], 5), "push_tasks": st["tasks"]}
+                for path in paths:
+                    row[f"{path}_us"] = round(_time_call(
+                        torch, lambda: ctx.spmspv_raw(A, dxi, dxv, y_idx, y_val, y_nnz, path=path), 10), 1)
+                rows.append(row)
+                log(f"[ablation] {row}")
+        return rows
+
+    # (1) crossover
+    A = dbs.Matrix.from_csr(a.m, a.n, a.row_ptr, a.col_idx, a.vals)
+    ctx = dbs.Context(A)
+    rows = sweep(A, ctx, dens, KINDS, ("push", "pull"))
+    cross = {}
+    for kind in KINDS:
+        rk = [r for r in rows if r["x"] == kind]
+        c = None
+        for r0, r1 in zip(rk, rk[1:]):
+            if r0["push_us"] <= r0["pull_us"] and r1["push_us"] > r1["pull_us"]:
+                # interpolate log(push/pull) = 0 in log s_b
+                import math
+                l0, l1 = math.log(r0["push_us"] / r0["pull_us"]), math.log(r1["push_us"] / r1["pull_us"])
+                s0, s1 = math.log(max(r0["s_b"], 1e-9)), math.log(max(r1["s_b"], 1e-9))
+                c = round(math.exp(s0 + (s1 - s0) * (-l0) / (l1 - l0)), 4)
+                break
+        cross[kind] = c
+    out["path_crossover"] = {"rows": rows, "crossover_s_b": cross}
+    log(f"[ablation] push/pull crossover in s_b: {cross}")
+    del ctx, A
+
+    # (2) forced formats (all blocks COO / all patched CSR / classifier)
+    fmt = {}
+    for name, force in (("classifier", -1), ("coo_only", 0), ("csr_only", 4)):
+        opts = dbs.default_opts() if force < 0 else dbs.default_opts(force_type=force)
+        A = dbs.Matrix.from_csr(a.m, a.n, a.row_ptr, a.col_idx, a.vals, opts)
+        ctx = dbs.Context(A)
+        info = A.info()
+        fmt[name] = {"blocks_by_type": info["blocks_by_type"], "payload_MB": round(info["payload_bytes"] / 1e6, 1),
+                     "rows": sweep(A, ctx, [1e-3, 1e-2, 1e-1], ["uniform"], ("push", "pull"))}
+        del ctx, A
+    out["formats"] = fmt
+
+    # (3) BFS under candidate th3
+    if args.bfs_scale > 0:
+        g = wl.rmat(args.bfs_scale, values=False)
+        srcs = wl.bfs_sources(g, min(args.bfs_sources, 8), key=0)
+        G = dbs.Matrix.from_csr(g.m, g.n, g.row_ptr, g.col_idx, None)
+        gctx = dbs.Context(G)
+        level = torch.empty(g.n, dtype=torch.int32, device=dev)
+        parent = torch.empty(g.n, dtype=torch.int32, device=dev)
+        bfs = []
+        for th3 in (0.01, 0.02, 0.05, 0.1):
+            ms = []
+            for s0 in srcs:
+                gctx.bfs(G, int(s0), level=level, parent=parent, th3=th3)
+                ms.append(_time_call(torch, lambda: gctx.bfs(G, int(s0), level=level, parent=parent, th3=th3), 3) / 1e3)
+            bfs.append({"th3": th3, "ms_mean": round(float(np.mean(ms)), 3)})
+            log(f"[ablation] BFS th3={th3}: {bfs[-1]}")
+        out["bfs_th3"] = bfs
+    print(json.dumps(out), flush=True)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            json.dump(out, f)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -74,6 +175,10 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--point-reps", type=int, default=20)
     ap.add_argument("--json-out", default=None)
+    ap.add_argument("--ablation", action="store_true",
+                    help="path / format / selector ablation on R-MAT (no bench line): push vs pull over a "
+                         "finer density grid, the crossover in s_b = N_nzblk / N_blk, forced block formats, "
+                         "and BFS under candidate th3 values")
     ap.add_argument("--profile-run", action="store_true",
                     help="short run for rocprofv3 counter passes: a 1 GiB device copy (counter "
                          "calibration) then warm-up + timed steps of the sweep only")
@@ -92,6 +197,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
+    if args.ablation:
+        run_ablation(args, torch, dbs, wl, dev)
+        return
     if args.profile_run:
         # plain copy of known size: 1 GiB read + 1 GiB written per launch
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
@@ -139,6 +247,7 @@ def main():
     step_bytes = sum(p["model"]["bytes_total"] for p in points)
     step_main_bytes = sum(p["model"]["bytes_main"] for p in points)
     step_useful = sum(p["model"]["useful_nnz"] for p in points)
+    step_comp = sum(p["model"]["bytes_compulsory"] for p in points)
 
     # ------------------------------------------------------------ timed steps
     for _ in range(args.warmup):
@@ -183,7 +292,8 @@ def main():
     for p in points:
         row = {"density": p["density"], "x": p["kind"], "k": p["model"]["k"], "path": p["path"],
                "n_nzblk": p["model"]["n_nzblk"], "useful_nnz": p["model"]["useful_nnz"],
-               "y_nnz": p["model"]["y_nnz"], "bytes": p["model"]["bytes_total"]}
+               "y_nnz": p["model"]["y_nnz"], "bytes": p["model"]["bytes_total"],
+               "compulsory_bytes": p["model"]["bytes_compulsory"]}
         for path in ("auto", "push", "pull"):
             mod = p["model"] if path == "auto" else model.call(p["x_idx"], path)
             ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -229,13 +339,19 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"rmat{args.scale}_spmspv_density_sweep", "scale": args.scale,
                    "edge_factor": 16, "n": a.n, "nnz": a.nnz, "densities": DENSITIES, "x_kinds": KINDS,
-                   "calls_per_step": len(points), "semiring": "plus_times", "path": "auto", "th3": 0.01,
+                   "calls_per_step": len(points), "semiring": "plus_times", "path": "auto", "th3": 0.05,
                    "nblk": info["nblk"], "db_build_s": round(build_s, 2),
                    "useful_GFLOPs": round(2 * step_useful * args.steps / elapsed / 1e9, 2)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_traffic(kernel_sources_digest()),
                      "kernel": "k_main (push/pull traversal)", "avg_launch_us": round(main_avg_ms * 1e3, 2),
                      "algorithmic_bytes_per_launch": round(step_main_bytes / len(points))},
+        # path-independent view: the compulsory bytes (every stored entry of
+        # the active columns, its x value and the y output) per second; the
+        # model bytes depend on the path taken (push touches fewer)
+        "compulsory": {"bytes_per_step": int(step_comp),
+                       "GBs": round(step_comp * args.steps / elapsed / 1e9, 2),
+                       "model_over_compulsory": round(step_bytes / step_comp, 3)},
         "cpu_baseline": {"value": round(cpu_value, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
                          "sample": f"{reps} passes over the same 8 x vectors on R-MAT {args.scale} "
                                    f"({cpu_s:.1f} s, CSC built once outside the timing)"},

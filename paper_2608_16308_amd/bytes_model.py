@@ -87,18 +87,23 @@ class BytesModel:
         em = xact[self.ec]
         eb_m = self.eb[em]
         match_b = np.bincount(eb_m, minlength=self.nblk)
-        popc_b = _POPC16[mx_b]
         t = self.btype
+        # record bytes the kernels read per active block: stored COO blocks and,
+        # in push, every format are taken entry-parallel (all coordinates and
+        # values; the 48-byte mask + start header for the non-COO formats, 32
+        # bytes of row masks for Dense); pull takes Dense with 4 lanes per row
+        # (masks + all 256 values) and the other formats entry-parallel.
         rec = np.zeros(self.nblk, dtype=np.int64)
+        nnz_b = self.bnnz
         sel = act_b & (t == COO) & ~self.binline   # inline blocks live in the descriptor
-        rec[sel] = self.bnnz[sel] + V * match_b[sel]
+        rec[sel] = (1 + V) * nnz_b[sel]
+        sel = act_b & ((t == FCSR) | (t == FCSC) | (t == CSR))
+        rec[sel] = 48 + V * nnz_b[sel]
         sel = act_b & (t == DENSE)
         rec[sel] = 32 + 256 * V
-        sel = act_b & ((t == FCSR) | (t == FCSC) | ((t == CSR) & (popc_b >= 8)))
-        rec[sel] = 48 + V * match_b[sel]
-        sel = act_b & (t == CSR) & (popc_b < 8)
-        rec[sel] = 64 + (1 + V) * match_b[sel]
-        rec_bytes = int(rec.sum())
+        rec_pull = int(rec.sum())
+        rec[sel] = 32 + V * nnz_b[sel]
+        rec_push = int(rec.sum())
         nact_blocks = int(act_b.sum())
         # y structure
         row_key_blk = np.unique(eb_m * 16 + self.er_local[em])
@@ -112,9 +117,9 @@ class BytesModel:
         blocker = k * (4 + V) + k * V + 4 * k
         scan = 2 * self.nbc + 16 * N
         if path == "push":
-            main = 16 * N + nact_blocks * (4 + 4 + 8) + rec_bytes + 8 * blk_rows + 4 * blks_hit
+            main = 16 * N + nact_blocks * (4 + 4 + 8) + rec_push + 8 * blk_rows + 4 * blks_hit
         else:
-            main = 4 * self.nseg + 64 * self.nseg + 2 * self.nblk + 8 * nact_blocks + rec_bytes \
+            main = 4 * self.nseg + 64 * self.nseg + 2 * self.nblk + 8 * nact_blocks + rec_pull \
                 + 8 * seg_rows + 4 * segs_hit
         main += V * k
         finalize = 2 * self.nbr + y_nnz * (8 + 8 + 4 + V) + 4 * N

@@ -390,7 +390,7 @@ extern "C" dbs_status dbs_ctx_read_timing(dbs_ctx *ctx, dbs_timing *out)
 // ---------------------------------------------------------------------------
 // SpMSpV
 // ---------------------------------------------------------------------------
-static float norm_th3(float th3) { return th3 > 0.f ? th3 : 0.01f; }
+static float norm_th3(float th3) { return th3 > 0.f ? th3 : DBS_TH3_DEFAULT; }
 
 extern "C" dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring sr, int32_t x_nnz,
                                  const int32_t *d_x_idx, const void *d_x_val, const uint32_t *d_mask,

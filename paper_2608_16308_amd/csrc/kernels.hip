@@ -507,6 +507,40 @@ __device__ __forceinline__ void hdr_locate(const Hdr16 &h, uint32_t e, uint32_t 
     other = nth_bit16(gm, e - gs);
 }
 
+// Entry e (row-major; column-major for ForceCSC) of a Dense, ForceCSR,
+// ForceCSC or patched-CSR record: its local row and column and the index of
+// its value in the record's value array.  Dense records hold 16 row masks and
+// all 256 values; the row starts are the prefix sums of the row popcounts.
+__device__ __forceinline__ void hdr_entry(const uint8_t *rec, uint32_t type, uint32_t e, uint32_t &r,
+                                          uint32_t &c, uint32_t &vi)
+{
+    Hdr16 h;
+    const uint4 m0 = ((const uint4 *)(rec + HDR_MASK))[0], m1 = ((const uint4 *)(rec + HDR_MASK))[1];
+    h.m[0] = m0.x; h.m[1] = m0.y; h.m[2] = m0.z; h.m[3] = m0.w;
+    h.m[4] = m1.x; h.m[5] = m1.y; h.m[6] = m1.z; h.m[7] = m1.w;
+    if (type == T_DENSE) {
+        uint32_t acc = 0;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            uint32_t wv = 0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                wv |= acc << (8 * u);
+                acc += __popc(hdr_mask(h, 4 * t + u));
+            }
+            h.s[t] = wv;
+        }
+    } else {
+        const uint4 st = *(const uint4 *)(rec + HDR_START);
+        h.s[0] = st.x; h.s[1] = st.y; h.s[2] = st.z; h.s[3] = st.w;
+    }
+    uint32_t g, o;
+    hdr_locate(h, e, g, o);
+    r = type == T_FCSC ? o : g;
+    c = type == T_FCSC ? g : o;
+    vi = type == T_DENSE ? r * BS + c : e;
+}
+
 template <int MODE>
 __device__ __forceinline__ uint32_t xd_raw(const void *xd, int64_t j)
 {
@@ -754,7 +788,6 @@ struct HeavyStage {
         if constexpr (PUSH) R[e] = r;
         mxam[e] = mx | (am << 16);
     }
-    __device__ __forceinline__ uint32_t hits(int e) const { return (uint32_t)J[e]; }
 };
 
 // Staged word of a stored COO block in the entry-parallel pass: payload
@@ -778,7 +811,7 @@ struct FlatEntries {
 // Finds the blocks of this lane's entries of the window starting at base
 // and issues their coordinate and value loads.  carry: 1 + the block of the
 // last entry of the previous window.
-template <int MODE, bool PUSH>
+template <int MODE, bool PUSH, bool ANYTYPE>
 __device__ __forceinline__ FlatEntries flat_issue(const MainArgs &a, HeavyStage<PUSH> *hs,
                                                   const uint32_t (&cnt)[SLOTS], const uint32_t (&excl)[SLOTS],
                                                   uint32_t tot, uint32_t base, uint32_t &carry)
@@ -813,10 +846,22 @@ __device__ __forceinline__ FlatEntries flat_issue(const MainArgs &a, HeavyStage<
         const uint64_t w = hs->d[o];
         const uint64_t off = w >> 25;
         const uint32_t nnz = (uint32_t)((w >> 17) & 0xFFu) + 1u, e = g - (uint32_t)(w & 0x1FFFFu);
-        const uint32_t cd = valid ? a.pay[off + (uint64_t)a.vb * nnz + e] : 0u;
-        f.ocd[j] = (valid ? 0x80000000u : 0u) | (o << 8) | cd;
+        uint32_t cd = 0;
         f.val[j] = 0.f;
-        if constexpr (valued<MODE>()) f.val[j] = valid ? VT<MODE>::load(a.pay + off, e) : 0.f;
+        const uint32_t type = ANYTYPE ? ((uint32_t)hs->J[o] >> 28) : (uint32_t)T_COO;
+        if (type == T_COO) {
+            cd = valid ? a.pay[off + (uint64_t)a.vb * nnz + e] : 0u;
+            if constexpr (valued<MODE>()) f.val[j] = valid ? VT<MODE>::load(a.pay + off, e) : 0.f;
+        } else if constexpr (ANYTYPE) {
+            // the other formats: locate the entry from the record header
+            if (valid) {
+                uint32_t r, c, vi;
+                hdr_entry(a.pay + off, type, e, r, c, vi);
+                cd = (r << 4) | c;
+                if constexpr (valued<MODE>()) f.val[j] = VT<MODE>::load(a.pay + off + values_at(type, nnz), vi);
+            }
+        }
+        f.ocd[j] = (valid ? 0x80000000u : 0u) | (o << 8) | cd;
     }
     return f;
 }
@@ -834,13 +879,13 @@ __device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> 
     for (int j = 0; j < FLAT_E; ++j) {
         const uint32_t o = (f.ocd[j] >> 8) & 0xFFu, r = (f.ocd[j] >> 4) & 15u, c = f.ocd[j] & 15u;
         const bool adm = (f.ocd[j] >> 31) && ((hs->mxam[o] >> (16 + r)) & 1u);
-        raw[j] = (adm && !known) ? x_gather<MODE>(a, hs->J[o], c) : 0u;
+        raw[j] = (adm && !known) ? x_gather<MODE>(a, hs->J[o] & 0x0FFFFFFF, c) : 0u;
         if (!adm) f.ocd[j] = 0u;
     }
 #pragma unroll
     for (int j = 0; j < FLAT_E; ++j) {
         const uint32_t o = (f.ocd[j] >> 8) & 0xFFu, r = (f.ocd[j] >> 4) & 15u, c = f.ocd[j] & 15u;
-        const int32_t J = hs->J[o];
+        const int32_t J = hs->J[o] & 0x0FFFFFFF;
         const bool present = known ? ((hs->mxam[o] >> c) & 1u) != 0 : x_present<MODE>(raw[j], J, c);
         if ((f.ocd[j] >> 31) && present) {
             const int ko = (int)(o >> 6), lo = (int)(o & (WAVE - 1));
@@ -872,7 +917,7 @@ __device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> 
 //         collected per slot quarter in hitw[slot * 4 + quarter].
 //   push: products go straight to the fp64 accumulators of the owner's
 //         block row; rows hit are collected per block in hitw[entry].
-template <int MODE, bool PUSH, bool MXK, class Between>
+template <int MODE, bool PUSH, bool MXK, bool ANYTYPE, class Between>
 __device__ void flat_pass(const MainArgs &a, HeavyStage<PUSH> *hs, const uint32_t (&cnt)[SLOTS],
                           const uint64_t (&d)[SLOTS], float *sy, int32_t *sp, Between &&between)
 {
@@ -897,56 +942,16 @@ __device__ void flat_pass(const MainArgs &a, HeavyStage<PUSH> *hs, const uint32_
     uint32_t carry = 0;
     // the first window is peeled: its record loads are in flight while the
     // caller's inline products are formed
-    FlatEntries f = flat_issue<MODE, PUSH>(a, hs, cnt, excl, tot, 0u, carry);
+    FlatEntries f = flat_issue<MODE, PUSH, ANYTYPE>(a, hs, cnt, excl, tot, 0u, carry);
     between();
     flat_finish<MODE, PUSH, MXK>(a, hs, f, sy, sp);
     for (uint32_t base = FLAT_W; base < tot; base += FLAT_W) {
-        f = flat_issue<MODE, PUSH>(a, hs, cnt, excl, tot, base, carry);
+        f = flat_issue<MODE, PUSH, ANYTYPE>(a, hs, cnt, excl, tot, base, carry);
         flat_finish<MODE, PUSH, MXK>(a, hs, f, sy, sp);
     }
     wave_lds_sync();
 }
 
-// Processes the staged blocks of the wave one at a time with the whole wave.
-// Pull: the partial row sums go to the owning quarter's LDS accumulators of
-// that slot.  Push: each block's row sums are committed to HBM at once.  The
-// rows hit are handed back through hs->hits to the lane that staged the block.
-template <int MODE, bool PUSH>
-__device__ void run_staged(const MainArgs &a, HeavyStage<PUSH> *hs, const uint64_t (&hv)[SLOTS], float *sy,
-                           int32_t *sp)
-{
-    const int lane = lane_id();
-    for (int k = 0; k < SLOTS; ++k) {
-        uint64_t m = k == 0 ? hv[0] : k == 1 ? hv[1] : k == 2 ? hv[2] : hv[3];
-        while (m) {
-            const int L = ctz64(m);
-            m &= m - 1;
-            const int e = k * WAVE + L;
-            const uint64_t dL = hs->d[e];
-            const int32_t JL = hs->J[e];
-            const uint32_t mxam = hs->mxam[e];
-            float *dst = PUSH ? sy : sy + k * WAVE + (L >> 4) * 16;
-            int32_t *pdst = PUSH ? sp : sp + k * WAVE + (L >> 4) * 16;
-            const uint32_t h = heavy_block<MODE>(a.pay, a.vb, dL, JL, mxam & 0xFFFFu, mxam >> 16, a.xd, dst, pdst);
-            if constexpr (PUSH) {
-                const int32_t RL = hs->R[e];
-                wave_lds_sync();
-                if (lane < 16) {
-                    const int64_t row = (int64_t)RL * BS + lane;
-                    if ((h >> lane) & 1u) {
-                        if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], (double)sy[lane]);
-                        if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], sp[lane]);
-                    }
-                    if constexpr (valued<MODE>()) sy[lane] = 0.f;
-                    if constexpr (MODE == M_BFS) sp[lane] = INT_MAX;
-                }
-                wave_lds_sync();
-            }
-            if (lane == L) hs->J[e] = (int32_t)h;
-        }
-    }
-    wave_lds_sync();
-}
 
 // Pull (Sec. 3.3.2): a quarter-wave per row-block segment (<= 16 blocks,
 // one block per lane); a quarter takes SLOTS consecutive segments per
@@ -1095,7 +1100,7 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
         };
         if (ballot(cnt[0] | cnt[1] | cnt[2] | cnt[3])) {
             wave_lds_sync();
-            flat_pass<MODE, false, !LDSBITS>(a, hs, cnt, d, sy, sp, inline_products);
+            flat_pass<MODE, false, !LDSBITS, false>(a, hs, cnt, d, sy, sp, inline_products);
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k) hit[k] |= hs->hitw[k * 4 + q];
         } else {
@@ -1245,7 +1250,6 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             d[k] = act[k] ? a.sl_desc[bb[k]] : 0ull;
         }
         uint32_t hit[SLOTS], cnt[SLOTS];
-        uint64_t hv[SLOTS];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
             hit[k] = 0;
@@ -1253,24 +1257,19 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             if (lanework)
                 hit[k] = coo_block_push<MODE>(a.pay, a.vb, d[k], J[k], R[k], mx[k], am[k], a.xd, a.yacc,
                                               a.parent);
-            const bool flat = act[k] && flat_coo(d[k]);
+            // every block with a payload record (stored COO and the other
+            // formats) goes to the entry-parallel pass; the block column
+            // carries the format in its top bits there
+            const bool flat = act[k] && !desc_inline(d[k]);
             cnt[k] = flat ? desc_nnz(d[k]) : 0u;
-            const bool wavework = act[k] && desc_type(d[k]) != T_COO;
-            hv[k] = ballot(wavework);
-            if (wavework || flat) hs->stage(k * WAVE + lane, d[k], J[k], mx[k], am[k], R[k]);
+            if (flat)
+                hs->stage(k * WAVE + lane, d[k], J[k] | (int32_t)(desc_type(d[k]) << 28), mx[k], am[k], R[k]);
         }
         if (ballot(cnt[0] | cnt[1] | cnt[2] | cnt[3])) {
             wave_lds_sync();
-            flat_pass<MODE, true, true>(a, hs, cnt, d, sy, sp, [] {});
+            flat_pass<MODE, true, true, true>(a, hs, cnt, d, sy, sp, [] {});
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k) if (cnt[k]) hit[k] |= hs->hitw[k * WAVE + lane];
-            wave_lds_sync();
-        }
-        if (hv[0] | hv[1] | hv[2] | hv[3]) {
-            wave_lds_sync();
-            run_staged<MODE, true>(a, hs, hv, sy, sp);
-#pragma unroll
-            for (int k = 0; k < SLOTS; ++k) if ((hv[k] >> lane) & 1u) hit[k] |= hs->hits(k * WAVE + lane);
             wave_lds_sync();
         }
 #pragma unroll

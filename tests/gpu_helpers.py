@@ -55,7 +55,7 @@ def f16_ulp_dist(a16: np.ndarray, b16: np.ndarray) -> np.ndarray:
 
 
 def check_spmspv(ctx, A, om, a: wl.CSR, x_idx, x_val, path="auto", mask=None, complement=False,
-                 semiring="plus_times", expect_path=None, label=""):
+                 semiring="plus_times", expect_path=None, label="", th3=0.0):
     """Runs one SpMSpV on the GPU and checks it against the oracle."""
     torch = torch_mod()
     xi = to_dev(np.asarray(x_idx, dtype=np.int32))
@@ -65,7 +65,7 @@ def check_spmspv(ctx, A, om, a: wl.CSR, x_idx, x_val, path="auto", mask=None, co
         xv = to_dev(np.asarray(x_val, dtype=vdt))
     md = None if mask is None else to_dev(mask)
     y_idx, y_val, st = ctx.spmspv(A, xi, xv, semiring=semiring, mask=md, complement=complement,
-                                  path=path, stats=True)
+                                  path=path, th3=th3, stats=True)
     torch.cuda.synchronize()
     gi = y_idx.cpu().numpy()
     if semiring == "plus_times":

@@ -49,7 +49,7 @@ def test_tiny_config(torch):
         log(f"tiny 4096x4096 k=41 path={p}")
         st = check_spmspv(ctx, A, om, a, x_idx, x_val, path=p, label=f"tiny/{p}")
         if p == "auto":
-            assert st["path"] == "pull"  # s_b ~ 0.14 >= 0.01
+            assert st["path"] == "pull"  # s_b ~ 0.14 >= th3
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
@@ -126,15 +126,19 @@ def test_empty_x_and_threshold(torch):
     log("empty x")
     st = check_spmspv(ctx, A, om, a, np.zeros(0, np.int32), np.zeros(0, np.float32), label="empty x")
     assert st["y_nnz"] == 0 and st["n_nzblk"] == 0
-    # N_blk = 25: push iff N_nzblk < 0.25 -> never push with one active block;
-    # the explicit th3 moves the boundary.
+    # N_blk = 25, one active block: with the paper's th3 = 0.01 push needs
+    # N_nzblk < 0.25 (never); the default th3 (0.05) gives N_nzblk < 1.25.
     xi = np.array([5, 6], dtype=np.int32)
     xv = np.array([0.5, -2.0], dtype=np.float32)
+    log("threshold paper value")
+    check_spmspv(ctx, A, om, a, xi, xv, expect_path="pull", label="th 0.01", th3=0.01)
     log("threshold default")
-    check_spmspv(ctx, A, om, a, xi, xv, expect_path="pull", label="th default")
-    torch = torch_mod()
-    y_idx, y_val, st = ctx.spmspv(A, to_dev(xi), to_dev(xv), th3=0.05, stats=True)
-    assert st["path"] == "push" and st["n_nzblk"] == 1 and st["n_blk"] == 25
+    st = check_spmspv(ctx, A, om, a, xi, xv, expect_path="push", label="th default")
+    assert st["n_nzblk"] == 1 and st["n_blk"] == 25
+    # exact boundary: 2 active blocks, th3 = 0.08 -> 2 < 2.0 is false -> pull
+    xi2 = np.array([5, 200], dtype=np.int32)
+    check_spmspv(ctx, A, om, a, xi2, xv, expect_path="pull", label="th boundary", th3=0.08)
+    check_spmspv(ctx, A, om, a, xi2, xv, expect_path="push", label="th above boundary", th3=0.0801)
 
 
 def test_context_reuse_across_matrices(torch):
