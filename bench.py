@@ -141,6 +141,49 @@ def run_ablation(args, torch, dbs, wl, dev):
         del ctx, A
     out["formats"] = fmt
 
+    # (2b) the same on a FEM-like natural-order matrix, where most blocks are
+    # patched CSR (the regime of the paper's matrices)
+    f = wl.fem(56, 3)
+    fy_idx = torch.empty(f.m, dtype=torch.int32, device=dev)
+    fy_val = torch.empty(f.m, dtype=torch.float32, device=dev)
+    fem = {}
+    for name, force, th0 in (("classifier", -1, 32), ("classifier_th0_97", -1, 97), ("classifier_th0_129", -1, 129),
+                             ("coo_only", 0, 32), ("csr_only", 4, 32), ("dense_only", 1, 32)):
+        opts = dbs.default_opts(th0=th0) if force < 0 else dbs.default_opts(force_type=force)
+        A = dbs.Matrix.from_csr(f.m, f.n, f.row_ptr, f.col_idx, f.vals, opts)
+        ctx = dbs.Context(A)
+        info = A.info()
+        rows = []
+        for di, d in enumerate([1e-3, 1e-2, 1e-1]):
+            xi, xv = wl.sparse_x(f.n, d, "uniform", key=(22, di))
+            dxi, dxv = torch.from_numpy(xi).to(dev), torch.from_numpy(xv).to(dev)
+            st = ctx.spmspv_raw(A, dxi, dxv, fy_idx, fy_val, y_nnz, stats=True)
+            row = {"density": d, "s_b": round(st["n_nzblk"] / st["n_blk"], 4), "auto_path": "push" if st["path"] == 1 else "pull"}
+            for path in ("auto", "push", "pull"):
+                row[f"{path}_us"] = round(_time_call(
+                    torch, lambda: ctx.spmspv_raw(A, dxi, dxv, fy_idx, fy_val, y_nnz, path=path), 10), 1)
+            rows.append(row)
+            log(f"[ablation] fem {name} {row}")
+        fem[name] = {"blocks_by_type": info["blocks_by_type"], "db_MB": round(info["db_bytes"] / 2**20, 1),
+                     "rows": rows}
+        del ctx, A
+    out["fem_formats"] = {"matrix": f"fem 56^3 x 3 dof, n={f.n}, nnz={f.nnz}", "results": fem}
+
+    # (2c) storage (Table 4 analog): DB vs CSR vs CSR+CSC for every config
+    store = []
+    for name, mk in (("tiny", lambda: wl.tiny()), ("rmat20", lambda: a), ("mesh126", lambda: wl.mesh()),
+                     ("fem56x3", lambda: f), ("decode_11008x4096", lambda: wl.decode_layer(11008, 4096)),
+                     ("decode_4096x14336", lambda: wl.decode_layer(4096, 14336))):
+        mtx = mk()
+        info = dbs.HostMatrix.from_csr(mtx.m, mtx.n, mtx.row_ptr, mtx.col_idx, mtx.vals).info()
+        store.append({"config": name, "n": mtx.n, "nnz": mtx.nnz, "nblk": info["nblk"],
+                      "blocks_by_type": info["blocks_by_type"],
+                      "db_MiB": round(info["db_bytes"] / 2**20, 2), "csr_MiB": round(info["csr_bytes"] / 2**20, 2),
+                      "csr_csc_MiB": round(info["csr_csc_bytes"] / 2**20, 2),
+                      "saving_vs_csr_csc": round(1 - info["db_bytes"] / info["csr_csc_bytes"], 4)})
+        log(f"[ablation] storage {store[-1]}")
+    out["storage"] = store
+
     # (3) BFS under candidate th3
     if args.bfs_scale > 0:
         g = wl.rmat(args.bfs_scale, values=False)

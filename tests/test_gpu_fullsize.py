@@ -7,6 +7,9 @@ benchmark times (one context, automatic path plus forced push / pull):
   parent[] bit-exact, plus reuse of one context across calls;
 * relabelled 126^3 mesh with 5% random entries, BFS-ball x at 0.1%-10%;
 * fp16 decode layers 11008x4096 and 4096x14336 with 10%-dense activations;
+* a FEM-like natural-order matrix (27-point stencil, 3 unknowns per node:
+  72% patched-CSR blocks) with uniform and clustered x, OR-AND, BFS, and
+  every block forced into each format;
 * a mid-size R-MAT (scale 17) where the look-back scans span several tiles.
 """
 import numpy as np
@@ -180,3 +183,52 @@ def test_decode_layers(torch, shape):
             assert oracle.within_tol(y32.cpu().numpy(), y64, S, REL_TOL).all(), label
             if p == "auto":
                 assert st["path"] == "pull"
+
+
+# ------------------------------------------------------------------ FEM-like
+@pytest.fixture(scope="module")
+def fem(torch):
+    log("generating FEM 24^3 x 3")
+    a = wl.fem(24, 3)
+    return a, gpu_matrix(a), oracle_matrix(a)
+
+
+def test_fem_spmspv(fem):
+    a, A, om = fem
+    info = A.info()
+    assert info["blocks_by_type"]["csr"] > info["blocks_by_type"]["coo"] > 0
+    ctx = dbs.Context(A)
+    for di, d in enumerate([1e-3, 1e-2, 1e-1, 0.5]):
+        for kind in ("uniform", "clustered"):
+            xi, xv = wl.sparse_x(a.n, d, kind, key=(60, di), lo=-1.0, hi=1.0)
+            for p in ("auto", "push", "pull"):
+                label = f"fem d={d} {kind} path={p}"
+                log(label)
+                check_spmspv(ctx, A, om, a, xi, xv, path=p, label=label)
+                if d == 1e-2:
+                    check_spmspv(ctx, A, om, a, xi, None, path=p, semiring="or_and", label=label + " or_and")
+
+
+@pytest.mark.parametrize("force", [0, 1, 2, 3, 4])
+def test_fem_forced_formats(fem, force):
+    a, _, om = fem
+    A = gpu_matrix(a, dbs.default_opts(force_type=force))
+    ctx = dbs.Context(A)
+    for di, d in enumerate([1e-2, 0.2]):
+        xi, xv = wl.sparse_x(a.n, d, "uniform", key=(61, di), lo=-1.0, hi=1.0)
+        for p in ("push", "pull"):
+            label = f"fem force={force} d={d} path={p}"
+            log(label)
+            check_spmspv(ctx, A, om, a, xi, xv, path=p, label=label)
+
+
+def test_fem_bfs(fem):
+    a, _, _ = fem
+    g = wl.CSR(a.m, a.n, a.row_ptr, a.col_idx, None)
+    G, og = gpu_matrix(g), oracle_matrix(g)
+    ctx = dbs.Context(G)
+    rng = wl.rng_for(wl.W_RAND, 62, 0)
+    for s in rng.choice(a.n, 3, replace=False):
+        for policy in ("auto", "push", "pull"):
+            log(f"fem bfs source={s} policy={policy}")
+            bfs_exact(ctx, G, og, s, policy, f"fem bfs {s} {policy}")

@@ -80,7 +80,7 @@ def seed64_for(*key: int) -> int:
 
 
 # workload ids used in the seed keys
-W_TINY, W_RMAT, W_MESH, W_DECODE, W_CRAFT, W_RAND = 1, 2, 3, 5, 7, 9
+W_TINY, W_RMAT, W_MESH, W_DECODE, W_CRAFT, W_RAND, W_FEM = 1, 2, 3, 5, 7, 9, 11
 
 
 @dataclass
@@ -254,6 +254,41 @@ def mesh(side: int = 126, extra_frac: float = 0.05) -> CSR:
     a = csr_from_coo(N, N, perm[r], perm[c])
     a.vals = _nonzero_normal(rng_for(W_MESH, 2), 1.0, a.nnz)
     return a
+
+
+def fem(side: int = 56, dof: int = 3) -> CSR:
+    """FEM-like matrix in natural order: a side^3 grid with `dof` unknowns per
+    node and a 27-point stencil coupling every unknown of a node with every
+    unknown of its (up to 26) neighbours and itself.  Rows and columns are
+    node-major, dof-minor (no relabelling), so 16x16 blocks near the diagonal
+    are dense-ish, the regime of the paper's FEM matrices.  Values N(0,1)."""
+    N = side ** 3
+    v = np.arange(N, dtype=np.int64)
+    x, rem = np.divmod(v, side * side)
+    y, z = np.divmod(rem, side)
+    nbs = []
+    for dx in (-1, 0, 1):           # lexicographic offsets: ascending neighbour ids
+        for dy in (-1, 0, 1):
+            for dz in (-1, 0, 1):
+                ok = ((x + dx >= 0) & (x + dx < side) & (y + dy >= 0) & (y + dy < side)
+                      & (z + dz >= 0) & (z + dz < side))
+                nbs.append(np.where(ok, v + dx * side * side + dy * side + dz, -1))
+    nb = np.stack(nbs, axis=1)                       # [N, 27], -1 = outside
+    cnt = (nb >= 0).sum(axis=1)                      # neighbours per node (incl. itself)
+    row_len = np.repeat(cnt * dof, dof)              # every unknown of a node: same columns
+    row_ptr = np.zeros(N * dof + 1, dtype=np.int64)
+    np.cumsum(row_len, out=row_ptr[1:])
+    nbv = nb[nb >= 0]                                # flattened valid neighbours, node-major
+    node_cols = (nbv[:, None] * dof + np.arange(dof)[None, :]).reshape(-1)
+    node_ptr = np.zeros(N + 1, dtype=np.int64)
+    np.cumsum(cnt * dof, out=node_ptr[1:])
+    # each of the dof rows of node v repeats node_cols[node_ptr[v]:node_ptr[v+1]]
+    rep_start = np.repeat(node_ptr[:-1], dof)
+    lens = np.repeat(cnt * dof, dof)
+    idx = np.repeat(rep_start - row_ptr[:-1], lens) + np.arange(int(row_ptr[-1]), dtype=np.int64)
+    col = node_cols[idx].astype(np.int32)
+    vals = _nonzero_normal(rng_for(W_FEM, side, dof), 1.0, col.size)
+    return CSR(N * dof, N * dof, row_ptr, col, vals)
 
 
 def symmetric_pattern(a: CSR):
