@@ -17,15 +17,19 @@
 //                         ascending sparse y, and reset of the scratch it used
 //
 // Wave64 mapping (differs from the paper's warp-32 kernels):
-//  * a hypersparse COO block is processed by ONE lane (a quarter-wave of 16
-//    lanes covers the <= 16 blocks of a pull segment; a full wave covers 64
-//    push tasks); blocks of the other formats are processed by the whole wave,
-//    one at a time, picked by a ballot.
-//  * Dense / ForceCSR / patched-CSR row kernels use 4 lanes per block row
-//    (16 rows x 4 = 64 lanes); ForceCSC uses 16 row lanes x 4 column quarters.
+//  * pull: a quarter-wave (16 lanes) per segment, one block per lane, four
+//    segments per lane in flight; blocks whose vector block is empty are
+//    dropped by an activity bitmap in LDS before anything is gathered.
+//  * a COO block whose entries sit in its descriptor is taken by one lane
+//    (one x gather, which also tells whether x_j is stored); COO blocks with
+//    a record are taken entry-parallel by the whole wave (flat_pass), as are
+//    all record blocks in push.  Pull takes the other formats from an
+//    upload-time list ahead of the segment loop, one whole-wave block at a
+//    time (heavy_block).
 //  * fp32 partial sums per row block go through LDS atomics (ds_add_f32), and
 //    are committed to an fp64 accumulator per row: a plain store when the
 //    block row has one segment, a global fp64 atomic otherwise.
+//  * wave scans and row reductions use DPP row shifts and broadcasts.
 #include <climits>
 
 #include "device_common.hpp"
@@ -321,44 +325,24 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
 // block microkernels
 // ---------------------------------------------------------------------------
 
-// Coordinate bytes (row << 4 | col) of a COO block with at most 8 entries,
-// byte e of the result for entry e: from the descriptor when the block is
-// held inline, else with at most three aligned dword loads covering the
-// record's coordinate bytes (the payload is padded to 16 bytes, so the last
-// covering dword is inside it).
-__device__ __forceinline__ uint64_t coo_coords(uint64_t d, const uint8_t *pay, uint32_t vb, uint32_t nnz)
+// Coordinate bytes (row << 4 | col) of a COO block held in its descriptor
+// (at most 6 entries), byte e of the result for entry e.
+__device__ __forceinline__ uint64_t inline_coords(uint64_t d, uint32_t vb, uint32_t nnz)
 {
-    if (desc_inline(d)) {
-        if (nnz == 1) return (d >> 16) & 0xFFull;  // the common hypersparse case
-        uint64_t c = 0;
-        for (uint32_t e = 0; e < nnz; ++e) c |= ((d >> inline_shift(e, vb)) & 0xFFull) << (8 * e);
-        return c;
-    }
-    // the coordinates follow the values; read them as aligned words of the
-    // (256-byte aligned) payload, indexed from its base so that the loads
-    // stay global loads
-    const uint64_t at = desc_off(d) + (uint64_t)vb * nnz;
-    const uint32_t mis = (uint32_t)(at & 3u);
-    const uint32_t *w = (const uint32_t *)pay + (at >> 2);
-    const uint32_t nw = (mis + nnz + 3) / 4;
-    const uint32_t w0 = w[0], w1 = nw > 1 ? w[1] : 0u, w2 = nw > 2 ? w[2] : 0u;
-    const uint64_t lo = ((uint64_t)w1 << 32) | w0;
-    return mis ? ((lo >> (8 * mis)) | ((uint64_t)w2 << (64 - 8 * mis))) : lo;
+    if (nnz == 1) return (d >> 16) & 0xFFull;  // the common hypersparse case
+    uint64_t c = 0;
+    for (uint32_t e = 0; e < nnz; ++e) c |= ((d >> inline_shift(e, vb)) & 0xFFull) << (8 * e);
+    return c;
 }
 
-// Value of entry e of a COO block (inline or from its record).
+// Value of entry e of a COO block held in its descriptor.
 template <int MODE>
-__device__ __forceinline__ float coo_value(uint64_t d, const uint8_t *rec, uint32_t vb, uint32_t e)
+__device__ __forceinline__ float inline_value(uint64_t d, uint32_t vb, uint32_t e)
 {
-    if constexpr (MODE == M_F32) {
-        if (desc_inline(d)) return __uint_as_float((uint32_t)(d >> (inline_shift(e, vb) + 8)));
-        return VT<MODE>::load(rec, e);
-    } else if constexpr (MODE == M_F16) {
-        if (desc_inline(d)) return h2f((uint16_t)(d >> (inline_shift(e, vb) + 8)));
-        return VT<MODE>::load(rec, e);
-    } else {
-        return 0.f;
-    }
+    const uint32_t bits = (uint32_t)(d >> (inline_shift(e, vb) + 8));
+    if constexpr (MODE == M_F32) return __uint_as_float(bits);
+    else if constexpr (MODE == M_F16) return h2f((uint16_t)bits);
+    else return 0.f;
 }
 
 // Bit e set for every entry e of a COO block whose column is active in the
@@ -380,14 +364,12 @@ __device__ __forceinline__ uint32_t coo_matches(uint64_t cds, uint32_t nnz, uint
 // is kept (the first match met, columns ascend within a row).  Returns the
 // rows hit.
 template <int MODE>
-__device__ __forceinline__ uint32_t coo_block_push(const uint8_t *__restrict__ pay, uint32_t vb,
-                                                   uint64_t d, int32_t J, int32_t R, uint32_t mx,
-                                                   uint32_t am, const void *__restrict__ xd,
-                                                   double *yacc, int32_t *parent)
+__device__ __forceinline__ uint32_t inline_block_push(uint32_t vb, uint64_t d, int32_t J, int32_t R,
+                                                      uint32_t mx, uint32_t am, const void *__restrict__ xd,
+                                                      double *yacc, int32_t *parent)
 {
     const uint32_t nnz = desc_nnz(d);
-    const uint8_t *rec = pay + (desc_inline(d) ? 0 : desc_off(d));
-    const uint64_t cds = coo_coords(d, pay, vb, nnz);
+    const uint64_t cds = inline_coords(d, vb, nnz);
     uint32_t mm = coo_matches(cds, nnz, mx, am);
     uint32_t hit = 0;
     int cur = -1;
@@ -397,7 +379,7 @@ __device__ __forceinline__ uint32_t coo_block_push(const uint8_t *__restrict__ p
         mm &= mm - 1;
         const uint32_t cd = (uint32_t)(cds >> (8 * e)) & 0xFFu, r = cd >> 4, c = cd & 15u;
         if constexpr (valued<MODE>()) {
-            const float prod = coo_value<MODE>(d, rec, vb, e) * VT<MODE>::x(xd, (int64_t)J * BS + c);
+            const float prod = inline_value<MODE>(d, vb, e) * VT<MODE>::x(xd, (int64_t)J * BS + c);
             if ((int)r != cur) {
                 if (cur >= 0) atomicAdd(&yacc[(int64_t)R * BS + cur], (double)acc);
                 cur = (int)r;
@@ -729,8 +711,7 @@ __device__ __forceinline__ uint32_t inline_block(const MainArgs &a, uint64_t d, 
         const uint32_t raw = xr[valued<MODE>() ? e : 0];
         if (!x_present<MODE>(raw, J, c) || !((am >> r) & 1u)) continue;
         if constexpr (valued<MODE>()) {
-            const uint32_t vbits = (uint32_t)(d >> (inline_shift((uint32_t)e, vb) + 8));
-            const float prod = (MODE == M_F32 ? __uint_as_float(vbits) : h2f((uint16_t)vbits)) * x_value<MODE>(raw);
+            const float prod = inline_value<MODE>(d, vb, (uint32_t)e) * x_value<MODE>(raw);
             if ((int)r != cur) {
                 if (cur >= 0) atomicAdd(&dst16[cur], acc);
                 cur = (int)r;
@@ -1255,8 +1236,7 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             hit[k] = 0;
             const bool lanework = act[k] && lane_coo(d[k]);
             if (lanework)
-                hit[k] = coo_block_push<MODE>(a.pay, a.vb, d[k], J[k], R[k], mx[k], am[k], a.xd, a.yacc,
-                                              a.parent);
+                hit[k] = inline_block_push<MODE>(a.vb, d[k], J[k], R[k], mx[k], am[k], a.xd, a.yacc, a.parent);
             // every block with a payload record (stored COO and the other
             // formats) goes to the entry-parallel pass; the block column
             // carries the format in its top bits there
