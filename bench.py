@@ -77,6 +77,128 @@ def _time_call(torch, fn, reps):
     return e0.elapsed_time(e1) * 1e3 / reps
 
 
+def _cold_us(torch, fn, reps, flush, ctx=None):
+    """Cold timing: every call runs alone after a write of the 1 GiB flush
+    buffer, which evicts the 256 MB Infinity Cache and the L2 of every XCD.
+    Returns (median, mean) microseconds of the whole call and, with ctx,
+    the median microseconds of its traversal kernels (HIP events on the
+    library's stream, taken in a second set of calls so that they do not
+    add to the first)."""
+    whole, trav = [], []
+    for rnd in range(2 if ctx is not None else 1):
+        if rnd:
+            ctx.enable_timing(True)
+            ctx.read_timing()
+        for i in range(reps):
+            flush.fill_(float(i + 1))
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            if rnd:
+                ms, launches = ctx.read_timing()["main"]
+                trav.append(ms * 1e3)
+            else:
+                whole.append(e0.elapsed_time(e1) * 1e3)
+        if rnd:
+            ctx.enable_timing(False)
+    out = (float(np.median(whole)), float(np.mean(whole)))
+    return out + ((float(np.median(trav)),) if ctx is not None else ())
+
+
+def copy_bandwidth(torch, dev, reps=10):
+    """GB/s of a 1 GiB device-to-device copy (1 GiB read + 1 GiB written):
+    the achievable-bandwidth line beside the 8 TB/s peak."""
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    us = _time_call(torch, lambda: dst.copy_(src), reps)
+    del src, dst
+    return 2 * (1 << 30) / (us * 1e-6) / 1e9
+
+
+def other_configs(args, torch, dbs, wl, dev, flush):
+    """Mesh-like SpMSpV (126^3 7-point stencil, relabelled, 5% random
+    entries; x from BFS balls at 0.1%, 1%, 10%) and the two sparse decode
+    layers (fp16, 50% kept, 10% dense activation, dense fp16 y), warm and
+    cold, in the units of the main sweep; the decode layers also beside a
+    dense fp16 F.linear of the same weights (the paper's PyTorch baseline)."""
+    from paper_2608_16308_amd.bytes_model import BytesModel
+    out = {}
+    reps = args.point_reps
+    # ---- mesh
+    t0 = time.time()
+    a = wl.mesh()
+    S = wl.symmetric_pattern(a)
+    hm = dbs.HostMatrix.from_csr(a.m, a.n, a.row_ptr, a.col_idx, a.vals)
+    info = hm.info()
+    model = BytesModel(a.m, a.n, a.row_ptr, a.col_idx, hm.arrays(), info, 4)
+    A = dbs.Matrix.upload(hm)
+    del hm
+    ctx = dbs.Context(A)
+    log(f"[bench] mesh 126^3: n={a.n} nnz={a.nnz} nblk={info['nblk']} ready in {time.time() - t0:.1f}s")
+    y_idx = torch.empty(a.m, dtype=torch.int32, device=dev)
+    y_val = torch.empty(a.m, dtype=torch.float32, device=dev)
+    y_nnz = torch.zeros(1, dtype=torch.int32, device=dev)
+    rows = []
+    for d in (1e-3, 1e-2, 1e-1):
+        xi, xv = wl.ball_x(a, d, key=int(d * 1e4), S=S)
+        dxi, dxv = torch.from_numpy(xi).to(dev), torch.from_numpy(xv).to(dev)
+        call = lambda: ctx.spmspv_raw(A, dxi, dxv, y_idx, y_val, y_nnz)
+        st = ctx.spmspv_raw(A, dxi, dxv, y_idx, y_val, y_nnz, stats=True)
+        mod = model.call(xi, st["path"])
+        us = _time_call(torch, call, reps)
+        cold, _, cold_trav = _cold_us(torch, call, reps, flush, ctx)
+        rows.append({"density": d, "k": int(xi.size), "path": st["path"], "n_nzblk": st["n_nzblk"],
+                     "y_nnz": st["y_nnz"], "bytes": mod["bytes_total"], "us": round(us, 2),
+                     "GBs": round(mod["bytes_total"] / (us * 1e-6) / 1e9, 1),
+                     "cold_us": round(cold, 2), "cold_GBs": round(mod["bytes_total"] / (cold * 1e-6) / 1e9, 1),
+                     "cold_traversal_GBs": round(mod["bytes_main"] / (cold_trav * 1e-6) / 1e9, 1),
+                     "useful_GFLOPs": round(2 * mod["useful_nnz"] / (us * 1e-6) / 1e9, 2)})
+        log(f"[bench] mesh {rows[-1]}")
+    out["mesh126"] = {"n": a.n, "nnz": a.nnz, "nblk": info["nblk"], "x": "BFS balls", "points": rows}
+    del ctx, A, S, a, y_idx, y_val
+    torch.cuda.empty_cache()
+    # ---- decode layers
+    import torch.nn.functional as F
+    layers = []
+    for out_f, in_f in ((11008, 4096), (4096, 14336)):
+        w = wl.decode_layer(out_f, in_f)
+        hm = dbs.HostMatrix.from_csr(w.m, w.n, w.row_ptr, w.col_idx, w.vals)
+        info = hm.info()
+        model = BytesModel(w.m, w.n, w.row_ptr, w.col_idx, hm.arrays(), info, 2)
+        A = dbs.Matrix.upload(hm)
+        del hm
+        ctx = dbs.Context(A)
+        a16 = wl.decode_activation(in_f, key=0)
+        nz = np.nonzero(a16)[0].astype(np.int32)
+        x = torch.from_numpy(a16.view(np.int16)).to(dev).view(torch.float16)
+        y = torch.empty(out_f, dtype=torch.float16, device=dev)
+        _, st = ctx.spmspv_dense(A, x, y=y, stats=True)
+        mod = model.call_dense(nz, st["path"])
+        call = lambda: ctx.spmspv_dense(A, x, y=y)
+        us = _time_call(torch, call, reps)
+        cold, _, cold_trav = _cold_us(torch, call, reps, flush, ctx)
+        wd = torch.from_numpy(w.dense().astype(np.float16)).to(dev)
+        xr = x.view(1, in_f)
+        lin = lambda: F.linear(xr, wd)
+        lin_us = _time_call(torch, lin, reps)
+        lin_cold = _cold_us(torch, lin, reps, flush)[0]
+        layers.append({"shape": [out_f, in_f], "nnz": w.nnz, "blocks_by_type": info["blocks_by_type"],
+                       "path": st["path"], "bytes": mod["bytes_total"], "us": round(us, 2),
+                       "GBs": round(mod["bytes_total"] / (us * 1e-6) / 1e9, 1), "cold_us": round(cold, 2),
+                       "cold_GBs": round(mod["bytes_total"] / (cold * 1e-6) / 1e9, 1),
+                       "cold_traversal_GBs": round(mod["bytes_main"] / (cold_trav * 1e-6) / 1e9, 1),
+                       "dense_f16_linear_us": round(lin_us, 2), "dense_f16_linear_cold_us": round(lin_cold, 2),
+                       "speedup_vs_dense_cold": round(lin_cold / cold, 2)})
+        log(f"[bench] decode {layers[-1]}")
+        del ctx, A, wd
+        torch.cuda.empty_cache()
+    out["decode"] = {"activation": "10% nonzero, 70% of them in 10% of the 64-wide blocks, |N(0,1)| fp16",
+                     "layers": layers}
+    return out
+
+
 def run_ablation(args, torch, dbs, wl, dev):
     """Paper Sec. 5 style ablations on the synthetic R-MAT matrices: (1) the
     push / pull crossover over a finer density grid, as a function of
@@ -129,6 +251,28 @@ def run_ablation(args, torch, dbs, wl, dev):
     log(f"[ablation] push/pull crossover in s_b: {cross}")
     del ctx, A
 
+    # (1b) the basic push / pull of Alg. 1 (plain CSC / CSR, no blocks) on the
+    # bench's sweep points, beside the blocked method's automatic path
+    basic = []
+    B = dbs.BasicMatrix(a.m, a.n, a.row_ptr, a.col_idx, a.vals)
+    A = dbs.Matrix.from_csr(a.m, a.n, a.row_ptr, a.col_idx, a.vals)
+    ctx = dbs.Context(A)
+    yd = torch.empty(a.m, dtype=torch.float32, device=dev)
+    for di, d in enumerate(DENSITIES):
+        for kind in KINDS:
+            xi, xv = wl.sparse_x(a.n, d, kind, key=(20, di, KINDS.index(kind)))
+            dxi, dxv = torch.from_numpy(xi).to(dev), torch.from_numpy(xv).to(dev)
+            row = {"density": d, "x": kind, "k": int(xi.size)}
+            row["db_auto_us"] = round(_time_call(
+                torch, lambda: ctx.spmspv_raw(A, dxi, dxv, y_idx, y_val, y_nnz), 10), 1)
+            for path in ("pull", "push"):
+                row[f"basic_{path}_us"] = round(_time_call(torch, lambda: B.spmspv(path, dxi, dxv, yd), 10), 1)
+            row["speedup_vs_best_basic"] = round(min(row["basic_pull_us"], row["basic_push_us"]) / row["db_auto_us"], 2)
+            basic.append(row)
+            log(f"[ablation] basic {row}")
+    out["basic_alg1"] = {"matrix": f"R-MAT {args.scale}", "rows": basic}
+    del ctx, A, B
+
     # (2) forced formats (all blocks COO / all patched CSR / classifier)
     fmt = {}
     for name, force in (("classifier", -1), ("coo_only", 0), ("csr_only", 4)):
@@ -158,7 +302,7 @@ def run_ablation(args, torch, dbs, wl, dev):
             xi, xv = wl.sparse_x(f.n, d, "uniform", key=(22, di))
             dxi, dxv = torch.from_numpy(xi).to(dev), torch.from_numpy(xv).to(dev)
             st = ctx.spmspv_raw(A, dxi, dxv, fy_idx, fy_val, y_nnz, stats=True)
-            row = {"density": d, "s_b": round(st["n_nzblk"] / st["n_blk"], 4), "auto_path": "push" if st["path"] == 1 else "pull"}
+            row = {"density": d, "s_b": round(st["n_nzblk"] / st["n_blk"], 4), "auto_path": st["path"]}
             for path in ("auto", "push", "pull"):
                 row[f"{path}_us"] = round(_time_call(
                     torch, lambda: ctx.spmspv_raw(A, dxi, dxv, fy_idx, fy_val, y_nnz, path=path), 10), 1)
@@ -218,6 +362,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--point-reps", type=int, default=20)
     ap.add_argument("--json-out", default=None)
+    ap.add_argument("--other-configs", type=int, default=1,
+                    help="also time the mesh-like matrix and the two decode layers (0 to skip)")
     ap.add_argument("--ablation", action="store_true",
                     help="path / format / selector ablation on R-MAT (no bench line): push vs pull over a "
                          "finer density grid, the crossover in s_b = N_nzblk / N_blk, forced block formats, "
@@ -331,6 +477,10 @@ def main():
         return
 
     # ------------------------------------------------------------ per point
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    copy_gbs = copy_bandwidth(torch, dev)
+    log(f"[bench] 1 GiB device copy: {copy_gbs:.1f} GB/s")
+    cold_main_s = cold_whole_s = 0.0
     sweep = []
     for p in points:
         row = {"density": p["density"], "x": p["kind"], "k": p["model"]["k"], "path": p["path"],
@@ -353,8 +503,19 @@ def main():
             if path == "auto":
                 row["useful_GFLOPs"] = round(2 * p["model"]["useful_nnz"] / (us * 1e-6) / 1e9, 2)
                 row["spmv_conv_GFLOPs"] = round(2 * a.nnz / (us * 1e-6) / 1e9, 1)
+        cold, cold_mean, cold_trav = _cold_us(torch, lambda: run(p), args.point_reps, flush, ctx)
+        row["cold_us"] = round(cold, 2)
+        row["cold_mean_us"] = round(cold_mean, 2)
+        row["cold_GBs"] = round(p["model"]["bytes_total"] / (cold * 1e-6) / 1e9, 1)
+        row["cold_traversal_us"] = round(cold_trav, 2)
+        cold_main_s += cold_trav * 1e-6
+        cold_whole_s += cold * 1e-6
         sweep.append(row)
         log(f"[bench] {row}")
+
+    cold_achieved = step_main_bytes / cold_main_s / 1e9
+    extra = other_configs(args, torch, dbs, wl, dev, flush) if args.other_configs else None
+    del flush
 
     # ------------------------------------------------------------ CPU oracle
     import oracle
@@ -388,7 +549,14 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_traffic(kernel_sources_digest()),
                      "kernel": "k_main (push/pull traversal)", "avg_launch_us": round(main_avg_ms * 1e3, 2),
-                     "algorithmic_bytes_per_launch": round(step_main_bytes / len(points))},
+                     "algorithmic_bytes_per_launch": round(step_main_bytes / len(points)),
+                     "copy_GBs": round(copy_gbs, 1), "frac_of_copy": round(achieved / copy_gbs, 4)},
+        # the same kernels with the Infinity Cache and L2 flushed before
+        # every call (one call at a time, median per point)
+        "roofline_cold": {"achieved": round(cold_achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(cold_achieved / HBM_PEAK_GBS, 4),
+                          "frac_of_copy": round(cold_achieved / copy_gbs, 4),
+                          "whole_path_GBs": round(step_bytes / cold_whole_s / 1e9, 1)},
         # path-independent view: the compulsory bytes (every stored entry of
         # the active columns, its x value and the y output) per second; the
         # model bytes depend on the path taken (push touches fewer)
@@ -400,6 +568,8 @@ def main():
                                    f"({cpu_s:.1f} s, CSC built once outside the timing)"},
         "sweep": sweep,
     }
+    if extra is not None:
+        result["other_configs"] = extra
 
     # ------------------------------------------------------------ BFS GTEPS
     if args.bfs_scale > 0:

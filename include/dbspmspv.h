@@ -269,6 +269,41 @@ dbs_status dbs_bfs(dbs_ctx *ctx, const dbs_matrix *A, int32_t source, int32_t *d
                    int32_t *d_parent, dbs_path policy, float th3, dbs_bfs_stats *stats);
 
 /* ---------------------------------------------------------------------- */
+/* Basic push / pull baselines (Alg. 1, Sec. 2.1-2.2).                    */
+/* ---------------------------------------------------------------------- */
+
+/* The two fixed paradigms the method is measured against in the paper's
+ * motivation: column-driven push over a plain CSC and row-driven pull over
+ * a plain CSR, with no blocking, no selector and no load balancing.  They
+ * exist for ablation and comparison only; the blocked method never uses
+ * them.  F32 only. */
+typedef struct dbs_basic_matrix dbs_basic_matrix;
+
+/* Copies the CSR of A (same conventions as dbs_host_build_csr: row_ptr of
+ * m+1 int64, nnz int32 columns in [0, n), nnz float values) to the current
+ * device and builds its CSC there-from on the host (rows ascending within a
+ * column).  Duplicate (i, j) entries are kept and summed.  Allocates
+ * O(m + n + nnz) device memory, including an n-float dense-x scratch that
+ * is all zero between calls.                                              */
+dbs_status dbs_basic_build(int32_t m, int32_t n, int64_t nnz, const int64_t *row_ptr,
+                           const int32_t *col_idx, const float *vals, dbs_basic_matrix **out);
+void dbs_basic_destroy(dbs_basic_matrix *B);
+
+/* y = A x into a DENSE fp32 d_y[m] (rows without a product are 0).
+ *   path = DBS_PATH_PULL: every row i sums a_ij * x_j over all its stored
+ *          entries against the dense x scratch (x scattered into it, then
+ *          cleared again after the row pass); fp32 sums, one write per row.
+ *   path = DBS_PATH_PUSH: d_y is zeroed, then every listed x_j adds
+ *          a_ij * x_j into d_y[i] along column j with fp32 atomics (order,
+ *          hence rounding, not deterministic).
+ * x: x_nnz unique int32 indices (out-of-range ones are skipped) and fp32
+ * values, device memory.  Asynchronous on `stream` (a hipStream_t, NULL =
+ * default stream).  Calls that share one dbs_basic_matrix must not overlap
+ * in time (the dense-x scratch is shared).                                 */
+dbs_status dbs_basic_spmspv(dbs_basic_matrix *B, dbs_path path, int32_t x_nnz, const int32_t *d_x_idx,
+                            const float *d_x_val, float *d_y, void *stream);
+
+/* ---------------------------------------------------------------------- */
 /* Measurement hooks.                                                     */
 /* ---------------------------------------------------------------------- */
 

@@ -22,7 +22,7 @@ from . import _lib
 from ._lib import (BLOCK_TYPE_NAMES, DBS_F16, DBS_F32, DBS_OR_AND, DBS_PATH_AUTO, DBS_PATH_PULL,
                    DBS_PATH_PUSH, DBS_PATTERN, DBS_PLUS_TIMES, DbsError, check)
 
-__all__ = ["HostMatrix", "Matrix", "Context", "DbsError", "default_opts", "storage_model",
+__all__ = ["HostMatrix", "Matrix", "Context", "BasicMatrix", "DbsError", "default_opts", "storage_model",
            "DBS_F32", "DBS_F16", "DBS_PATTERN", "PATHS"]
 
 PATHS = {"auto": DBS_PATH_AUTO, "push": DBS_PATH_PUSH, "pull": DBS_PATH_PULL}
@@ -152,6 +152,36 @@ class Matrix:
 
 def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+class BasicMatrix:
+    """Plain CSR + CSC copies of an fp32 matrix on the current GPU for the
+    basic push and pull of Alg. 1 (comparison baselines only)."""
+
+    def __init__(self, m, n, row_ptr, col_idx, vals):
+        rp = np.ascontiguousarray(row_ptr, dtype=np.int64)
+        ci = np.ascontiguousarray(col_idx, dtype=np.int32)
+        va = np.ascontiguousarray(vals, dtype=np.float32)
+        out = ctypes.c_void_p()
+        check(lib().dbs_basic_build(int(m), int(n), int(rp[-1]), rp.ctypes.data, ci.ctypes.data,
+                                    va.ctypes.data, ctypes.byref(out)))
+        self._h = out
+        self.m, self.n = int(m), int(n)
+
+    def spmspv(self, path, x_idx, x_val, y, stream=None):
+        """Dense fp32 y[m] = A x by "push" or "pull" (torch CUDA tensors)."""
+        import torch
+        s = (stream or torch.cuda.current_stream()).cuda_stream
+        k = 0 if x_idx is None else int(x_idx.numel())
+        check(lib().dbs_basic_spmspv(self._h, PATHS[path], k, _ptr(x_idx), _ptr(x_val), _ptr(y),
+                                     ctypes.c_void_p(s)))
+        return y
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            lib().dbs_basic_destroy(h)
+            self._h = None
 
 
 class Context:

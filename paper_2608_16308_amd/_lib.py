@@ -25,7 +25,8 @@ EXPORTED = [
     "dbs_host_destroy", "dbs_storage_model", "dbs_matrix_upload", "dbs_matrix_build_csr",
     "dbs_matrix_info_get", "dbs_matrix_destroy", "dbs_ctx_create", "dbs_ctx_set_stream",
     "dbs_ctx_destroy", "dbs_spmspv", "dbs_spmspv_dense", "dbs_bfs", "dbs_ctx_enable_timing",
-    "dbs_ctx_read_timing", "dbs_last_error", "dbs_version",
+    "dbs_ctx_read_timing", "dbs_last_error", "dbs_version", "dbs_basic_build", "dbs_basic_destroy",
+    "dbs_basic_spmspv",
 ]
 
 
@@ -114,6 +115,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dbs_bfs": (ctypes.c_int, [vp, vp, i32, vp, vp, ctypes.c_int, f32, P(BfsStats)]),
         "dbs_ctx_enable_timing": (ctypes.c_int, [vp, ctypes.c_int]),
         "dbs_ctx_read_timing": (ctypes.c_int, [vp, P(Timing)]),
+        "dbs_basic_build": (ctypes.c_int, [i32, i32, i64, vp, vp, vp, P(vp)]),
+        "dbs_basic_destroy": (None, [vp]),
+        "dbs_basic_spmspv": (ctypes.c_int, [vp, ctypes.c_int, i32, vp, vp, vp, vp]),
         "dbs_last_error": (ctypes.c_char_p, []),
         "dbs_version": (ctypes.c_char_p, []),
     }

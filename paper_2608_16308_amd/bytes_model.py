@@ -129,3 +129,17 @@ class BytesModel:
                 "useful_nnz": useful, "y_nnz": y_nnz, "bytes_blocker": blocker, "bytes_scan": scan,
                 "bytes_main": int(main), "bytes_finalize": finalize, "bytes_total": int(total),
                 "bytes_compulsory": int(compulsory)}
+
+    def call_dense(self, x_idx, path: str, th3: float = 0.01) -> dict:
+        """The same for a dense activation and a dense y (decoding, Sec. 4.1):
+        the blocker reads all n values, writes the padded dense x and the
+        n-bit mask; the finalize reads every fp64 accumulator, writes y (V
+        bytes per row) and resets the accumulators, the y and x masks and
+        the dense x.  x_idx are the nonzero positions of the activation."""
+        r = self.call(x_idx, path, th3)
+        V, m, n = self.V, self.m, self.n
+        r["bytes_blocker"] = 2 * V * n + n // 8
+        r["bytes_finalize"] = m * (8 + 8 + V) + m // 8 + n // 8 + V * n
+        r["bytes_total"] = r["bytes_blocker"] + r["bytes_scan"] + r["bytes_main"] + r["bytes_finalize"]
+        r["bytes_compulsory"] = r["useful_nnz"] * (V + 1) + V * n + V * m
+        return r

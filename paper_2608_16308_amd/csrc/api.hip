@@ -41,14 +41,18 @@ dbs_status check_device()
     return DBS_OK;
 }
 
+// pad: zeroed bytes after the data (the payload gets 16, so that a 16-byte
+// load of the chunk holding a record's last byte stays inside the allocation)
 template <class T>
-dbs_status dev_upload(std::vector<void *> &allocs, const std::vector<T> &h, const T **out)
+dbs_status dev_upload(std::vector<void *> &allocs, const std::vector<T> &h, const T **out, size_t pad = 0)
 {
-    size_t bytes = std::max<size_t>(h.size() * sizeof(T), 16);
+    const size_t data = h.size() * sizeof(T);
+    size_t bytes = std::max<size_t>(data + pad, 16);
     void *p = nullptr;
     HIP_TRY(hipMalloc(&p, bytes), "hipMalloc (matrix)");
     allocs.push_back(p);
-    if (!h.empty()) HIP_TRY(hipMemcpy(p, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice), "hipMemcpy (matrix)");
+    if (bytes > data) HIP_TRY(hipMemset((char *)p + data, 0, bytes - data), "hipMemset (matrix)");
+    if (!h.empty()) HIP_TRY(hipMemcpy(p, h.data(), data, hipMemcpyHostToDevice), "hipMemcpy (matrix)");
     *out = (const T *)p;
     return DBS_OK;
 }
@@ -187,8 +191,8 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
     d.nseg = h->nseg;
     d.dtype = h->dtype;
     // primary order -> pull-segment slots (see DevMatrix)
-    std::vector<int32_t> sl_col, csc_slot, hv_slot;
-    std::vector<uint64_t> sl_desc;
+    std::vector<int32_t> sl_col, csc_slot, hv_col, hv_cstart, hv_crow;
+    std::vector<uint64_t> sl_desc, hv_desc;
     std::vector<uint32_t> seg_rs;
     try {
         const size_t nslots = (size_t)16 * (size_t)h->nseg;
@@ -207,10 +211,18 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
                 sl_desc[slot] = dd;
                 slot_of[first + i] = (int32_t)slot;
                 if (desc_type(dd) != T_COO) {
-                    // whole-wave block: pulled from the heavy list, flagged in
-                    // the slot by the sign bit of its block column
+                    // pulled from the non-COO list (flagged in the slot by the
+                    // sign bit of its block column); a new chunk starts at a
+                    // new block row or after HV_CHUNK blocks
                     sl_col[slot] |= (int32_t)0x80000000u;
-                    hv_slot.push_back((int32_t)slot);
+                    const int32_t brow = (int32_t)seg_brow(sg);
+                    if (hv_crow.empty() || hv_crow.back() != brow ||
+                        (int64_t)hv_col.size() - hv_cstart.back() == HV_CHUNK) {
+                        hv_cstart.push_back((int32_t)hv_col.size());
+                        hv_crow.push_back(brow);
+                    }
+                    hv_col.push_back(h->cb_col[first + i]);
+                    hv_desc.push_back(dd);
                     heavy = true;
                 }
             }
@@ -218,6 +230,7 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
             // places: its segments commit with atomics then
             seg_rs[s] = seg_brow(sg) | (seg_single(sg) && !heavy ? 0x80000000u : 0u);
         }
+        hv_cstart.push_back((int32_t)hv_col.size());
         csc_slot.resize((size_t)h->nblk);
         for (int64_t q = 0; q < h->nblk; ++q) csc_slot[q] = slot_of[h->csc2csr[q]];
     } catch (const std::bad_alloc &) {
@@ -235,13 +248,17 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
         (s2 = dev_upload(A->allocs, h->cb_ptr, &d.cb_ptr)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->csc_row, &d.csc_row)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, csc_slot, &d.csc_slot)) != DBS_OK ||
-        (s2 = dev_upload(A->allocs, hv_slot, &d.hv_slot)) != DBS_OK ||
-        (s2 = dev_upload(A->allocs, h->payload, &d.pay)) != DBS_OK) {
+        (s2 = dev_upload(A->allocs, hv_col, &d.hv_col)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, hv_desc, &d.hv_desc)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, hv_cstart, &d.hv_cstart)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, hv_crow, &d.hv_crow)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, h->payload, &d.pay, 16)) != DBS_OK) {
         free_all(A->allocs);
         delete A;
         return s2;
     }
-    d.nheavy = (int64_t)hv_slot.size();
+    d.nheavy = (int64_t)hv_col.size();
+    d.nchunk = (int64_t)hv_crow.size();
     fill_info(*h, &A->info);
     *out = A;
     return DBS_OK;

@@ -24,8 +24,8 @@
 //    (one x gather, which also tells whether x_j is stored); COO blocks with
 //    a record are taken entry-parallel by the whole wave (flat_pass), as are
 //    all record blocks in push.  Pull takes the other formats from an
-//    upload-time list ahead of the segment loop, one whole-wave block at a
-//    time (heavy_block).
+//    upload-time list ahead of the segment loop, in chunks of up to 16
+//    blocks of one block row, with one lane per row (pull_rows).
 //  * fp32 partial sums per row block go through LDS atomics (ds_add_f32), and
 //    are committed to an fp64 accumulator per row: a plain store when the
 //    block row has one segment, a global fp64 atomic otherwise.
@@ -401,8 +401,8 @@ __device__ __forceinline__ uint32_t inline_block_push(uint32_t vb, uint64_t d, i
 
 // COO blocks whose entries sit in the descriptor are processed by one lane
 // (no payload loads); COO blocks with a payload record are processed
-// entry-parallel by the whole wave (flat_pass); the other formats by the
-// whole wave, one block at a time (heavy_block).
+// entry-parallel by the whole wave (flat_pass); in pull, the other formats
+// row-per-lane from their own list (pull_rows).
 __device__ __forceinline__ bool lane_coo(uint64_t d) { return desc_inline(d); }
 __device__ __forceinline__ bool flat_coo(uint64_t d) { return !desc_inline(d) && desc_type(d) == T_COO; }
 
@@ -530,114 +530,6 @@ __device__ __forceinline__ uint32_t xd_raw(const void *xd, int64_t j)
     else return ((const uint16_t *)xd)[j];
 }
 
-// Whole wave, one block of a non-COO format.  Adds the row sums of the
-// admitted rows into dst16 (LDS); for BFS records the smallest active
-// column per row in pdst16.  Returns the rows hit (uniform).
-//   ForceCSR, patched CSR (row view) and ForceCSC (column view) are taken
-//   entry-parallel (Alg. 2 and 3 re-mapped to wave64): lane t takes entries
-//   t, t + 64, ...; it locates its entry's row and column from the record
-//   header, which every lane loads together with its values, then gathers
-//   x (value and presence in one word) -- two dependent loads in all,
-//   whatever the vector-block mask.
-//   Dense (Alg. 4): 4 lanes per row, 4 consecutive columns each.
-//   Boolean modes need only the masks (Alg. 5).
-template <int MODE>
-__device__ uint32_t heavy_block(const uint8_t *__restrict__ pay, uint32_t vb, uint64_t d, int32_t J,
-                                uint32_t mx, uint32_t am, const void *__restrict__ xd, float *dst16,
-                                int32_t *pdst16)
-{
-    const int lane = lane_id();
-    const uint32_t type = desc_type(d), nnz = desc_nnz(d);
-    const uint8_t *rec = pay + desc_off(d);
-    const uint16_t *msk = (const uint16_t *)(rec + HDR_MASK);
-    const int64_t xb = (int64_t)J * BS;
-
-    if constexpr (!valued<MODE>()) {
-        // Boolean propagation (Alg. 5): per row lane, the active columns with a
-        // stored entry; the first one is the smallest candidate parent.
-        const Hdr16 h = load_hdr(rec);
-        const uint32_t r = (uint32_t)lane & 15u;
-        uint32_t cand = 0, rm = 0;
-#pragma unroll
-        for (int t = 0; t < 16; ++t) {
-            const uint32_t mt = hdr_mask(h, t);
-            cand |= (((mx >> t) & (mt >> r)) & 1u) << t;  // ForceCSC: column masks
-            rm = (uint32_t)t == r ? mt : rm;             // the others: row masks
-        }
-        if (type != T_FCSC) cand = rm & mx;
-        bool hl = lane < 16 && cand != 0 && ((am >> r) & 1u);
-        uint32_t hits = (uint32_t)ballot(hl) & 0xFFFFu;
-        if constexpr (MODE == M_BFS) {
-            if (hl) atomicMin(&pdst16[r], (int32_t)xb + ctz32(cand));
-        }
-        return hits;
-    } else {
-        const uint32_t VB = VT<MODE>::VB;
-        if (type == T_DENSE) {
-            // Alg. 4 on wave64: 4 lanes per row, 4 consecutive columns each,
-            // one coalesced 1 KB (fp32) / 512 B (fp16) read of the block.
-            const int r = lane >> 2, c0 = (lane & 3) * 4;
-            const uint8_t *vrow = rec + HDR_START + (uint32_t)(r * BS + c0) * VB;
-            float s = 0.f;
-            if constexpr (MODE == M_F32) {
-                float4 v = *(const float4 *)vrow;
-                float4 x = *(const float4 *)((const float *)xd + xb + c0);
-                if ((mx >> (c0 + 0)) & 1u) s = fmaf(v.x, x.x, s);
-                if ((mx >> (c0 + 1)) & 1u) s = fmaf(v.y, x.y, s);
-                if ((mx >> (c0 + 2)) & 1u) s = fmaf(v.z, x.z, s);
-                if ((mx >> (c0 + 3)) & 1u) s = fmaf(v.w, x.w, s);
-            } else {
-                uint2 v = *(const uint2 *)vrow;
-                uint2 x = *(const uint2 *)((const uint16_t *)xd + xb + c0);
-                uint16_t vv[4] = {(uint16_t)v.x, (uint16_t)(v.x >> 16), (uint16_t)v.y, (uint16_t)(v.y >> 16)};
-                uint16_t xx[4] = {(uint16_t)x.x, (uint16_t)(x.x >> 16), (uint16_t)x.y, (uint16_t)(x.y >> 16)};
-#pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    if ((mx >> (c0 + k)) & 1u) s = fmaf(h2f(vv[k]), h2f(xx[k]), s);
-            }
-            s += __shfl_xor(s, 1, WAVE);
-            s += __shfl_xor(s, 2, WAVE);
-            const int rr = lane & 15;
-            float srow = __shfl(s, rr * 4, WAVE);
-            bool h = lane < 16 && (msk[rr] & mx) != 0 && ((am >> rr) & 1u);
-            uint32_t hits = (uint32_t)ballot(h) & 0xFFFFu;
-            if (h) atomicAdd(&dst16[rr], srow);
-            return hits;
-        }
-        // entry-parallel ForceCSR / patched CSR / ForceCSC
-        const bool colview = type == T_FCSC;
-        const uint8_t *vals = rec + values_at(type, nnz);
-        const Hdr16 h = load_hdr(rec);
-        uint32_t hl = 0;
-        for (uint32_t e0 = 0; e0 < nnz; e0 += 2 * WAVE) {
-            // two entries per lane per pass, loads issued together
-            const uint32_t e[2] = {e0 + (uint32_t)lane, e0 + WAVE + (uint32_t)lane};
-            float v[2];
-            uint32_t r[2], c[2], raw[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) v[u] = e[u] < nnz ? VT<MODE>::load(vals, e[u]) : 0.f;
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                uint32_t g, o;
-                hdr_locate(h, e[u], g, o);
-                r[u] = colview ? o : g;
-                c[u] = colview ? g : o;
-                const bool adm = e[u] < nnz && ((am >> r[u]) & 1u);
-                raw[u] = adm ? xd_raw<MODE>(xd, xb + c[u]) : (MODE == M_F32 ? X_ABSENT32 : X_ABSENT16);
-            }
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                if (raw[u] != (MODE == M_F32 ? X_ABSENT32 : X_ABSENT16)) {
-                    atomicAdd(&dst16[r[u]], v[u] * x_value<MODE>(raw[u]));
-                    hl |= 1u << r[u];
-                }
-            }
-        }
-        (void)VB;
-        return wave_or(hl);
-    }
-}
-
 // ---------------------------------------------------------------------------
 // main traversal kernel
 // ---------------------------------------------------------------------------
@@ -650,8 +542,11 @@ struct MainArgs {
     int32_t nbc;
     const int32_t *csc_row;
     const int32_t *csc_slot;
-    const int32_t *hv_slot;  // slots of the non-COO blocks (pull: whole-wave list)
-    int64_t nheavy;
+    const int32_t *hv_col;     // the non-COO list and its chunks (see DevMatrix)
+    const uint64_t *hv_desc;
+    const int32_t *hv_cstart;
+    const int32_t *hv_crow;
+    int64_t nchunk;
     int64_t nseg;
     const void *xd;
     const uint32_t *xmask;
@@ -951,50 +846,228 @@ extern __shared__ uint32_t lds_bits[];
 
 __device__ __forceinline__ bool block_active(int32_t J) { return (lds_bits[J >> 5] >> (J & 31)) & 1u; }
 
-// Pull: the non-COO blocks, listed at upload, spread over all waves ahead of
-// the segment loop.  Lane t of a wave loads the metadata of the wave's t-th
-// listed block (block column, block row, admitted rows, vector-block mask,
-// descriptor: all independent of each other, so they are in flight
-// together); the active blocks are then processed one at a time by the
-// whole wave (heavy_block) and committed with atomics (the segments of such
-// a block row commit with atomics as well).
-template <int MODE, bool LDSBITS>
-__device__ void pull_heavy(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp)
+// Pull: the non-COO blocks (Dense, ForceCSR, ForceCSC, patched CSR), listed
+// at upload in block-CSR order and cut into chunks of at most HV_CHUNK
+// consecutive blocks of one block row, spread over the workgroups ahead of
+// the segment loop (16 chunks per workgroup and round, 4 per wave).  A
+// quarter-wave takes a chunk with one lane per row of the block row:
+//  1. lane i loads the metadata of the chunk's i-th block (block column,
+//     activity, descriptor), then its record header (row masks and starts,
+//     or column masks and starts for ForceCSC) and its vector-block mask,
+//     all into the wave's LDS;
+//  2. the active blocks follow one at a time: lane r reads row r's mask and
+//     start (ForceCSC: every column's) from LDS, loads the 16 x words of the
+//     block's vector block and row r's matching values -- Dense: its 16
+//     values; the other formats: entry by entry (fp32), or (fp16) from a
+//     copy of the block's value array that the quarter brings into LDS with
+//     16-byte loads -- and forms row r's share of the block in registers
+//     (Alg. 2 and 4 with a row per lane; Alg. 3's column view for ForceCSC);
+//  3. lane r keeps an fp64 running sum of its per-block fp32 sums; the
+//     workgroup's chunks are then combined in LDS, each run of chunks of one
+//     block row summed there and committed with one atomic per row (the
+//     segments of such a block row commit with atomics as well).
+constexpr int HV_WORDS = 13;       // LDS words per staged block: 8 mask words, 4 start words, x mask
+constexpr int HV_VAL_BYTES = 512;  // per quarter: LDS copy of one fp16 block's value array
+
+// Raw bits of value i of a record's value array, and the per-lane value
+// words of pull_rows (fp32: one per column; fp16: two per word).
+template <int MODE>
+__device__ __forceinline__ uint32_t value_raw(const uint8_t *vals, uint32_t i)
 {
-    const int lane = lane_id();
-    for (int64_t h0 = gw; h0 < a.nheavy; h0 += (int64_t)nw * WAVE) {
-        const int64_t h = h0 + (int64_t)lane * nw;
-        const bool valid = h < a.nheavy;
-        const int32_t b = valid ? a.hv_slot[h] : 0;
-        const int32_t J = valid ? (a.sl_col[b] & 0x7FFFFFFF) : 0;
-        const int32_t R = valid ? (int32_t)(a.seg_rs[b >> 4] & 0x7FFFFFFFu) : 0;
+    if constexpr (MODE == M_F32) return ((const uint32_t *)vals)[i];
+    else return ((const uint16_t *)vals)[i];
+}
+template <int MODE, int N>
+__device__ __forceinline__ void put_value(uint32_t (&v)[N], int c, uint32_t raw)
+{
+    if constexpr (MODE == M_F32) v[c] = raw;
+    else if ((c & 1) == 0) v[c >> 1] = raw;
+    else v[c >> 1] |= raw << 16;
+}
+template <int MODE, int N>
+__device__ __forceinline__ float get_value(const uint32_t (&v)[N], int c)
+{
+    if constexpr (MODE == M_F32) return __uint_as_float(v[c]);
+    else return h2f((uint16_t)(v[c >> 1] >> ((c & 1) * 16)));
+}
+
+// Row r's matching values of a ForceCSR / patched-CSR (row view) or
+// ForceCSC (column view, header hs in LDS) block from its value array.
+template <int MODE, int N>
+__device__ __forceinline__ void row_values(const uint8_t *vals, bool colview, const uint32_t *hs, uint32_t rm,
+                                           uint32_t rs, uint32_t mx, uint32_t r, bool on, uint32_t (&v)[N])
+{
+    if (colview) {
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+            const uint32_t m = (hs[c >> 1] >> ((c & 1) * 16)) & 0xFFFFu;
+            const uint32_t st = (hs[8 + (c >> 2)] >> ((c & 3) * 8)) & 0xFFu;
+            const bool ld = on && (((mx >> c) & (m >> r)) & 1u);
+            put_value<MODE>(v, c, ld ? value_raw<MODE>(vals, st + __popc(m & ((1u << r) - 1u))) : 0u);
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+            const bool ld = on && (((rm & mx) >> c) & 1u);
+            put_value<MODE>(v, c, ld ? value_raw<MODE>(vals, rs + __popc(rm & ((1u << c) - 1u))) : 0u);
+        }
+    }
+}
+
+template <int MODE, bool LDSBITS>
+__device__ void pull_rows(const MainArgs &a, uint32_t *wg_lds, int slice_words)
+{
+    const int lane = lane_id(), q = lane >> 4, wv = threadIdx.x >> 6;
+    const uint32_t r = (uint32_t)lane & 15u;
+    uint32_t *hv = wg_lds + wv * slice_words;
+    uint8_t *qvals = (uint8_t *)(hv + HV_WORDS * WAVE) + q * HV_VAL_BYTES;
+    constexpr int CPG = 4 * (TPB / WAVE);  // chunks per workgroup and round
+    constexpr int VW = MODE == M_F16 ? 8 : 16;
+    for (int64_t c0 = (int64_t)blockIdx.x * CPG; c0 < a.nchunk; c0 += (int64_t)gridDim.x * CPG) {
+        const int64_t ch = c0 + wv * 4 + q;
+        const bool valid = ch < a.nchunk;
+        const int32_t h0 = valid ? a.hv_cstart[ch] : 0;
+        const int32_t h1 = valid ? a.hv_cstart[ch + 1] : 0;
+        const int32_t R = valid ? a.hv_crow[ch] : 0;
         const uint32_t am = valid ? row_admit(a, R) : 0u;
-        bool act = am != 0;
+        const int32_t h = h0 + (int32_t)r;
+        bool act = h < h1 && am != 0;
+        const int32_t J = act ? a.hv_col[h] : 0;
         if constexpr (LDSBITS) act = act && block_active(J);
         const uint32_t mx = act ? mask16(a.xmask, J) : 0u;
+        const uint64_t d = act ? a.hv_desc[h] : 0ull;
         act = act && mx != 0;
-        const uint64_t d = act ? a.sl_desc[b] : 0ull;
-        uint64_t m = ballot(act);
-        while (m) {
-            const int L = ctz64(m);
-            m &= m - 1;
-            const int32_t JL = (int32_t)readlane_u32((uint32_t)J, L), RL = (int32_t)readlane_u32((uint32_t)R, L);
-            const uint32_t mxL = readlane_u32(mx, L), amL = readlane_u32(am, L);
-            const uint64_t dL = readlane_u64(d, L);
-            const uint32_t hit = heavy_block<MODE>(a.pay, a.vb, dL, JL, mxL, amL, a.xd, sy, sp);
-            wave_lds_sync();
-            if (lane < 16) {
-                if ((hit >> lane) & 1u) {
-                    const int64_t row = (int64_t)RL * BS + lane;
-                    if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], (double)sy[lane]);
-                    if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], sp[lane]);
-                }
-                if constexpr (valued<MODE>()) sy[lane] = 0.f;
-                if constexpr (MODE == M_BFS) sp[lane] = INT_MAX;
-            }
-            if (lane == 0 && hit) or_mask16(a.ybits, RL, hit);
-            wave_lds_sync();
+        // 1. headers and x masks of the chunk's active blocks into LDS
+        if (act) {
+            const uint4 *hp = (const uint4 *)(a.pay + desc_off(d));
+            const uint4 m0 = hp[0], m1 = hp[1];
+            const uint4 st = desc_type(d) == T_DENSE ? make_uint4(0, 0, 0, 0) : hp[2];
+            uint32_t *dst = hv + lane * HV_WORDS;
+            dst[0] = m0.x; dst[1] = m0.y; dst[2] = m0.z; dst[3] = m0.w;
+            dst[4] = m1.x; dst[5] = m1.y; dst[6] = m1.z; dst[7] = m1.w;
+            dst[8] = st.x; dst[9] = st.y; dst[10] = st.z; dst[11] = st.w;
+            dst[12] = mx;
         }
+        wave_lds_sync();
+        uint32_t mine = (uint32_t)(ballot(act) >> (q * 16)) & 0xFFFFu;
+        const bool adm = (am >> r) & 1u;
+        double acc = 0.0;
+        int32_t pmin = INT_MAX;
+        uint32_t hit = 0;
+        // 2. the active blocks, one at a time per quarter
+        while (ballot(mine != 0)) {
+            const bool blk = mine != 0;  // the quarter has a block this round
+            const int src = q * 16 + (blk ? ctz32(mine) : 0);
+            mine &= mine - 1u;
+            const int32_t JB = __shfl(J, src, WAVE);
+            const uint64_t dB = shfl_u64(d, src);
+            const bool on = blk && adm;  // and lane r's row is admitted
+            const uint32_t *hs = hv + src * HV_WORDS;
+            const uint32_t type = desc_type(dB), nnz = desc_nnz(dB);
+            const uint32_t mxB = hs[12];
+            const uint32_t rm = (hs[r >> 1] >> ((r & 1) * 16)) & 0xFFFFu;   // row r's mask
+            const uint32_t rs = (hs[8 + (r >> 2)] >> ((r & 3) * 8)) & 0xFFu;  // row r's start
+            const uint8_t *rec = a.pay + desc_off(dB);
+            const bool colview = type == T_FCSC;
+            uint32_t w[16], v[VW];
+            bool staged = false;
+            if constexpr (valued<MODE>()) {
+                constexpr int NX = MODE == M_F32 ? 4 : 2;
+                const uint4 *xp = (const uint4 *)((const uint8_t *)a.xd + (int64_t)JB * BS * VT<MODE>::VB);
+#pragma unroll
+                for (int t = 0; t < NX; ++t) {
+                    const uint4 z = on ? xp[t] : make_uint4(0, 0, 0, 0);
+                    w[4 * t] = z.x; w[4 * t + 1] = z.y; w[4 * t + 2] = z.z; w[4 * t + 3] = z.w;
+                }
+                const uint8_t *vals = rec + values_at(type, nnz);
+                if (type == T_DENSE) {
+                    const uint4 *vp = (const uint4 *)(rec + HDR_START + r * BS * VT<MODE>::VB);
+#pragma unroll
+                    for (int t = 0; t < VW / 4; ++t) {
+                        const uint4 z = on ? vp[t] : make_uint4(0, 0, 0, 0);
+                        v[4 * t] = z.x; v[4 * t + 1] = z.y; v[4 * t + 2] = z.z; v[4 * t + 3] = z.w;
+                    }
+                } else if (MODE == M_F16 && nnz * 2 <= HV_VAL_BYTES) {
+                    // the block's value array into the quarter's LDS buffer,
+                    // 16 bytes per lane (every lane of the quarter helps)
+                    const uint4 *srcv = (const uint4 *)vals;
+                    const uint32_t nq = (nnz * 2 + 15) / 16;
+#pragma unroll
+                    for (int p = 0; p < HV_VAL_BYTES / 256; ++p) {
+                        const uint32_t k = (uint32_t)p * 16 + r;
+                        if (blk && k < nq) ((uint4 *)qvals)[k] = srcv[k];
+                    }
+                    staged = true;
+                } else {
+                    row_values<MODE>(vals, colview, hs, rm, rs, mxB, r, on, v);
+                }
+            }
+            if (ballot(staged)) {
+                wave_lds_sync();
+                if (staged) row_values<MODE>(qvals, colview, hs, rm, rs, mxB, r, on, v);
+                wave_lds_sync();  // the buffer is refilled for the next block
+            }
+            if (on) {
+                uint32_t cand = rm & mxB;
+                if (colview) {
+                    cand = 0;
+#pragma unroll
+                    for (int c = 0; c < 16; ++c) {
+                        const uint32_t m = (hs[c >> 1] >> ((c & 1) * 16)) & 0xFFFFu;
+                        cand |= (((mxB >> c) & (m >> r)) & 1u) << c;
+                    }
+                }
+                if (cand) {
+                    hit = 1u;
+                    if constexpr (valued<MODE>()) {
+                        float sb = 0.f;
+#pragma unroll
+                        for (int c = 0; c < 16; ++c)
+                            if ((cand >> c) & 1u) sb = fmaf(get_value<MODE>(v, c), get_value<MODE>(w, c), sb);
+                        acc += (double)sb;
+                    }
+                    if constexpr (MODE == M_BFS) pmin = min(pmin, JB * BS + (int32_t)ctz32(cand));
+                }
+            }
+        }
+        // 3. the workgroup's chunks of one block row are summed in LDS first:
+        // one commit per row and run of such chunks
+        wave_lds_sync();  // every lane is done with the staged headers
+        const uint32_t hq = or16_in_quarter(hit << r);
+        if constexpr (valued<MODE>()) ((double *)hv)[lane] = acc;
+        else ((int32_t *)hv)[2 * lane] = pmin;
+        if (r == 0) {
+            hv[128 + q] = valid ? (uint32_t)R : 0xFFFFFFFFu;
+            hv[132 + q] = hq;
+        }
+        __syncthreads();
+        {
+            const int c = threadIdx.x >> 4;
+            const uint32_t rr = threadIdx.x & 15u;
+            auto crow = [&](int cc) { return (int32_t)wg_lds[(cc >> 2) * slice_words + 128 + (cc & 3)]; };
+            const int32_t Rc = crow(c);
+            if (Rc >= 0 && (c == 0 || crow(c - 1) != Rc)) {
+                double sum = 0.0;
+                int32_t pm = INT_MAX;
+                uint32_t run = 0;
+                for (int cc = c; cc < CPG && crow(cc) == Rc; ++cc) {
+                    const uint32_t *sl = wg_lds + (cc >> 2) * slice_words;
+                    const uint32_t hm = sl[132 + (cc & 3)];
+                    run |= hm;
+                    if ((hm >> rr) & 1u) {
+                        if constexpr (valued<MODE>()) sum += ((const double *)sl)[(cc & 3) * 16 + rr];
+                        else pm = min(pm, ((const int32_t *)sl)[2 * ((cc & 3) * 16 + rr)]);
+                    }
+                }
+                if ((run >> rr) & 1u) {
+                    const int64_t row = (int64_t)Rc * BS + rr;
+                    if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], sum);
+                    if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], pm);
+                }
+                if (rr == 0 && run) or_mask16(a.ybits, Rc, run);
+            }
+        }
+        __syncthreads();  // the next round overwrites the slices
     }
 }
 
@@ -1050,7 +1123,7 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
         // flat_pass) the records of the stored COO blocks; the inline products
         // are formed while the record loads are in flight.  Blocks of the
         // other formats are not in the slots' work (negative block column):
-        // pull_heavy takes them.
+        // pull_rows takes them.
         uint32_t hit[SLOTS], cnt[SLOTS];
         uint32_t xr[SLOTS][IM];
 #pragma unroll
@@ -1264,6 +1337,9 @@ struct WaveLds {
     uint32_t acc[SLOTS * WAVE];  // row accumulators: fp32 sums, or BFS minimum parents
     HeavyStage<PUSH> hs;
 };
+static_assert(sizeof(WaveLds<false>) >= WAVE * HV_WORDS * sizeof(uint32_t) + 4 * HV_VAL_BYTES &&
+                  sizeof(WaveLds<false>) % 4 == 0,
+              "the non-COO pull pass stages its headers and chunk sums in a wave's LDS slice");
 
 
 // The traversal kernels (one per path).  Both are launched for an automatic
@@ -1283,10 +1359,13 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(Mai
     WaveLds<PATH == PATH_PUSH> &L = lds[w];
     float *sy = (float *)L.acc;
     int32_t *sp = (int32_t *)L.acc;
+    auto init_acc = [&]() {
 #pragma unroll
-    for (int k = 0; k < SLOTS; ++k) L.acc[k * WAVE + lane] = MODE == M_BFS ? (uint32_t)INT_MAX : 0u;
+        for (int k = 0; k < SLOTS; ++k) L.acc[k * WAVE + lane] = MODE == M_BFS ? (uint32_t)INT_MAX : 0u;
+    };
     const int gw = blockIdx.x * (TPB / WAVE) + w, nw = gridDim.x * (TPB / WAVE);
     if constexpr (PATH == PATH_PUSH) {
+        init_acc();
         wave_lds_sync();
         push_loop<MODE>(a, gw, nw, sy, sp, &L.hs);
     } else {
@@ -1297,11 +1376,15 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(Mai
         if (nwords <= LDS_BITMAP_WORDS) {
             for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
             __syncthreads();
-            pull_heavy<MODE, true>(a, gw, nw, sy, sp);
+            // the non-COO pass stages its headers over the wave's whole LDS slice
+            pull_rows<MODE, true>(a, (uint32_t *)lds, (int)(sizeof(WaveLds<false>) / 4));
+            init_acc();
+            wave_lds_sync();
             pull_loop<MODE, true>(a, gw, nw, sy, sp, &L.hs, spec);
         } else {
+            pull_rows<MODE, false>(a, (uint32_t *)lds, (int)(sizeof(WaveLds<false>) / 4));
+            init_acc();
             wave_lds_sync();
-            pull_heavy<MODE, false>(a, gw, nw, sy, sp);
             pull_loop<MODE, false>(a, gw, nw, sy, sp, &L.hs, spec);
         }
     }
@@ -1603,8 +1686,11 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
 {
     MainArgs a;
     a.sl_col = A.sl_col;
-    a.hv_slot = A.hv_slot;
-    a.nheavy = A.nheavy;
+    a.hv_col = A.hv_col;
+    a.hv_desc = A.hv_desc;
+    a.hv_cstart = A.hv_cstart;
+    a.hv_crow = A.hv_crow;
+    a.nchunk = A.nchunk;
     a.sl_desc = A.sl_desc;
     a.seg_rs = A.seg_rs;
     a.pay = A.pay;
@@ -1612,7 +1698,8 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
     a.nbc = A.nbc;
     a.csc_row = A.csc_row;
     a.csc_slot = A.csc_slot;
-    a.nseg = A.nseg;
+    // without COO blocks every block is in the non-COO list: no segment has work
+    a.nseg = A.nheavy < A.nblk ? A.nseg : 0;
     a.xd = xd;
     a.xmask = C.xmask;
     a.xbits = C.xbits;

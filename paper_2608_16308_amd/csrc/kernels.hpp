@@ -18,14 +18,21 @@ struct DevMatrix {
     int32_t m = 0, n = 0, nbr = 0, nbc = 0;
     int64_t nblk = 0, nseg = 0;
     int32_t dtype = 0;  // dbs_dtype
-    const int32_t *sl_col = nullptr;    // 16 nseg: block column, -1 = padding, sign bit = listed in hv_slot
+    const int32_t *sl_col = nullptr;    // 16 nseg: block column, -1 = padding, sign bit = non-COO (listed)
     const uint64_t *sl_desc = nullptr;  // 16 nseg: descriptor
     const uint32_t *seg_rs = nullptr;   // nseg: block row | 1 << 31 if the row has one segment
     const int32_t *cb_ptr = nullptr;    // block-CSC view: column pointer (nbc + 1)
     const int32_t *csc_row = nullptr;   // block row per CSC position
     const int32_t *csc_slot = nullptr;  // slot per CSC position
-    const int32_t *hv_slot = nullptr;   // slots of the non-COO blocks (pull: whole-wave list)
-    int64_t nheavy = 0;
+    // The non-COO blocks in block-CSR order (pull takes them row-per-lane,
+    // see pull_rows), cut into chunks of at most HV_CHUNK consecutive blocks
+    // of one block row: chunk c holds list entries hv_cstart[c] ..
+    // hv_cstart[c + 1] - 1 of block row hv_crow[c].
+    const int32_t *hv_col = nullptr;     // nheavy: block column
+    const uint64_t *hv_desc = nullptr;   // nheavy: descriptor
+    const int32_t *hv_cstart = nullptr;  // nchunk + 1
+    const int32_t *hv_crow = nullptr;    // nchunk
+    int64_t nheavy = 0, nchunk = 0;
     const uint8_t *pay = nullptr;
 };
 
@@ -44,6 +51,12 @@ enum Counter : int {
     C_COUNT = 12
 };
 constexpr int PATH_PUSH = 1, PATH_PULL = 2;
+#ifndef HV_CHUNK_BLOCKS
+#define HV_CHUNK_BLOCKS 16
+#endif
+// blocks per chunk of the non-COO list (at most one per lane of a quarter-wave)
+constexpr int HV_CHUNK = HV_CHUNK_BLOCKS;
+static_assert(HV_CHUNK >= 1 && HV_CHUNK <= 16, "chunk size");
 
 // Tile sizes of the look-back scans (vector blocks per thread of the active
 // block scan; 32-row structure words per workgroup of the y compaction).

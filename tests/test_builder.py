@@ -220,3 +220,22 @@ def test_device_calls_fail_cleanly_without_gpu():
     with pytest.raises(dbs.DbsError) as e:
         dbs.Matrix.upload(hm)
     assert e.value.status == _lib.DBS_ERR_DEVICE
+
+
+def test_basic_baseline_checks_input_before_any_device_call():
+    import torch
+    a = wl.random_csr(20, 20, 0.3, key=(2, 3))
+    col = a.col_idx.copy()
+    col[0] = 20
+    with pytest.raises(dbs.DbsError) as e:
+        dbs.BasicMatrix(a.m, a.n, a.row_ptr, col, a.vals)
+    assert e.value.status == _lib.DBS_ERR_ARG
+    rp = a.row_ptr.copy()
+    rp[5], rp[6] = rp[6], rp[5] - 1
+    with pytest.raises(dbs.DbsError) as e:
+        dbs.BasicMatrix(a.m, a.n, rp, a.col_idx, a.vals)
+    assert e.value.status == _lib.DBS_ERR_ARG
+    if not torch.cuda.is_available():
+        with pytest.raises(dbs.DbsError) as e:
+            dbs.BasicMatrix(a.m, a.n, a.row_ptr, a.col_idx, a.vals)
+        assert e.value.status == _lib.DBS_ERR_DEVICE
