@@ -848,26 +848,43 @@ __device__ __forceinline__ bool block_active(int32_t J) { return (lds_bits[J >> 
 
 // Pull: the non-COO blocks (Dense, ForceCSR, ForceCSC, patched CSR), listed
 // at upload in block-CSR order and cut into chunks of at most HV_CHUNK
-// consecutive blocks of one block row, spread over the workgroups ahead of
-// the segment loop (16 chunks per workgroup and round, 4 per wave).  A
-// quarter-wave takes a chunk with one lane per row of the block row:
-//  1. lane i loads the metadata of the chunk's i-th block (block column,
-//     activity, descriptor), then its record header (row masks and starts,
-//     or column masks and starts for ForceCSC) and its vector-block mask,
-//     all into the wave's LDS;
-//  2. the active blocks follow one at a time: lane r reads row r's mask and
-//     start (ForceCSC: every column's) from LDS, loads the 16 x words of the
-//     block's vector block and row r's matching values -- Dense: its 16
-//     values; the other formats: entry by entry (fp32), or (fp16) from a
-//     copy of the block's value array that the quarter brings into LDS with
-//     16-byte loads -- and forms row r's share of the block in registers
-//     (Alg. 2 and 4 with a row per lane; Alg. 3's column view for ForceCSC);
-//  3. lane r keeps an fp64 running sum of its per-block fp32 sums; the
-//     workgroup's chunks are then combined in LDS, each run of chunks of one
-//     block row summed there and committed with one atomic per row (the
-//     segments of such a block row commit with atomics as well).
-constexpr int HV_WORDS = 13;       // LDS words per staged block: 8 mask words, 4 start words, x mask
-constexpr int HV_VAL_BYTES = 512;  // per quarter: LDS copy of one fp16 block's value array
+// consecutive blocks of one block row, taken 16 chunks per workgroup and
+// round ahead of the segment loop:
+//  1. thread t (chunk t / 16, block t % 16 of it) loads its block's metadata
+//     (block column, activity, descriptor), then its record header (row
+//     masks and starts, or column masks and starts for ForceCSC) and its
+//     vector-block mask into LDS; the active blocks of the round are listed
+//     in LDS by a workgroup prefix sum;
+//  2. the 16 quarter-waves of the workgroup deal the listed blocks out
+//     round-robin (a chunk with more active blocks than others does not hold
+//     the round up), one lane per row of the block: lane r reads row r's mask
+//     and start (ForceCSC: every column's) from LDS, loads the 16 x words of
+//     the block's vector block and row r's matching values -- Dense: its 16
+//     values; the other formats: entry by entry (fp32), or (fp16) from a copy
+//     of the block's value array that the quarter brings into LDS with
+//     16-byte loads -- and forms row r's fp32 share of the block (Alg. 2 and 4
+//     with a row per lane; Alg. 3's column view for ForceCSC), added to the
+//     chunk's fp64 row accumulator in LDS;
+//  3. each run of the round's chunks of one block row is summed in LDS and
+//     committed with one fp64 atomic per row (the segments of such a block
+//     row commit with atomics as well).
+constexpr int HV_WORDS = 16;       // LDS words per staged block: 8 mask words, 4 start words,
+                                   // x mask | admitted rows << 16, block column, descriptor
+constexpr int HV_VAL_BYTES = 256;  // per quarter: LDS copy of one fp16 block's value array
+
+// LDS layout of the non-COO pass (32-bit words)
+template <int MODE> struct RowsLds {
+    static constexpr int NT = TPB;                 // staged blocks: one per thread
+    static constexpr int NQ = TPB / 16;            // quarter-waves = chunks per round
+    static constexpr int ST = 0;                                          // staged entries
+    static constexpr int VB = ST + NT * HV_WORDS;                         // fp16 value buffers
+    static constexpr int AC = VB + (MODE == M_F16 ? NQ * HV_VAL_BYTES / 4 : 0);  // fp64 [chunk][row]
+    static constexpr int HM = AC + NQ * 16 * 2;    // rows hit per chunk
+    static constexpr int CR = HM + NQ;             // block row per chunk (-1: none)
+    static constexpr int NI = CR + NQ;             // active blocks per wave
+    static constexpr int IT = NI + 8;              // listed blocks (staging index, one byte each)
+    static constexpr int WORDS = IT + NT / 4;
+};
 
 // Raw bits of value i of a record's value array, and the per-lane value
 // words of pull_rows (fp32: one per column; fp16: two per word).
@@ -915,16 +932,19 @@ __device__ __forceinline__ void row_values(const uint8_t *vals, bool colview, co
 }
 
 template <int MODE, bool LDSBITS>
-__device__ void pull_rows(const MainArgs &a, uint32_t *wg_lds, int slice_words)
+__device__ void pull_rows(const MainArgs &a, uint32_t *L)
 {
-    const int lane = lane_id(), q = lane >> 4, wv = threadIdx.x >> 6;
-    const uint32_t r = (uint32_t)lane & 15u;
-    uint32_t *hv = wg_lds + wv * slice_words;
-    uint8_t *qvals = (uint8_t *)(hv + HV_WORDS * WAVE) + q * HV_VAL_BYTES;
-    constexpr int CPG = 4 * (TPB / WAVE);  // chunks per workgroup and round
+    using Y = RowsLds<MODE>;
+    const int t = threadIdx.x, lane = lane_id(), wv = t >> 6, cs = t >> 4;
+    const uint32_t r = (uint32_t)t & 15u;
+    double *acc = (double *)(L + Y::AC);
+    int32_t *pacc = (int32_t *)(L + Y::AC);
+    uint8_t *items = (uint8_t *)(L + Y::IT);
+    uint8_t *qvals = (uint8_t *)(L + Y::VB) + cs * HV_VAL_BYTES;
     constexpr int VW = MODE == M_F16 ? 8 : 16;
-    for (int64_t c0 = (int64_t)blockIdx.x * CPG; c0 < a.nchunk; c0 += (int64_t)gridDim.x * CPG) {
-        const int64_t ch = c0 + wv * 4 + q;
+    for (int64_t c0 = (int64_t)blockIdx.x * Y::NQ; c0 < a.nchunk; c0 += (int64_t)gridDim.x * Y::NQ) {
+        // 1. metadata, headers and x masks of the round's blocks; the list of the active ones
+        const int64_t ch = c0 + cs;
         const bool valid = ch < a.nchunk;
         const int32_t h0 = valid ? a.hv_cstart[ch] : 0;
         const int32_t h1 = valid ? a.hv_cstart[ch + 1] : 0;
@@ -937,75 +957,84 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *wg_lds, int slice_words)
         const uint32_t mx = act ? mask16(a.xmask, J) : 0u;
         const uint64_t d = act ? a.hv_desc[h] : 0ull;
         act = act && mx != 0;
-        // 1. headers and x masks of the chunk's active blocks into LDS
         if (act) {
             const uint4 *hp = (const uint4 *)(a.pay + desc_off(d));
             const uint4 m0 = hp[0], m1 = hp[1];
             const uint4 st = desc_type(d) == T_DENSE ? make_uint4(0, 0, 0, 0) : hp[2];
-            uint32_t *dst = hv + lane * HV_WORDS;
+            uint32_t *dst = L + Y::ST + t * HV_WORDS;
             dst[0] = m0.x; dst[1] = m0.y; dst[2] = m0.z; dst[3] = m0.w;
             dst[4] = m1.x; dst[5] = m1.y; dst[6] = m1.z; dst[7] = m1.w;
             dst[8] = st.x; dst[9] = st.y; dst[10] = st.z; dst[11] = st.w;
-            dst[12] = mx;
+            dst[12] = mx | (am << 16);
+            dst[13] = (uint32_t)J;
+            dst[14] = (uint32_t)d;
+            dst[15] = (uint32_t)(d >> 32);
         }
-        wave_lds_sync();
-        uint32_t mine = (uint32_t)(ballot(act) >> (q * 16)) & 0xFFFFu;
-        const bool adm = (am >> r) & 1u;
-        double acc = 0.0;
-        int32_t pmin = INT_MAX;
-        uint32_t hit = 0;
-        // 2. the active blocks, one at a time per quarter
-        while (ballot(mine != 0)) {
-            const bool blk = mine != 0;  // the quarter has a block this round
-            const int src = q * 16 + (blk ? ctz32(mine) : 0);
-            mine &= mine - 1u;
-            const int32_t JB = __shfl(J, src, WAVE);
-            const uint64_t dB = shfl_u64(d, src);
-            const bool on = blk && adm;  // and lane r's row is admitted
-            const uint32_t *hs = hv + src * HV_WORDS;
+        if constexpr (valued<MODE>()) acc[t] = 0.0;
+        else pacc[t] = INT_MAX;
+        if (r == 0) {
+            L[Y::HM + cs] = 0u;
+            L[Y::CR + cs] = valid ? (uint32_t)R : 0xFFFFFFFFu;
+        }
+        const uint64_t bm = ballot(act);
+        if (lane == 0) L[Y::NI + wv] = (uint32_t)__popcll(bm);
+        __syncthreads();
+        uint32_t base = 0, total = 0;
+#pragma unroll
+        for (int w = 0; w < TPB / WAVE; ++w) {
+            const uint32_t cw = L[Y::NI + w];
+            base += w < wv ? cw : 0u;
+            total += cw;
+        }
+        if (act) items[base + __popcll(bm & ((1ull << lane) - 1ull))] = (uint8_t)t;
+        __syncthreads();
+        // 2. the listed blocks, round-robin over the quarter-waves
+        for (uint32_t it = (uint32_t)cs; ballot(it < total); it += Y::NQ) {
+            const bool blk = it < total;  // the quarter has a block
+            const int src = blk ? items[it] : 0;
+            const uint32_t *hs = L + Y::ST + src * HV_WORDS;
+            const int csB = src >> 4;
+            const uint32_t mxB = hs[12] & 0xFFFFu;
+            const bool on = blk && ((hs[12] >> (16 + r)) & 1u);  // and lane r's row is admitted
+            const int32_t JB = (int32_t)hs[13];
+            const uint64_t dB = (uint64_t)hs[14] | ((uint64_t)hs[15] << 32);
             const uint32_t type = desc_type(dB), nnz = desc_nnz(dB);
-            const uint32_t mxB = hs[12];
             const uint32_t rm = (hs[r >> 1] >> ((r & 1) * 16)) & 0xFFFFu;   // row r's mask
             const uint32_t rs = (hs[8 + (r >> 2)] >> ((r & 3) * 8)) & 0xFFu;  // row r's start
-            const uint8_t *rec = a.pay + desc_off(dB);
             const bool colview = type == T_FCSC;
             uint32_t w[16], v[VW];
             bool staged = false;
             if constexpr (valued<MODE>()) {
+                const uint8_t *rec = a.pay + desc_off(dB);
                 constexpr int NX = MODE == M_F32 ? 4 : 2;
                 const uint4 *xp = (const uint4 *)((const uint8_t *)a.xd + (int64_t)JB * BS * VT<MODE>::VB);
 #pragma unroll
-                for (int t = 0; t < NX; ++t) {
-                    const uint4 z = on ? xp[t] : make_uint4(0, 0, 0, 0);
-                    w[4 * t] = z.x; w[4 * t + 1] = z.y; w[4 * t + 2] = z.z; w[4 * t + 3] = z.w;
+                for (int k = 0; k < NX; ++k) {
+                    const uint4 z = on ? xp[k] : make_uint4(0, 0, 0, 0);
+                    w[4 * k] = z.x; w[4 * k + 1] = z.y; w[4 * k + 2] = z.z; w[4 * k + 3] = z.w;
                 }
                 const uint8_t *vals = rec + values_at(type, nnz);
                 if (type == T_DENSE) {
                     const uint4 *vp = (const uint4 *)(rec + HDR_START + r * BS * VT<MODE>::VB);
 #pragma unroll
-                    for (int t = 0; t < VW / 4; ++t) {
-                        const uint4 z = on ? vp[t] : make_uint4(0, 0, 0, 0);
-                        v[4 * t] = z.x; v[4 * t + 1] = z.y; v[4 * t + 2] = z.z; v[4 * t + 3] = z.w;
+                    for (int k = 0; k < VW / 4; ++k) {
+                        const uint4 z = on ? vp[k] : make_uint4(0, 0, 0, 0);
+                        v[4 * k] = z.x; v[4 * k + 1] = z.y; v[4 * k + 2] = z.z; v[4 * k + 3] = z.w;
                     }
                 } else if (MODE == M_F16 && nnz * 2 <= HV_VAL_BYTES) {
                     // the block's value array into the quarter's LDS buffer,
                     // 16 bytes per lane (every lane of the quarter helps)
-                    const uint4 *srcv = (const uint4 *)vals;
                     const uint32_t nq = (nnz * 2 + 15) / 16;
-#pragma unroll
-                    for (int p = 0; p < HV_VAL_BYTES / 256; ++p) {
-                        const uint32_t k = (uint32_t)p * 16 + r;
-                        if (blk && k < nq) ((uint4 *)qvals)[k] = srcv[k];
-                    }
+                    if (blk && r < nq) ((uint4 *)qvals)[r] = ((const uint4 *)vals)[r];
                     staged = true;
                 } else {
                     row_values<MODE>(vals, colview, hs, rm, rs, mxB, r, on, v);
                 }
-            }
-            if (ballot(staged)) {
-                wave_lds_sync();
-                if (staged) row_values<MODE>(qvals, colview, hs, rm, rs, mxB, r, on, v);
-                wave_lds_sync();  // the buffer is refilled for the next block
+                if (ballot(staged)) {
+                    wave_lds_sync();
+                    if (staged) row_values<MODE>(qvals, colview, hs, rm, rs, mxB, r, on, v);
+                    wave_lds_sync();  // the buffer is refilled for the next block
+                }
             }
             if (on) {
                 uint32_t cand = rm & mxB;
@@ -1018,45 +1047,34 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *wg_lds, int slice_words)
                     }
                 }
                 if (cand) {
-                    hit = 1u;
+                    atomicOr(&L[Y::HM + csB], 1u << r);
                     if constexpr (valued<MODE>()) {
                         float sb = 0.f;
 #pragma unroll
                         for (int c = 0; c < 16; ++c)
                             if ((cand >> c) & 1u) sb = fmaf(get_value<MODE>(v, c), get_value<MODE>(w, c), sb);
-                        acc += (double)sb;
+                        atomicAdd(&acc[csB * 16 + r], (double)sb);
                     }
-                    if constexpr (MODE == M_BFS) pmin = min(pmin, JB * BS + (int32_t)ctz32(cand));
+                    if constexpr (MODE == M_BFS) atomicMin(&pacc[csB * 16 + r], JB * BS + (int32_t)ctz32(cand));
                 }
             }
         }
-        // 3. the workgroup's chunks of one block row are summed in LDS first:
-        // one commit per row and run of such chunks
-        wave_lds_sync();  // every lane is done with the staged headers
-        const uint32_t hq = or16_in_quarter(hit << r);
-        if constexpr (valued<MODE>()) ((double *)hv)[lane] = acc;
-        else ((int32_t *)hv)[2 * lane] = pmin;
-        if (r == 0) {
-            hv[128 + q] = valid ? (uint32_t)R : 0xFFFFFFFFu;
-            hv[132 + q] = hq;
-        }
         __syncthreads();
+        // 3. one commit per row and run of the round's chunks of one block row
         {
-            const int c = threadIdx.x >> 4;
-            const uint32_t rr = threadIdx.x & 15u;
-            auto crow = [&](int cc) { return (int32_t)wg_lds[(cc >> 2) * slice_words + 128 + (cc & 3)]; };
-            const int32_t Rc = crow(c);
-            if (Rc >= 0 && (c == 0 || crow(c - 1) != Rc)) {
+            const int c = cs;
+            const uint32_t rr = r;
+            const int32_t Rc = (int32_t)L[Y::CR + c];
+            if (Rc >= 0 && (c == 0 || (int32_t)L[Y::CR + c - 1] != Rc)) {
                 double sum = 0.0;
                 int32_t pm = INT_MAX;
                 uint32_t run = 0;
-                for (int cc = c; cc < CPG && crow(cc) == Rc; ++cc) {
-                    const uint32_t *sl = wg_lds + (cc >> 2) * slice_words;
-                    const uint32_t hm = sl[132 + (cc & 3)];
+                for (int cc = c; cc < Y::NQ && (int32_t)L[Y::CR + cc] == Rc; ++cc) {
+                    const uint32_t hm = L[Y::HM + cc];
                     run |= hm;
                     if ((hm >> rr) & 1u) {
-                        if constexpr (valued<MODE>()) sum += ((const double *)sl)[(cc & 3) * 16 + rr];
-                        else pm = min(pm, ((const int32_t *)sl)[2 * ((cc & 3) * 16 + rr)]);
+                        if constexpr (valued<MODE>()) sum += acc[cc * 16 + rr];
+                        else pm = min(pm, pacc[cc * 16 + rr]);
                     }
                 }
                 if ((run >> rr) & 1u) {
@@ -1067,7 +1085,7 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *wg_lds, int slice_words)
                 if (rr == 0 && run) or_mask16(a.ybits, Rc, run);
             }
         }
-        __syncthreads();  // the next round overwrites the slices
+        __syncthreads();  // the next round overwrites the staging
     }
 }
 
@@ -1337,9 +1355,16 @@ struct WaveLds {
     uint32_t acc[SLOTS * WAVE];  // row accumulators: fp32 sums, or BFS minimum parents
     HeavyStage<PUSH> hs;
 };
-static_assert(sizeof(WaveLds<false>) >= WAVE * HV_WORDS * sizeof(uint32_t) + 4 * HV_VAL_BYTES &&
-                  sizeof(WaveLds<false>) % 4 == 0,
-              "the non-COO pull pass stages its headers and chunk sums in a wave's LDS slice");
+
+// LDS of a traversal kernel: the waves' slices, or (pull, before the
+// segment loop) the non-COO pass's layout over the same bytes
+template <int MODE, int PATH>
+constexpr size_t traverse_lds_bytes()
+{
+    const size_t waves = (TPB / WAVE) * sizeof(WaveLds<PATH == PATH_PUSH>);
+    const size_t rows = PATH == PATH_PULL ? RowsLds<MODE>::WORDS * sizeof(uint32_t) : 0;
+    return waves > rows ? waves : rows;
+}
 
 
 // The traversal kernels (one per path).  Both are launched for an automatic
@@ -1350,7 +1375,8 @@ static_assert(sizeof(WaveLds<false>) >= WAVE * HV_WORDS * sizeof(uint32_t) + 4 *
 template <int MODE, int PATH>
 __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(MainArgs a)
 {
-    __shared__ WaveLds<PATH == PATH_PUSH> lds[TPB / WAVE];
+    __shared__ __align__(16) uint8_t lds_raw[traverse_lds_bytes<MODE, PATH>()];
+    WaveLds<PATH == PATH_PUSH> *lds = (WaveLds<PATH == PATH_PUSH> *)lds_raw;
     // BFS: the host has read the frontier size of this level; restart the count
     if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
     const int32_t N = a.counters[C_NZBLK];
@@ -1377,16 +1403,39 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(Mai
             for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
             __syncthreads();
             // the non-COO pass stages its headers over the wave's whole LDS slice
-            pull_rows<MODE, true>(a, (uint32_t *)lds, (int)(sizeof(WaveLds<false>) / 4));
+            pull_rows<MODE, true>(a, (uint32_t *)lds_raw);
             init_acc();
             wave_lds_sync();
             pull_loop<MODE, true>(a, gw, nw, sy, sp, &L.hs, spec);
         } else {
-            pull_rows<MODE, false>(a, (uint32_t *)lds, (int)(sizeof(WaveLds<false>) / 4));
+            pull_rows<MODE, false>(a, (uint32_t *)lds_raw);
             init_acc();
             wave_lds_sync();
             pull_loop<MODE, false>(a, gw, nw, sy, sp, &L.hs, spec);
         }
+    }
+}
+
+// Pull for a matrix without COO blocks (every block is in the non-COO list,
+// as in a decode layer): the non-COO pass alone, in a kernel of its own so
+// that its registers do not compete with the segment loop's; one workgroup
+// per round of 16 chunks (the grid is sized to the chunks, not to
+// residency).
+template <int MODE>
+__global__ __launch_bounds__(TPB) void k_rows(MainArgs a)
+{
+    __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE>::WORDS];
+    // BFS: the host has read the frontier size of this level; restart the count
+    if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
+    const int32_t N = a.counters[C_NZBLK];
+    if (N == 0 || a.counters[C_PATH] != PATH_PULL) return;
+    const int32_t nwords = (a.nbc + 31) >> 5;
+    if (nwords <= LDS_BITMAP_WORDS) {
+        for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
+        __syncthreads();
+        pull_rows<MODE, true>(a, rows_lds);
+    } else {
+        pull_rows<MODE, false>(a, rows_lds);
     }
 }
 
@@ -1630,6 +1679,10 @@ static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStre
     const int64_t waves = PATH == PATH_PULL ? (A.nseg + 3) / 4 : (A.nblk + WAVE - 1) / WAVE;
     const int32_t nwords = (A.nbc + 31) >> 5;
     const size_t dyn = (PATH == PATH_PULL && nwords <= LDS_BITMAP_WORDS) ? (size_t)nwords * 4 : 0;
+    if (PATH == PATH_PULL && A.nblk > 0 && A.nheavy == A.nblk) {
+        hipLaunchKernelGGL((k_rows<MODE>), dim3(grid_for(A.nchunk, 4 * (TPB / WAVE), INT_MAX)), dim3(TPB), dyn, s, a);
+        return hipGetLastError();
+    }
     int g = grid_for(waves, TPB / WAVE, MAX_MAIN_GRID);
     const int cap = resident_grid<MODE, PATH>(dyn);
     if (g > cap) g = cap;
