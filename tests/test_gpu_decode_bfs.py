@@ -7,7 +7,7 @@ import oracle
 import oracle_pins
 import paper_2608_16308_amd as dbs
 import workloads as wl
-from gpu_helpers import REL_TOL, f16_ulp_dist, gpu_matrix, log, oracle_matrix, to_dev, torch_mod
+from gpu_helpers import REL_TOL, check_spmspv, f16_ulp_dist, gpu_matrix, log, oracle_matrix, to_dev, torch_mod
 
 pytestmark = pytest.mark.gpu
 
@@ -86,6 +86,10 @@ def bfs_check(ctx, A, om, source, policy, label):
         raise AssertionError(f"{label}: parent differs at {bad}: gpu {gp[bad]} ref {ep[bad]}")
     assert st["levels"] == nl, (st["levels"], nl)
     assert st["reached"] == int(np.sum(el >= 0))
+    # per-level frontier sizes (recorded on the device for the first 64 levels)
+    sizes = np.bincount(el[el >= 0], minlength=nl)
+    k = min(nl, 64)
+    assert st["frontier"][:k] == sizes[:k].tolist(), (st["frontier"][:k], sizes[:k].tolist())
     return st
 
 
@@ -147,3 +151,22 @@ def test_bfs_rmat_small(torch):
             st = bfs_check(ctx, A, om, int(s), pol, label)
             if pol == "auto":
                 log(f"  levels={st['levels']} paths={st['path']} frontier={st['frontier']}")
+
+
+def test_bfs_and_spmspv_share_a_context(torch):
+    """BFS levels are launched ahead of the host's termination check; the
+    scans that find a finished BFS must leave the context clean for the
+    calls after it (OR-AND SpMSpV, plus-times SpMSpV on another matrix of the
+    same size, another BFS)."""
+    a = wl.rmat(11, values=False)
+    b = wl.random_csr(a.m, a.n, 0.002, key=(31, 1))
+    A, B = gpu_matrix(a), gpu_matrix(b)
+    oa, ob = oracle_matrix(a), oracle_matrix(b)
+    ctx = dbs.Context(A)
+    srcs = [int(s) for s in wl.bfs_sources(a, 3, key=2)]
+    xi, xv = wl.sparse_x(a.n, 0.01, "uniform", key=(31, 2))
+    for rep in range(2):
+        for s in srcs:
+            bfs_check(ctx, A, oa, s, "auto", f"bfs rmat11 src={s} rep={rep}")
+            check_spmspv(ctx, A, oa, a, xi, None, semiring="or_and", label=f"or_and after bfs {s}")
+            check_spmspv(ctx, B, ob, b, xi, xv, label=f"plus_times after bfs {s}")
