@@ -184,13 +184,24 @@ def other_configs(args, torch, dbs, wl, dev, flush):
         lin = lambda: F.linear(xr, wd)
         lin_us = _time_call(torch, lin, reps)
         lin_cold = _cold_us(torch, lin, reps, flush)[0]
+        # batched decoding (several tokens per pass): warm us per call at nb
+        # activations, beside a dense F.linear of the same batch
+        batched = {}
+        for nb in (4, 8):
+            Xb = torch.from_numpy(np.stack([wl.decode_activation(in_f, key=kk) for kk in range(nb)])
+                                  .view(np.int16)).to(dev).view(torch.float16)
+            Yb = torch.empty((nb, out_f), dtype=torch.float16, device=dev)
+            bus = _time_call(torch, lambda: ctx.spmm_dense(A, Xb, Y=Yb), reps)
+            lus = _time_call(torch, lambda: F.linear(Xb, wd), reps)
+            batched[f"nb{nb}"] = {"us": round(bus, 2), "us_per_token": round(bus / nb, 2),
+                                  "dense_f16_linear_us": round(lus, 2)}
         layers.append({"shape": [out_f, in_f], "nnz": w.nnz, "blocks_by_type": info["blocks_by_type"],
                        "path": st["path"], "bytes": mod["bytes_total"], "us": round(us, 2),
                        "GBs": round(mod["bytes_total"] / (us * 1e-6) / 1e9, 1), "cold_us": round(cold, 2),
                        "cold_GBs": round(mod["bytes_total"] / (cold * 1e-6) / 1e9, 1),
                        "cold_traversal_GBs": round(mod["bytes_main"] / (cold_trav * 1e-6) / 1e9, 1),
                        "dense_f16_linear_us": round(lin_us, 2), "dense_f16_linear_cold_us": round(lin_cold, 2),
-                       "speedup_vs_dense_cold": round(lin_cold / cold, 2)})
+                       "speedup_vs_dense_cold": round(lin_cold / cold, 2), "batched": batched})
         log(f"[bench] decode {layers[-1]}")
         del ctx, A, wd
         torch.cuda.empty_cache()

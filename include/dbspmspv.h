@@ -248,6 +248,25 @@ dbs_status dbs_spmspv_dense(dbs_ctx *ctx, const dbs_matrix *A, const void *d_x_d
                             dbs_path path, float th3, void *d_y_dense, float *d_y_f32,
                             dbs_call_stats *stats);
 
+/* Batched sparse decode: Y = A X for nb dense activations at once (several
+ * tokens per pass), each as in dbs_spmspv_dense (Sec. 4.3); the paper leaves
+ * several vectors per pass (SpMM) to future work (Limitations).
+ *   d_x        nb x n activations, row-major, A's dtype (active iff nonzero)
+ *   d_y        nb x m outputs, row-major, A's dtype, rounded to nearest even
+ *              from the fp64 sums; d_y_f32 (NULL allowed) nb x m fp32 sums
+ *   nb         1 .. DBS_MAX_BATCH
+ * For a matrix without COO blocks (every block Dense / ForceCSR / ForceCSC /
+ * patched CSR, the regime of pruned decode layers) the nb vectors share one
+ * pull pass: the blocks active for any vector are visited once and every
+ * stored value is loaded once for all of them (the path is pull; N_nzblk in
+ * stats counts the union of the vectors' vector blocks).  Otherwise, or for
+ * nb = 1, the vectors are taken one dbs_spmspv_dense call each.  The first
+ * batched call allocates DBS_MAX_BATCH padded x copies and fp64 accumulator
+ * sets for the context's largest shape (kept until dbs_ctx_destroy).        */
+#define DBS_MAX_BATCH 8
+dbs_status dbs_spmm_dense(dbs_ctx *ctx, const dbs_matrix *A, int32_t nb, const void *d_x, void *d_y,
+                          float *d_y_f32, dbs_call_stats *stats);
+
 #define DBS_BFS_MAX_LEVEL_STATS 64
 typedef struct {
     int32_t levels;               /* nonempty levels including the source's */

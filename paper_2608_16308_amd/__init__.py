@@ -254,6 +254,18 @@ class Context:
                                      ctypes.byref(st) if st is not None else None))
         return (y[:m], _stats_dict(st)) if stats else y[:m]
 
+    def spmm_dense(self, A: Matrix, X, Y=None, Y32=None, stats=False):
+        """Batched dense activations X [nb, n] (active iff nonzero); returns Y [nb, m]."""
+        torch = self._torch
+        m, n = A.shape
+        nb = int(X.shape[0])
+        if Y is None:
+            Y = torch.empty((nb, max(m, 1)), dtype=X.dtype, device=X.device)
+        st = _lib.CallStats() if stats else None
+        check(lib().dbs_spmm_dense(self._h, A._h, nb, _ptr(X), _ptr(Y), _ptr(Y32),
+                                   ctypes.byref(st) if st is not None else None))
+        return (Y, _stats_dict(st)) if stats else Y
+
     def bfs(self, A: Matrix, source: int, policy="auto", th3=0.0, level=None, parent=None, stats=False):
         torch = self._torch
         m, n = A.shape

@@ -24,7 +24,7 @@ EXPORTED = [
     "dbs_build_opts_default", "dbs_host_build_csr", "dbs_host_info", "dbs_host_arrays_get",
     "dbs_host_destroy", "dbs_storage_model", "dbs_matrix_upload", "dbs_matrix_build_csr",
     "dbs_matrix_info_get", "dbs_matrix_destroy", "dbs_ctx_create", "dbs_ctx_set_stream",
-    "dbs_ctx_destroy", "dbs_spmspv", "dbs_spmspv_dense", "dbs_bfs", "dbs_ctx_enable_timing",
+    "dbs_ctx_destroy", "dbs_spmspv", "dbs_spmspv_dense", "dbs_spmm_dense", "dbs_bfs", "dbs_ctx_enable_timing",
     "dbs_ctx_read_timing", "dbs_last_error", "dbs_version", "dbs_basic_build", "dbs_basic_destroy",
     "dbs_basic_spmspv",
 ]
@@ -112,6 +112,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dbs_spmspv": (ctypes.c_int, [vp, vp, ctypes.c_int, i32, vp, vp, vp, ctypes.c_int, ctypes.c_int,
                                       f32, vp, vp, vp, P(CallStats)]),
         "dbs_spmspv_dense": (ctypes.c_int, [vp, vp, vp, ctypes.c_int, f32, vp, vp, P(CallStats)]),
+        "dbs_spmm_dense": (ctypes.c_int, [vp, vp, i32, vp, vp, vp, P(CallStats)]),
         "dbs_bfs": (ctypes.c_int, [vp, vp, i32, vp, vp, ctypes.c_int, f32, P(BfsStats)]),
         "dbs_ctx_enable_timing": (ctypes.c_int, [vp, ctypes.c_int]),
         "dbs_ctx_read_timing": (ctypes.c_int, [vp, P(Timing)]),

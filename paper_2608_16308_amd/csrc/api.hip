@@ -95,6 +95,10 @@ struct dbs_ctx {
     double ms[DBS_K_COUNT] = {0};
     int64_t launches[DBS_K_COUNT] = {0};
     bool broken = false;
+    // batched dense activations: DBS_MAX_BATCH padded x copies and
+    // accumulator sets, allocated by the first batched call
+    void *xdb = nullptr;
+    double *yaccb = nullptr;
 };
 
 namespace {
@@ -370,6 +374,8 @@ extern "C" void dbs_ctx_destroy(dbs_ctx *ctx)
     }
     for (auto e : ctx->pool) (void)hipEventDestroy(e);
     free_all(ctx->allocs);
+    if (ctx->xdb) (void)hipFree(ctx->xdb);
+    if (ctx->yaccb) (void)hipFree(ctx->yaccb);
     if (ctx->h_counters) (void)hipHostFree(ctx->h_counters);
     delete ctx;
 }
@@ -491,6 +497,55 @@ extern "C" dbs_status dbs_spmspv_dense(dbs_ctx *ctx, const dbs_matrix *A, const 
         stats->y_nnz = A->d.m;
         stats->tasks = h[C_PATH] == PATH_PUSH ? (int64_t)h[C_TASKS] : A->d.nseg;
         stats->error_flags = h[C_ERR_LAST];
+    }
+    return DBS_OK;
+}
+
+extern "C" dbs_status dbs_spmm_dense(dbs_ctx *ctx, const dbs_matrix *A, int32_t nb, const void *d_x,
+                                     void *d_y, float *d_y_f32, dbs_call_stats *stats)
+{
+    dbs_status st = check_ctx(ctx, A);
+    if (st != DBS_OK) return st;
+    if (A->d.dtype == DBS_PATTERN) return dbs_fail(DBS_ERR_ARG, "dense activations need a valued matrix");
+    if (nb < 1 || nb > DBS_MAX_BATCH) return dbs_fail(DBS_ERR_ARG, "nb = %d outside [1, %d]", nb, DBS_MAX_BATCH);
+    if (!d_x || !d_y) return dbs_fail(DBS_ERR_ARG, "NULL activations or outputs");
+    const int mode = A->d.dtype == DBS_F16 ? M_F16 : M_F32;
+    const size_t vb = A->d.dtype == DBS_F16 ? 2 : 4;
+    if (nb == 1 || A->d.nheavy < A->d.nblk || A->d.nblk == 0) {
+        // one vector, or a matrix with COO blocks (their segment loop is
+        // single-vector): one dense-activation call per vector
+        for (int32_t b = 0; b < nb; ++b) {
+            st = dbs_spmspv_dense(ctx, A, (const char *)d_x + (size_t)b * A->d.n * vb, DBS_PATH_AUTO, 0.f,
+                                  (char *)d_y + (size_t)b * A->d.m * vb, d_y_f32 ? d_y_f32 + (size_t)b * A->d.m : nullptr,
+                                  b + 1 == nb ? stats : nullptr);
+            if (st != DBS_OK) return st;
+        }
+        return DBS_OK;
+    }
+    if (!ctx->xdb) {
+        const size_t xb = (size_t)DBS_MAX_BATCH * BS * ctx->max_nbc * 4;
+        const size_t yb = (size_t)DBS_MAX_BATCH * BS * ctx->max_nbr * sizeof(double);
+        HIP_TRY(hipMalloc(&ctx->xdb, xb), "hipMalloc (batched x)");
+        HIP_TRY(hipMemset(ctx->xdb, 0, xb), "hipMemset (batched x)");
+        HIP_TRY(hipMalloc((void **)&ctx->yaccb, yb), "hipMalloc (batched y)");
+        HIP_TRY(hipMemset(ctx->yaccb, 0, yb), "hipMemset (batched y)");
+    }
+    const int32_t NB = nb <= 2 ? 2 : nb <= 4 ? 4 : 8;
+    const hipStream_t s = ctx->stream;
+    LAUNCH(ctx, DBS_K_SCATTER, launch_ballot_batch(A->d, ctx->c, mode, d_x, nb, NB, ctx->xdb, s));
+    LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, PATH_PULL, 0.0, s));
+    LAUNCH(ctx, DBS_K_MAIN, launch_rows_batch(A->d, ctx->c, mode, NB, ctx->xdb, ctx->yaccb, s));
+    LAUNCH(ctx, DBS_K_FINALIZE, launch_finalize_batch(A->d, ctx->c, mode, nb, NB, ctx->yaccb, d_y, d_y_f32, s));
+    if (stats) {
+        if ((st = sync_counters(ctx)) != DBS_OK) return st;
+        const int32_t *h = ctx->h_counters;
+        std::memset(stats, 0, sizeof *stats);
+        stats->path = PATH_PULL;
+        stats->n_nzblk = h[C_NZBLK];
+        stats->n_blk = A->d.nbc;
+        stats->y_nnz = A->d.m;
+        stats->tasks = A->d.nchunk;
+        stats->error_flags = 0;
     }
     return DBS_OK;
 }

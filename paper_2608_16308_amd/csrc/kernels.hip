@@ -549,6 +549,7 @@ struct MainArgs {
     int64_t nchunk;
     int64_t nseg;
     const void *xd;
+    int64_t xstride;        // batched pull: elements between the dense x of consecutive vectors
     const uint32_t *xmask;
     const uint32_t *xbits;       // one activity bit per vector block (global copy)
     const int32_t *act;          // push work items (see k_scan)
@@ -558,6 +559,7 @@ struct MainArgs {
     const uint32_t *omask;  // output mask bitmap (NULL = none); BFS: visited
     int32_t complement;
     double *yacc;
+    int64_t ystride;        // batched pull: accumulators between consecutive vectors
     uint32_t *ybits;        // y structure; BFS: next-frontier bitmap
     int32_t *parent;        // BFS only
 };
@@ -873,13 +875,13 @@ constexpr int HV_WORDS = 16;       // LDS words per staged block: 8 mask words, 
 constexpr int HV_VAL_BYTES = 256;  // per quarter: LDS copy of one fp16 block's value array
 
 // LDS layout of the non-COO pass (32-bit words)
-template <int MODE> struct RowsLds {
+template <int MODE, int NB = 1> struct RowsLds {
     static constexpr int NT = TPB;                 // staged blocks: one per thread
     static constexpr int NQ = TPB / 16;            // quarter-waves = chunks per round
     static constexpr int ST = 0;                                          // staged entries
     static constexpr int VB = ST + NT * HV_WORDS;                         // fp16 value buffers
-    static constexpr int AC = VB + (MODE == M_F16 ? NQ * HV_VAL_BYTES / 4 : 0);  // fp64 [chunk][row]
-    static constexpr int HM = AC + NQ * 16 * 2;    // rows hit per chunk
+    static constexpr int AC = VB + (MODE == M_F16 ? NQ * HV_VAL_BYTES / 4 : 0);  // fp64 [vector][chunk][row]
+    static constexpr int HM = AC + NB * NQ * 16 * 2;  // rows hit per chunk
     static constexpr int CR = HM + NQ;             // block row per chunk (-1: none)
     static constexpr int NI = CR + NQ;             // active blocks per wave
     static constexpr int IT = NI + 8;              // listed blocks (staging index, one byte each)
@@ -931,10 +933,15 @@ __device__ __forceinline__ void row_values(const uint8_t *vals, bool colview, co
     }
 }
 
-template <int MODE, bool LDSBITS>
+// NB > 1 (valued modes): NB vectors at once (batched decoding): the blocks
+// active for any of them are visited, each row value is loaded once and
+// multiplied with the NB dense x (zeros where a vector has no entry), and
+// the NB sums go to NB accumulator sets (x and accumulators NB-strided).
+template <int MODE, bool LDSBITS, int NB = 1>
 __device__ void pull_rows(const MainArgs &a, uint32_t *L)
 {
-    using Y = RowsLds<MODE>;
+    using Y = RowsLds<MODE, NB>;
+    static_assert(NB == 1 || valued<MODE>(), "batched pull is for valued modes");
     const int t = threadIdx.x, lane = lane_id(), wv = t >> 6, cs = t >> 4;
     const uint32_t r = (uint32_t)t & 15u;
     double *acc = (double *)(L + Y::AC);
@@ -970,8 +977,12 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *L)
             dst[14] = (uint32_t)d;
             dst[15] = (uint32_t)(d >> 32);
         }
-        if constexpr (valued<MODE>()) acc[t] = 0.0;
-        else pacc[t] = INT_MAX;
+        if constexpr (valued<MODE>()) {
+#pragma unroll
+            for (int b = 0; b < NB; ++b) acc[b * TPB + t] = 0.0;
+        } else {
+            pacc[t] = INT_MAX;
+        }
         if (r == 0) {
             L[Y::HM + cs] = 0u;
             L[Y::CR + cs] = valid ? (uint32_t)R : 0xFFFFFFFFu;
@@ -1049,11 +1060,26 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *L)
                 if (cand) {
                     atomicOr(&L[Y::HM + csB], 1u << r);
                     if constexpr (valued<MODE>()) {
-                        float sb = 0.f;
 #pragma unroll
-                        for (int c = 0; c < 16; ++c)
-                            if ((cand >> c) & 1u) sb = fmaf(get_value<MODE>(v, c), get_value<MODE>(w, c), sb);
-                        atomicAdd(&acc[csB * 16 + r], (double)sb);
+                        for (int b = 0; b < NB; ++b) {
+                            if (b > 0) {
+                                // vector b's x words (vector 0's were loaded with the values)
+                                constexpr int NX = MODE == M_F32 ? 4 : 2;
+                                const uint4 *xp = (const uint4 *)((const uint8_t *)a.xd +
+                                                                  ((int64_t)b * a.xstride + (int64_t)JB * BS) *
+                                                                      VT<MODE>::VB);
+#pragma unroll
+                                for (int k = 0; k < NX; ++k) {
+                                    const uint4 z = xp[k];
+                                    w[4 * k] = z.x; w[4 * k + 1] = z.y; w[4 * k + 2] = z.z; w[4 * k + 3] = z.w;
+                                }
+                            }
+                            float sb = 0.f;
+#pragma unroll
+                            for (int c = 0; c < 16; ++c)
+                                if ((cand >> c) & 1u) sb = fmaf(get_value<MODE>(v, c), get_value<MODE>(w, c), sb);
+                            atomicAdd(&acc[(b * Y::NQ + csB) * 16 + r], (double)sb);
+                        }
                     }
                     if constexpr (MODE == M_BFS) atomicMin(&pacc[csB * 16 + r], JB * BS + (int32_t)ctz32(cand));
                 }
@@ -1066,20 +1092,29 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *L)
             const uint32_t rr = r;
             const int32_t Rc = (int32_t)L[Y::CR + c];
             if (Rc >= 0 && (c == 0 || (int32_t)L[Y::CR + c - 1] != Rc)) {
-                double sum = 0.0;
+                double sum[NB];
+#pragma unroll
+                for (int b = 0; b < NB; ++b) sum[b] = 0.0;
                 int32_t pm = INT_MAX;
                 uint32_t run = 0;
                 for (int cc = c; cc < Y::NQ && (int32_t)L[Y::CR + cc] == Rc; ++cc) {
                     const uint32_t hm = L[Y::HM + cc];
                     run |= hm;
                     if ((hm >> rr) & 1u) {
-                        if constexpr (valued<MODE>()) sum += acc[cc * 16 + rr];
-                        else pm = min(pm, pacc[cc * 16 + rr]);
+                        if constexpr (valued<MODE>()) {
+#pragma unroll
+                            for (int b = 0; b < NB; ++b) sum[b] += acc[(b * Y::NQ + cc) * 16 + rr];
+                        } else {
+                            pm = min(pm, pacc[cc * 16 + rr]);
+                        }
                     }
                 }
                 if ((run >> rr) & 1u) {
                     const int64_t row = (int64_t)Rc * BS + rr;
-                    if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], sum);
+                    if constexpr (valued<MODE>()) {
+#pragma unroll
+                        for (int b = 0; b < NB; ++b) atomicAdd(&a.yacc[(int64_t)b * a.ystride + row], sum[b]);
+                    }
                     if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], pm);
                 }
                 if (rr == 0 && run) or_mask16(a.ybits, Rc, run);
@@ -1421,10 +1456,10 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(Mai
 // that its registers do not compete with the segment loop's; one workgroup
 // per round of 16 chunks (the grid is sized to the chunks, not to
 // residency).
-template <int MODE>
+template <int MODE, int NB>
 __global__ __launch_bounds__(TPB) void k_rows(MainArgs a)
 {
-    __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE>::WORDS];
+    __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE, NB>::WORDS];
     // BFS: the host has read the frontier size of this level; restart the count
     if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
     const int32_t N = a.counters[C_NZBLK];
@@ -1433,9 +1468,9 @@ __global__ __launch_bounds__(TPB) void k_rows(MainArgs a)
     if (nwords <= LDS_BITMAP_WORDS) {
         for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
         __syncthreads();
-        pull_rows<MODE, true>(a, rows_lds);
+        pull_rows<MODE, true, NB>(a, rows_lds);
     } else {
-        pull_rows<MODE, false>(a, rows_lds);
+        pull_rows<MODE, false, NB>(a, rows_lds);
     }
 }
 
@@ -1574,6 +1609,72 @@ __global__ __launch_bounds__(TPB) void k_finalize_dense(double *__restrict__ yac
     }
 }
 
+// Batched dense activations (nb vectors of n entries, row-major): the
+// NB-strided padded copies (zeros where an entry is zero, past n, or past
+// nb) and the union of their vector-block masks.
+template <int MODE>
+__global__ __launch_bounds__(TPB) void k_ballot_batch(const void *__restrict__ x, int32_t nb, int32_t n,
+                                                      int64_t xstride, int32_t NB, void *__restrict__ xdb,
+                                                      uint32_t *__restrict__ xmask, int32_t nwords)
+{
+    const int64_t lanes = (xstride + WAVE - 1) / WAVE * WAVE;  // per vector, whole waves
+    const int64_t g = (int64_t)blockIdx.x * TPB + threadIdx.x;
+    const int32_t b = (int32_t)(g / lanes);
+    const int64_t j = g - (int64_t)b * lanes;
+    if (b >= NB) return;  // whole waves: b is wave-uniform
+    bool nz = false;
+    if (j < xstride) {
+        if constexpr (MODE == M_F16) {
+            const uint16_t v = (b < nb && j < n) ? ((const uint16_t *)x)[(int64_t)b * n + j] : (uint16_t)0;
+            nz = (v & 0x7FFFu) != 0;
+            ((uint16_t *)xdb)[(int64_t)b * xstride + j] = nz ? v : (uint16_t)0;
+        } else {
+            const uint32_t v = (b < nb && j < n) ? ((const uint32_t *)x)[(int64_t)b * n + j] : 0u;
+            nz = (v & 0x7FFFFFFFu) != 0;
+            ((uint32_t *)xdb)[(int64_t)b * xstride + j] = nz ? v : 0u;
+        }
+    }
+    const uint64_t bits = ballot(nz);
+    if (lane_id() == 0 && bits) {
+        const int64_t w = (j - lane_id()) >> 5;
+        if (w < nwords && (uint32_t)bits) atomicOr(&xmask[w], (uint32_t)bits);
+        if (w + 1 < nwords && (uint32_t)(bits >> 32)) atomicOr(&xmask[w + 1], (uint32_t)(bits >> 32));
+    }
+}
+
+// Batched dense output: vector b < nb of y from its fp64 accumulators (RNE),
+// every accumulator set and the masks reset.
+template <int MODE>
+__global__ __launch_bounds__(TPB) void k_finalize_batch(double *__restrict__ yaccb, int64_t ystride, int32_t nb,
+                                                        int32_t NB, int32_t m, void *__restrict__ y,
+                                                        float *__restrict__ y32, uint32_t *__restrict__ ybits,
+                                                        int32_t nywords, uint32_t *__restrict__ xmask,
+                                                        int32_t nxwords, int32_t *__restrict__ counters)
+{
+    const int64_t stride = (int64_t)gridDim.x * TPB;
+    const int64_t tot = (int64_t)NB * m;
+    for (int64_t g = (int64_t)blockIdx.x * TPB + threadIdx.x; g < tot; g += stride) {
+        const int32_t b = (int32_t)(g / m);
+        const int64_t i = g - (int64_t)b * m;
+        double *pa = yaccb + (int64_t)b * ystride + i;
+        const double v = *pa;
+        if (b < nb) {
+            if constexpr (MODE == M_F32) ((float *)y)[g] = (float)v;
+            else ((uint16_t *)y)[g] = f64_to_f16_rne(v);
+            if (y32) y32[g] = (float)v;
+        }
+        *pa = 0.0;
+    }
+    for (int64_t i = (int64_t)blockIdx.x * TPB + threadIdx.x; i < nywords; i += stride) ybits[i] = 0u;
+    for (int64_t i = (int64_t)blockIdx.x * TPB + threadIdx.x; i < nxwords; i += stride) xmask[i] = 0u;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        counters[C_YNNZ] = m;
+        counters[C_ERR_LAST] = 0;
+        counters[C_XBAD] = 0;
+        counters[C_XPOP] = 0;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // BFS (Sec. 4.2)
 // ---------------------------------------------------------------------------
@@ -1680,7 +1781,7 @@ static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStre
     const int32_t nwords = (A.nbc + 31) >> 5;
     const size_t dyn = (PATH == PATH_PULL && nwords <= LDS_BITMAP_WORDS) ? (size_t)nwords * 4 : 0;
     if (PATH == PATH_PULL && A.nblk > 0 && A.nheavy == A.nblk) {
-        hipLaunchKernelGGL((k_rows<MODE>), dim3(grid_for(A.nchunk, 4 * (TPB / WAVE), INT_MAX)), dim3(TPB), dyn, s, a);
+        hipLaunchKernelGGL((k_rows<MODE, 1>), dim3(grid_for(A.nchunk, 4 * (TPB / WAVE), INT_MAX)), dim3(TPB), dyn, s, a);
         return hipGetLastError();
     }
     int g = grid_for(waves, TPB / WAVE, MAX_MAIN_GRID);
@@ -1733,11 +1834,9 @@ hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th
     return e;
 }
 
-hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
-                       const uint32_t *omask, int complement, int32_t *parent, int forced_path,
-                       hipStream_t s)
+static void fill_main_args(const DevMatrix &A, const DevCtx &C, int mode, const void *xd, const uint32_t *omask,
+                           int complement, int32_t *parent, MainArgs &a)
 {
-    MainArgs a;
     a.sl_col = A.sl_col;
     a.hv_col = A.hv_col;
     a.hv_desc = A.hv_desc;
@@ -1765,6 +1864,16 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
     a.yacc = C.yacc;
     a.ybits = mode == M_BFS ? C.nextm : C.ybits;
     a.parent = parent;
+    a.xstride = 0;
+    a.ystride = 0;
+}
+
+hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
+                       const uint32_t *omask, int complement, int32_t *parent, int forced_path,
+                       hipStream_t s)
+{
+    MainArgs a;
+    fill_main_args(A, C, mode, xd, omask, complement, parent, a);
     switch (mode) {
     case M_F32: return launch_paths<M_F32>(A, a, forced_path, s);
     case M_F16: return launch_paths<M_F16>(A, a, forced_path, s);
@@ -1804,6 +1913,68 @@ hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, 
         hipLaunchKernelGGL(k_finalize_dense<M_F16>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, C.nxwords, C.xd, A.n, C.counters);
     else
         hipLaunchKernelGGL(k_finalize_dense<M_F32>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, C.nxwords, C.xd, A.n, C.counters);
+    return hipGetLastError();
+}
+
+hipError_t launch_ballot_batch(const DevMatrix &A, const DevCtx &C, int mode, const void *x, int32_t nb,
+                               int32_t NB, void *xdb, hipStream_t s)
+{
+    const int64_t xstride = (int64_t)A.nbc * BS;
+    const int64_t lanes = (xstride + WAVE - 1) / WAVE * WAVE * NB;
+    dim3 g(grid_for(lanes, TPB, INT_MAX)), b(TPB);
+    if (mode == M_F16)
+        hipLaunchKernelGGL(k_ballot_batch<M_F16>, g, b, 0, s, x, nb, A.n, xstride, NB, xdb, C.xmask, C.nxwords);
+    else
+        hipLaunchKernelGGL(k_ballot_batch<M_F32>, g, b, 0, s, x, nb, A.n, xstride, NB, xdb, C.xmask, C.nxwords);
+    return hipGetLastError();
+}
+
+template <int MODE, int NB>
+static hipError_t launch_rows_nb(const DevMatrix &A, const MainArgs &a, hipStream_t s)
+{
+    const int32_t nwords = (A.nbc + 31) >> 5;
+    const size_t dyn = nwords <= LDS_BITMAP_WORDS ? (size_t)nwords * 4 : 0;
+    hipLaunchKernelGGL((k_rows<MODE, NB>), dim3(grid_for(A.nchunk, 4 * (TPB / WAVE), INT_MAX)), dim3(TPB), dyn, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_rows_batch(const DevMatrix &A, const DevCtx &C, int mode, int32_t NB, const void *xdb,
+                             double *yaccb, hipStream_t s)
+{
+    MainArgs a;
+    fill_main_args(A, C, mode, xdb, nullptr, 0, nullptr, a);
+    a.xstride = (int64_t)A.nbc * BS;
+    a.yacc = yaccb;
+    a.ystride = (int64_t)A.nbr * BS;
+    if (mode == M_F16) {
+        switch (NB) {
+        case 2: return launch_rows_nb<M_F16, 2>(A, a, s);
+        case 4: return launch_rows_nb<M_F16, 4>(A, a, s);
+        case 8: return launch_rows_nb<M_F16, 8>(A, a, s);
+        default: return hipErrorInvalidValue;
+        }
+    }
+    switch (NB) {
+    case 2: return launch_rows_nb<M_F32, 2>(A, a, s);
+    case 4: return launch_rows_nb<M_F32, 4>(A, a, s);
+    case 8: return launch_rows_nb<M_F32, 8>(A, a, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_finalize_batch(const DevMatrix &A, const DevCtx &C, int mode, int32_t nb, int32_t NB,
+                                 double *yaccb, void *y, float *y32, hipStream_t s)
+{
+    const int32_t nyw = (A.nbr + 1) / 2;
+    const int64_t items = (int64_t)NB * A.m > C.nxwords ? (int64_t)NB * A.m : C.nxwords;
+    dim3 g(grid_for(items, TPB, 4096)), b(TPB);
+    const int64_t ystride = (int64_t)A.nbr * BS;
+    if (mode == M_F16)
+        hipLaunchKernelGGL(k_finalize_batch<M_F16>, g, b, 0, s, yaccb, ystride, nb, NB, A.m, y, y32, C.ybits, nyw,
+                           C.xmask, C.nxwords, C.counters);
+    else
+        hipLaunchKernelGGL(k_finalize_batch<M_F32>, g, b, 0, s, yaccb, ystride, nb, NB, A.m, y, y32, C.ybits, nyw,
+                           C.xmask, C.nxwords, C.counters);
     return hipGetLastError();
 }
 

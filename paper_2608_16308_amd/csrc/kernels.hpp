@@ -114,6 +114,16 @@ hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_i
                            hipStream_t s);
 hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, void *y,
                                  float *y32, hipStream_t s);
+// Batched dense activations (NB in {2, 4, 8} vectors per pass, nb <= NB of
+// them real): the padded copies into xdb (NB * 16 nbc entries) and their
+// union mask; the pull over a matrix without COO blocks into yaccb (NB * 16
+// nbr accumulators); the dense outputs of the nb real vectors.
+hipError_t launch_ballot_batch(const DevMatrix &A, const DevCtx &C, int mode, const void *x, int32_t nb,
+                               int32_t NB, void *xdb, hipStream_t s);
+hipError_t launch_rows_batch(const DevMatrix &A, const DevCtx &C, int mode, int32_t NB, const void *xdb,
+                             double *yaccb, hipStream_t s);
+hipError_t launch_finalize_batch(const DevMatrix &A, const DevCtx &C, int mode, int32_t nb, int32_t NB,
+                                 double *yaccb, void *y, float *y32, hipStream_t s);
 hipError_t launch_bfs_init(const DevMatrix &A, const DevCtx &C, int32_t source, int32_t *level,
                            int32_t *parent, hipStream_t s);
 hipError_t launch_bfs_update(const DevMatrix &A, const DevCtx &C, int32_t next_level,

@@ -170,3 +170,85 @@ def test_bfs_and_spmspv_share_a_context(torch):
             bfs_check(ctx, A, oa, s, "auto", f"bfs rmat11 src={s} rep={rep}")
             check_spmspv(ctx, A, oa, a, xi, None, semiring="or_and", label=f"or_and after bfs {s}")
             check_spmspv(ctx, B, ob, b, xi, xv, label=f"plus_times after bfs {s}")
+
+
+# ---------------------------------------------------------------- batched decoding
+def check_batched(ctx, A, om, X, label):
+    """Y = A X for the rows of X (dense activations, A's dtype) against the
+    oracle vector by vector: fp16 outputs within 1 ulp of the RNE of the fp64
+    sum, fp32 sums within 1e-5 S."""
+    torch = torch_mod()
+    nb = X.shape[0]
+    Xd = to_dev(np.ascontiguousarray(X))
+    Y32 = torch.empty((nb, om.m), dtype=torch.float32, device="cuda:0")
+    Y, st = ctx.spmm_dense(A, Xd, Y32=Y32, stats=True)
+    torch.cuda.synchronize()
+    g = Y.cpu().numpy()
+    g32 = Y32.cpu().numpy()
+    for b in range(nb):
+        idx = np.nonzero(X[b] != 0)[0].astype(np.int32)
+        ri, rv, rs = om.spmspv(idx, X[b][idx].astype(np.float64))
+        y64 = np.zeros(om.m)
+        S = np.zeros(om.m)
+        y64[ri] = rv
+        S[ri] = rs
+        if X.dtype == np.float16:
+            d = f16_ulp_dist(g[b], y64.astype(np.float16))
+            assert d.max(initial=0) <= 1, f"{label} vector {b}: fp16 output off by {d.max()} ulp"
+        else:
+            assert oracle.within_tol(g[b].astype(np.float64), y64.astype(np.float32).astype(np.float64),
+                                     S, REL_TOL).all(), f"{label} vector {b}: fp32 output"
+        ok = oracle.within_tol(g32[b], y64, S, REL_TOL)
+        assert ok.all(), f"{label} vector {b}: {np.sum(~ok)} fp32 sums out of tolerance"
+    return st
+
+
+@pytest.mark.parametrize("nb", [1, 2, 3, 5, 8])
+def test_spmm_dense_decode_layer(torch, nb):
+    w = wl.decode_layer(512, 1024)
+    A, om = gpu_matrix(w), oracle_matrix(w)
+    assert A.info()["blocks_by_type"]["coo"] == 0  # the shared-pass regime
+    ctx = dbs.Context(A)
+    X = np.stack([wl.decode_activation(1024, key=k) for k in range(nb)])
+    if nb >= 3:
+        X[1] = 0  # an all-zero activation
+        X[2, :5] = np.float16(-0.0)
+    for rep in range(2):  # the second call checks that the scratch was left clean
+        label = f"spmm decode 512x1024 nb={nb} rep={rep}"
+        log(label)
+        check_batched(ctx, A, om, X, label)
+        # and the single-vector path on the same context afterwards
+        check_decode(ctx, A, om, X[0], "auto", label + " then single")
+
+
+@pytest.mark.parametrize("force", [1, 2, 3, 4])
+def test_spmm_dense_forced_formats_f32(torch, force):
+    a = wl.random_csr(100, 190, 0.35, key=(42, force))
+    A = gpu_matrix(a, dbs.default_opts(force_type=force))
+    om = oracle_matrix(a)
+    ctx = dbs.Context(A)
+    rng = wl.rng_for(wl.W_RAND, 43, force)
+    X = np.where(rng.random((6, a.n)) < 0.15, rng.uniform(-1, 1, (6, a.n)), 0.0).astype(np.float32)
+    label = f"spmm f32 force={force}"
+    log(label)
+    check_batched(ctx, A, om, X, label)
+
+
+def test_spmm_dense_matrix_with_coo_blocks(torch):
+    # a sparse layer has COO blocks: the vectors are taken one call each
+    w = wl.decode_layer(300, 640, keep=0.05)
+    A, om = gpu_matrix(w), oracle_matrix(w)
+    assert A.info()["blocks_by_type"]["coo"] > 0
+    ctx = dbs.Context(A)
+    X = np.stack([wl.decode_activation(640, key=k) for k in range(4)])
+    log("spmm decode with COO blocks nb=4")
+    check_batched(ctx, A, om, X, "spmm coo blocks")
+
+
+def test_spmm_dense_rejects_bad_batch(torch):
+    w = wl.decode_layer(64, 128)
+    A = gpu_matrix(w)
+    ctx = dbs.Context(A)
+    X = to_dev(np.zeros((9, 128), dtype=np.float16))
+    with pytest.raises(dbs.DbsError):
+        ctx.spmm_dense(A, X)
