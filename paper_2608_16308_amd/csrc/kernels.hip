@@ -885,11 +885,14 @@ template <int MODE, int NB = 1> struct RowsLds {
     static constexpr int CR = HM + NQ;             // block row per chunk (-1: none)
     static constexpr int NI = CR + NQ;             // active blocks per wave
     static constexpr int IT = NI + 8;              // listed blocks (staging index, one byte each)
-    static constexpr int WORDS = IT + NT / 4;
+    static constexpr int XQ = IT + NT / 4;         // fp16, one vector: x of the quarter's block (fp32)
+    static constexpr int WORDS = XQ + (MODE == M_F16 && NB == 1 ? NQ * 16 : 0);
 };
 
 // Raw bits of value i of a record's value array, and the per-lane value
 // words of pull_rows (fp32: one per column; fp16: two per word).
+typedef _Float16 h2_t __attribute__((ext_vector_type(2)));  // packed fp16 pair
+
 template <int MODE>
 __device__ __forceinline__ uint32_t value_raw(const uint8_t *vals, uint32_t i)
 {
@@ -1015,7 +1018,92 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *L)
             const bool colview = type == T_FCSC;
             uint32_t w[16], v[VW];
             bool staged = false;
-            if constexpr (valued<MODE>()) {
+            float sb1 = 0.f;  // fp16, one vector: row r's share, formed below
+            if constexpr (MODE == M_F16 && NB == 1) {
+                const uint8_t *rec = a.pay + desc_off(dB);
+                const uint8_t *vals = rec + values_at(type, nnz);
+                const uint4 *xp = (const uint4 *)((const uint8_t *)a.xd + (int64_t)JB * BS * 2);
+                if (type == T_DENSE) {
+                    // 16 values of row r against the 16 x, the pairs outside
+                    // the stored entries with a stored x masked to 0, two
+                    // products per packed dot instruction
+                    const uint32_t cm = rm & mxB;
+                    const uint4 *vp = (const uint4 *)(rec + HDR_START + r * BS * 2);
+#pragma unroll
+                    for (int k = 0; k < 2; ++k) {
+                        const uint4 z = on ? xp[k] : make_uint4(0, 0, 0, 0);
+                        const uint4 u = on ? vp[k] : make_uint4(0, 0, 0, 0);
+                        w[4 * k] = z.x; w[4 * k + 1] = z.y; w[4 * k + 2] = z.z; w[4 * k + 3] = z.w;
+                        v[4 * k] = u.x; v[4 * k + 1] = u.y; v[4 * k + 2] = u.z; v[4 * k + 3] = u.w;
+                    }
+#pragma unroll
+                    for (int p2 = 0; p2 < 8; ++p2) {
+                        const uint32_t keep = (((cm >> (2 * p2)) & 1u) ? 0x0000FFFFu : 0u) |
+                                              (((cm >> (2 * p2 + 1)) & 1u) ? 0xFFFF0000u : 0u);
+                        sb1 = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2_t, v[p2] & keep),
+                                                     __builtin_bit_cast(h2_t, w[p2] & keep), sb1, false);
+                    }
+                } else if (nnz * 2 <= HV_VAL_BYTES) {
+                    // the block's value array and its 16 x into the quarter's
+                    // LDS buffers (every lane of the quarter helps); then lane
+                    // r walks its matching entries only
+                    const uint32_t nq = (nnz * 2 + 15) / 16;
+                    if (blk && r < nq) ((uint4 *)qvals)[r] = ((const uint4 *)vals)[r];
+                    if (blk) {
+                        const uint16_t xr = ((const uint16_t *)xp)[r];
+                        ((float *)(L + Y::XQ))[cs * 16 + r] = ((mxB >> r) & 1u) ? h2f(xr) : 0.f;
+                    }
+                    staged = true;
+                } else {
+                    constexpr int NX = 2;
+#pragma unroll
+                    for (int k = 0; k < NX; ++k) {
+                        const uint4 z = on ? xp[k] : make_uint4(0, 0, 0, 0);
+                        w[4 * k] = z.x; w[4 * k + 1] = z.y; w[4 * k + 2] = z.z; w[4 * k + 3] = z.w;
+                    }
+                    row_values<MODE>(vals, colview, hs, rm, rs, mxB, r, on, v);
+                    uint32_t cand = rm & mxB;
+                    if (colview) {
+                        cand = 0;
+#pragma unroll
+                        for (int c = 0; c < 16; ++c) {
+                            const uint32_t m = (hs[c >> 1] >> ((c & 1) * 16)) & 0xFFFFu;
+                            cand |= (((mxB >> c) & (m >> r)) & 1u) << c;
+                        }
+                    }
+#pragma unroll
+                    for (int c = 0; c < 16; ++c)
+                        if ((cand >> c) & 1u) sb1 = fmaf(get_value<MODE>(v, c), get_value<MODE>(w, c), sb1);
+                }
+                if (ballot(staged)) {
+                    wave_lds_sync();
+                    if (staged && on) {
+                        const uint16_t *q16 = (const uint16_t *)qvals;
+                        const float *xq = (const float *)(L + Y::XQ) + cs * 16;
+                        if (colview) {
+                            // ForceCSC: row r's entry in each matching column
+#pragma unroll 1
+                            for (uint32_t mm = mxB; mm;) {
+                                const uint32_t c = ctz32(mm);
+                                mm &= mm - 1u;
+                                const uint32_t m = (hs[c >> 1] >> ((c & 1) * 16)) & 0xFFFFu;
+                                if ((m >> r) & 1u) {
+                                    const uint32_t st = (hs[8 + (c >> 2)] >> ((c & 3) * 8)) & 0xFFu;
+                                    sb1 = fmaf(h2f(q16[st + __popc(m & ((1u << r) - 1u))]), xq[c], sb1);
+                                }
+                            }
+                        } else {
+#pragma unroll 1
+                            for (uint32_t mm = rm & mxB; mm;) {
+                                const uint32_t c = ctz32(mm);
+                                mm &= mm - 1u;
+                                sb1 = fmaf(h2f(q16[rs + __popc(rm & ((1u << c) - 1u))]), xq[c], sb1);
+                            }
+                        }
+                    }
+                    wave_lds_sync();  // the buffers are refilled for the next block
+                }
+            } else if constexpr (valued<MODE>()) {
                 const uint8_t *rec = a.pay + desc_off(dB);
                 constexpr int NX = MODE == M_F32 ? 4 : 2;
                 const uint4 *xp = (const uint4 *)((const uint8_t *)a.xd + (int64_t)JB * BS * VT<MODE>::VB);
@@ -1059,7 +1147,9 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *L)
                 }
                 if (cand) {
                     atomicOr(&L[Y::HM + csB], 1u << r);
-                    if constexpr (valued<MODE>()) {
+                    if constexpr (MODE == M_F16 && NB == 1) {
+                        atomicAdd(&acc[csB * 16 + r], (double)sb1);
+                    } else if constexpr (valued<MODE>()) {
 #pragma unroll
                         for (int b = 0; b < NB; ++b) {
                             if (b > 0) {
