@@ -9,10 +9,11 @@ distinct element once per kernel that needs it:
   blocker   k indices + k values read, k values written to the dense x,
             4 B mask word update per index
   scan      2 B mask per vector block, and per active vector block 8 B of
-            block-CSC pointers read + 8 B (list entry, task offset) written
-  push      per active vector block 8 B list entry + task offset; per
-            visited block 4 B csc_row + 4 B slot + 8 B descriptor +
-            the record bytes its microkernel reads; 8 B per (block, row) fp64
+            block-CSC pointers read + a 16 B work item (first task, vector
+            block, block-CSC base) written
+  push      per active vector block its 16 B work item; per visited block
+            4 B block row + 8 B descriptor (both in block-CSC order) + the
+            record bytes its microkernel reads; 8 B per (block, row) fp64
             accumulator update; 4 B structure-mask update per block with hits
   pull      4 B per segment + 4 B block column per segment slot (16 per
             segment, padding included) + 2 B x-mask per scanned block; per
@@ -115,9 +116,9 @@ class BytesModel:
         useful = int(em.sum())
 
         blocker = k * (4 + V) + k * V + 4 * k
-        scan = 2 * self.nbc + 16 * N
+        scan = 2 * self.nbc + 24 * N
         if path == "push":
-            main = 16 * N + nact_blocks * (4 + 4 + 8) + rec_push + 8 * blk_rows + 4 * blks_hit
+            main = 16 * N + nact_blocks * (4 + 8) + rec_push + 8 * blk_rows + 4 * blks_hit
         else:
             main = 4 * self.nseg + 64 * self.nseg + 2 * self.nblk + 8 * nact_blocks + rec_pull \
                 + 8 * seg_rows + 4 * segs_hit

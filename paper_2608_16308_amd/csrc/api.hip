@@ -195,15 +195,14 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
     d.nseg = h->nseg;
     d.dtype = h->dtype;
     // primary order -> pull-segment slots (see DevMatrix)
-    std::vector<int32_t> sl_col, csc_slot, hv_col, hv_cstart, hv_crow;
-    std::vector<uint64_t> sl_desc, hv_desc;
+    std::vector<int32_t> sl_col, hv_col, hv_cstart, hv_crow;
+    std::vector<uint64_t> sl_desc, hv_desc, csc_desc;
     std::vector<uint32_t> seg_rs;
     try {
         const size_t nslots = (size_t)16 * (size_t)h->nseg;
         sl_col.assign(nslots, -1);
         sl_desc.assign(nslots, 0ull);
         seg_rs.resize((size_t)h->nseg);
-        std::vector<int32_t> slot_of((size_t)h->nblk);
         for (int64_t s = 0; s < h->nseg; ++s) {
             const uint64_t sg = h->seg[s];
             const uint32_t first = seg_first(sg), nb = seg_nb(sg);
@@ -213,7 +212,6 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
                 const uint64_t dd = h->desc[first + i];
                 sl_col[slot] = h->cb_col[first + i];
                 sl_desc[slot] = dd;
-                slot_of[first + i] = (int32_t)slot;
                 if (desc_type(dd) != T_COO) {
                     // pulled from the non-COO list (flagged in the slot by the
                     // sign bit of its block column); a new chunk starts at a
@@ -235,8 +233,8 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
             seg_rs[s] = seg_brow(sg) | (seg_single(sg) && !heavy ? 0x80000000u : 0u);
         }
         hv_cstart.push_back((int32_t)hv_col.size());
-        csc_slot.resize((size_t)h->nblk);
-        for (int64_t q = 0; q < h->nblk; ++q) csc_slot[q] = slot_of[h->csc2csr[q]];
+        csc_desc.resize((size_t)h->nblk);
+        for (int64_t q = 0; q < h->nblk; ++q) csc_desc[q] = h->desc[h->csc2csr[q]];
     } catch (const std::bad_alloc &) {
         delete A;
         return dbs_fail(DBS_ERR_ALLOC, "host allocation failed during upload");
@@ -251,7 +249,7 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
         (s2 = dev_upload(A->allocs, seg_rs, &d.seg_rs)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->cb_ptr, &d.cb_ptr)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->csc_row, &d.csc_row)) != DBS_OK ||
-        (s2 = dev_upload(A->allocs, csc_slot, &d.csc_slot)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, csc_desc, &d.csc_desc)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, hv_col, &d.hv_col)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, hv_desc, &d.hv_desc)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, hv_cstart, &d.hv_cstart)) != DBS_OK ||
@@ -326,9 +324,7 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
     if ((st = dev_zeros(ctx->allocs, (size_t)16 * nb, &xd, 0xFF)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &xmask)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)(nb + 31) / 32 + 64, &c.xbits)) != DBS_OK ||
-        (st = dev_zeros(ctx->allocs, (size_t)nbc + 1, &c.act)) != DBS_OK ||
-        (st = dev_zeros(ctx->allocs, (size_t)nbc + 2, &c.task_off)) != DBS_OK ||
-        (st = dev_zeros(ctx->allocs, (size_t)nbc + 1, &c.pbase)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)nbc + 2, &c.items)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)16 * nbr, &c.yacc)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.nywords, &ybits)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &visited)) != DBS_OK ||

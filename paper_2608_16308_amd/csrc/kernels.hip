@@ -216,15 +216,14 @@ __global__ __launch_bounds__(TPB) void k_ballot(const void *__restrict__ x, int3
 }
 
 // Single-pass scan over vector blocks.  Every nonzero vector block J whose
-// block column holds matrix blocks becomes one push work item:
-//   act[a] = J, task_off[a] = first task, pbase[a] = cb_ptr[J] - task_off[a]
-// so that task t of item a visits block-CSC position pbase[a] + t.  The last
+// block column holds matrix blocks becomes one push work item
+//   items[a] = {first task, J, pbase = cb_ptr[J] - first task, 0}
+// so that task t of item a visits block-CSC position pbase + t.  The last
 // tile fixes N_nzblk (counted by the blocker), the task totals and the
 // global path: push iff N_nzblk < th3 N_blk (Sec. 3.3.1).
 __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask,
                                               const int32_t *__restrict__ cb_ptr, int32_t nbc,
-                                              int32_t *__restrict__ act, int32_t *__restrict__ task_off,
-                                              int32_t *__restrict__ pbase,
+                                              int4 *__restrict__ items,
                                               uint32_t *__restrict__ xbits,
                                               int32_t *__restrict__ counters, uint64_t *status,
                                               uint64_t *next_status, int32_t n_status,
@@ -297,9 +296,7 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
         if (len[k]) {
-            act[idx] = base + k;
-            task_off[idx] = (int32_t)off;
-            pbase[idx] = start[k] - (int32_t)off;
+            items[idx] = make_int4((int32_t)off, base + k, start[k] - (int32_t)off, 0);
             ++idx;
             off += len[k];
         }
@@ -314,7 +311,7 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
         counters[C_NZBLK] = N;
         counters[C_NTB] = NT;
         counters[C_TASKS] = T;
-        task_off[NT] = T;
+        items[NT] = make_int4(T, 0, 0, 0);
         int path = forced_path;
         if (path == 0) path = ((double)N < th3 * (double)nbc) ? PATH_PUSH : PATH_PULL;
         counters[C_PATH] = path;
@@ -541,7 +538,7 @@ struct MainArgs {
     uint32_t vb;            // value bytes of the matrix (4, 2 or 0)
     int32_t nbc;
     const int32_t *csc_row;
-    const int32_t *csc_slot;
+    const uint64_t *csc_desc;
     const int32_t *hv_col;     // the non-COO list and its chunks (see DevMatrix)
     const uint64_t *hv_desc;
     const int32_t *hv_cstart;
@@ -552,9 +549,7 @@ struct MainArgs {
     int64_t xstride;        // batched pull: elements between the dense x of consecutive vectors
     const uint32_t *xmask;
     const uint32_t *xbits;       // one activity bit per vector block (global copy)
-    const int32_t *act;          // push work items (see k_scan)
-    const int32_t *task_off;
-    const int32_t *pbase;
+    const int4 *items;           // push work items (see k_scan)
     int32_t *counters;
     const uint32_t *omask;  // output mask bitmap (NULL = none); BFS: visited
     int32_t complement;
@@ -1346,6 +1341,7 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
 // arr[a] <= target (arr increasing, arr[0] = 0 <= target): a 64-ary search in
 // which the whole wave probes 64 positions per round (log64 n rounds), the
 // SLOTS searches interleaved so that their loads overlap.
+template <int STRIDE>
 __device__ __forceinline__ void wave_search(const int32_t *__restrict__ arr, int32_t n,
                                             const int32_t (&target)[SLOTS], const bool (&valid)[SLOTS],
                                             int32_t (&res)[SLOTS])
@@ -1367,7 +1363,7 @@ __device__ __forceinline__ void wave_search(const int32_t *__restrict__ arr, int
         for (int k = 0; k < SLOTS; ++k) {
             step[k] = (hi[k] - lo[k] + WAVE - 1) / WAVE;
             pi[k] = lo[k] + lane * step[k];
-            v[k] = (hi[k] - lo[k] > 1 && pi[k] < hi[k]) ? arr[pi[k]] : INT_MAX;
+            v[k] = (hi[k] - lo[k] > 1 && pi[k] < hi[k]) ? arr[(int64_t)pi[k] * STRIDE] : INT_MAX;
         }
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
@@ -1397,7 +1393,7 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
     const int64_t nchunks = ((int64_t)T + WAVE - 1) / WAVE;
     const int cpw = nchunks >= (int64_t)nw * SLOTS * 2 ? SLOTS : 1;
     for (int64_t u = gw; u * cpw < nchunks; u += nw) {
-        int32_t t[SLOTS], a0[SLOTS], B[SLOTS], tgt[SLOTS];
+        int32_t t[SLOTS], a0[SLOTS], B[SLOTS], tgt[SLOTS];  // B: first task of the lane's item
         bool vt[SLOTS], vc[SLOTS];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
@@ -1407,44 +1403,51 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             vt[k] = vc[k] && t[k] < T;
             tgt[k] = vc[k] ? (int32_t)(c * WAVE) : 0;
         }
-        wave_search(a.task_off, NT, tgt, vc, a0);
+        wave_search<4>((const int32_t *)a.items, NT, tgt, vc, a0);
+        // lane l holds item a0 + l (the chunk's first task lies in item a0,
+        // and at most 63 further items start inside the chunk): a 6-step
+        // search over the lanes' first tasks finds each lane's item, whose
+        // vector block and block-CSC base come along by shuffles
+        int32_t BJ[SLOTS], Bp[SLOTS];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
-            const int32_t w = a0[k] + 1 + lane;
-            B[k] = (vc[k] && w <= NT) ? a.task_off[w] : INT_MAX;
+            const int32_t w = a0[k] + lane;
+            const int4 itm = (vc[k] && w < NT) ? a.items[w] : make_int4(INT_MAX, 0, 0, 0);
+            B[k] = itm.x;
+            BJ[k] = itm.y;
+            Bp[k] = itm.z;
         }
-        int32_t it[SLOTS];
+        int32_t J[SLOTS], p[SLOTS];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
             int lo = 0;
 #pragma unroll
             for (int st = 32; st > 0; st >>= 1) {
-                const int32_t v = __shfl(B[k], lo + st - 1, WAVE);
-                if (v <= t[k]) lo += st;
+                const int32_t v = __shfl(B[k], (lo + st) & (WAVE - 1), WAVE);
+                if (lo + st < WAVE && v <= t[k]) lo += st;
             }
-            it[k] = a0[k] + lo;
+            J[k] = __shfl(BJ[k], lo, WAVE);
+            p[k] = __shfl(Bp[k], lo, WAVE) + t[k];
+            if (!vt[k]) {
+                J[k] = 0;
+                p[k] = 0;
+            }
         }
-        int32_t J[SLOTS], p[SLOTS];
-#pragma unroll
-        for (int k = 0; k < SLOTS; ++k) {
-            J[k] = vt[k] ? a.act[it[k]] : 0;
-            p[k] = vt[k] ? a.pbase[it[k]] + t[k] : 0;
-        }
-        int32_t R[SLOTS], bb[SLOTS];
+        int32_t R[SLOTS];
         uint32_t mx[SLOTS], am[SLOTS];
-#pragma unroll
-        for (int k = 0; k < SLOTS; ++k) {
-            R[k] = vt[k] ? a.csc_row[p[k]] : 0;
-            bb[k] = vt[k] ? a.csc_slot[p[k]] : 0;
-            mx[k] = vt[k] ? mask16(a.xmask, J[k]) : 0u;
-        }
         bool act[SLOTS];
         uint64_t d[SLOTS];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
+            R[k] = vt[k] ? a.csc_row[p[k]] : 0;
+            d[k] = vt[k] ? a.csc_desc[p[k]] : 0ull;
+            mx[k] = vt[k] ? mask16(a.xmask, J[k]) : 0u;
+        }
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
             am[k] = vt[k] ? row_admit(a, R[k]) : 0u;
             act[k] = vt[k] && am[k] != 0;
-            d[k] = act[k] ? a.sl_desc[bb[k]] : 0ull;
+            if (!act[k]) d[k] = 0ull;
         }
         uint32_t hit[SLOTS], cnt[SLOTS];
 #pragma unroll
@@ -1917,7 +1920,7 @@ hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th
 {
     dim3 g(grid_for(A.nbc, SCAN_TILE, INT_MAX)), b(TPB);
     const int p = C.scan_parity;
-    hipLaunchKernelGGL(k_scan, g, b, 0, s, C.xmask, A.cb_ptr, A.nbc, C.act, C.task_off, C.pbase,
+    hipLaunchKernelGGL(k_scan, g, b, 0, s, C.xmask, A.cb_ptr, A.nbc, C.items,
                        C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) C.scan_parity = 1 - p;
@@ -1939,15 +1942,13 @@ static void fill_main_args(const DevMatrix &A, const DevCtx &C, int mode, const 
     a.vb = A.dtype == 0 ? 4u : (A.dtype == 1 ? 2u : 0u);
     a.nbc = A.nbc;
     a.csc_row = A.csc_row;
-    a.csc_slot = A.csc_slot;
+    a.csc_desc = A.csc_desc;
     // without COO blocks every block is in the non-COO list: no segment has work
     a.nseg = A.nheavy < A.nblk ? A.nseg : 0;
     a.xd = xd;
     a.xmask = C.xmask;
     a.xbits = C.xbits;
-    a.act = C.act;
-    a.task_off = C.task_off;
-    a.pbase = C.pbase;
+    a.items = C.items;
     a.counters = C.counters;
     a.omask = omask;
     a.complement = complement;

@@ -12,8 +12,9 @@ namespace dbs {
 // slots: segment s owns slots [16 s, 16 s + 16), its blocks in block-CSR
 // order followed by padding (block column -1).  A pull lane thus finds its
 // block column and descriptor at 16 s + lane without first reading the
-// segment, and the block-CSC view maps to slots (csc_slot) instead of
-// primary ids.  The payload records are unchanged.
+// segment.  The block-CSC view holds each block's descriptor (csc_desc)
+// next to its block row instead of its primary id, so that push reaches a
+// block's record in one step.  The payload records are unchanged.
 struct DevMatrix {
     int32_t m = 0, n = 0, nbr = 0, nbc = 0;
     int64_t nblk = 0, nseg = 0;
@@ -23,7 +24,7 @@ struct DevMatrix {
     const uint32_t *seg_rs = nullptr;   // nseg: block row | 1 << 31 if the row has one segment
     const int32_t *cb_ptr = nullptr;    // block-CSC view: column pointer (nbc + 1)
     const int32_t *csc_row = nullptr;   // block row per CSC position
-    const int32_t *csc_slot = nullptr;  // slot per CSC position
+    const uint64_t *csc_desc = nullptr; // descriptor per CSC position
     // The non-COO blocks in block-CSR order (pull takes them row-per-lane,
     // see pull_rows), cut into chunks of at most HV_CHUNK consecutive blocks
     // of one block row: chunk c holds list entries hv_cstart[c] ..
@@ -77,9 +78,11 @@ struct DevCtx {
     uint32_t *xmask = nullptr;    // blk_x_mask, two 16-bit masks per word
     int32_t nxwords = 0;
     uint32_t *xbits = nullptr;    // one activity bit per vector block, written by the scan
-    int32_t *act = nullptr;       // push work items: active vector blocks with blocks, ascending (nbc)
-    int32_t *task_off = nullptr;  // their first task (exclusive scan of block-CSC lengths) (nbc + 1)
-    int32_t *pbase = nullptr;     // block-CSC position of task t of item a = pbase[a] + t (nbc)
+    // push work items, one per active vector block with blocks, ascending
+    // (nbc + 1): {first task (exclusive scan of block-CSC lengths), vector
+    // block, pbase, 0}; task t of item a visits block-CSC position pbase + t;
+    // item NT holds the task count
+    int4 *items = nullptr;
     double *yacc = nullptr;       // y accumulators (16 * nbr)
     uint32_t *ybits = nullptr;    // y structure, two 16-bit row-block masks per word
     int32_t nywords = 0;
