@@ -258,8 +258,14 @@ def run_ablation(args, torch, dbs, wl, dev):
                 c = round(math.exp(s0 + (s1 - s0) * (-l0) / (l1 - l0)), 4)
                 break
         cross[kind] = c
-    out["path_crossover"] = {"rows": rows, "crossover_s_b": cross}
-    log(f"[ablation] push/pull crossover in s_b: {cross}")
+    # the single th3 that minimises the summed time of all points (the
+    # selector's constant), next to the first sign change per kind
+    cands = sorted({0.001, 0.002, 0.005, 0.01, 0.015, 0.02, 0.03, 0.05, 0.08, 0.1, 0.15, 0.2, 0.3})
+    tot = {th: round(sum(r["push_us"] if r["s_b"] < th else r["pull_us"] for r in rows), 1) for th in cands}
+    best_th3 = min(tot, key=tot.get)
+    out["path_crossover"] = {"rows": rows, "crossover_s_b": cross, "summed_us_by_th3": tot, "best_th3": best_th3,
+                             "best_path_us": round(sum(min(r["push_us"], r["pull_us"]) for r in rows), 1)}
+    log(f"[ablation] push/pull crossover in s_b: {cross}; best single th3 {best_th3} ({tot[best_th3]} us summed)")
     del ctx, A
 
     # (1b) the basic push / pull of Alg. 1 (plain CSC / CSR, no blocks) on the
