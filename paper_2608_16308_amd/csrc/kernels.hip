@@ -39,7 +39,11 @@ namespace dbs {
 
 constexpr int TPB = 256;            // threads per workgroup (4 waves)
 constexpr int SCAN_ITEMS = SCAN_ITEMS_PER_THREAD;  // vector blocks per thread in the scan
-constexpr int SCAN_TILE = TPB * SCAN_ITEMS;
+#ifndef SCAN_TPB
+#define SCAN_TPB 256
+#endif
+constexpr int STPB = SCAN_TPB;                  // threads per scan workgroup
+constexpr int SCAN_TILE = STPB * SCAN_ITEMS;
 static_assert(SCAN_ITEMS == 1 || SCAN_ITEMS == 2 || SCAN_ITEMS == 4, "scan items");
 constexpr int MAX_MAIN_GRID = 4096; // upper bound: 256 CUs x 16 workgroups
 
@@ -108,6 +112,7 @@ __device__ uint64_t lookback(const uint64_t *status, int tile)
 
 // Workgroup exclusive scan of one uint64 per thread; returns the exclusive
 // value and writes the workgroup total to *total (all threads).
+template <int NTH = TPB>
 __device__ uint64_t block_exclusive_scan(uint64_t v, uint64_t *total, uint64_t *lds4)
 {
     const int lane = lane_id(), w = threadIdx.x >> 6;
@@ -121,7 +126,7 @@ __device__ uint64_t block_exclusive_scan(uint64_t v, uint64_t *total, uint64_t *
     __syncthreads();
     uint64_t before = 0, tot = 0;
 #pragma unroll
-    for (int i = 0; i < TPB / WAVE; ++i) {
+    for (int i = 0; i < NTH / WAVE; ++i) {
         uint64_t t = lds4[i];
         if (i < w) before += t;
         tot += t;
@@ -221,7 +226,7 @@ __global__ __launch_bounds__(TPB) void k_ballot(const void *__restrict__ x, int3
 // so that task t of item a visits block-CSC position pbase + t.  The last
 // tile fixes N_nzblk (counted by the blocker), the task totals and the
 // global path: push iff N_nzblk < th3 N_blk (Sec. 3.3.1).
-__global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask,
+__global__ __launch_bounds__(STPB) void k_scan(const uint32_t *__restrict__ xmask,
                                               const int32_t *__restrict__ cb_ptr, int32_t nbc,
                                               int4 *__restrict__ items,
                                               uint32_t *__restrict__ xbits,
@@ -229,11 +234,11 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
                                               uint64_t *next_status, int32_t n_status,
                                               int32_t forced_path, double th3)
 {
-    __shared__ uint64_t lds4[TPB / WAVE];
-    __shared__ uint64_t s_cnt[TPB / WAVE];
+    __shared__ uint64_t lds4[STPB / WAVE];
+    __shared__ uint64_t s_cnt[STPB / WAVE];
     __shared__ uint64_t s_prefix;
     // clear the other copy of the status words for the next scan
-    for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < n_status; i += gridDim.x * TPB)
+    for (int32_t i = blockIdx.x * STPB + threadIdx.x; i < n_status; i += gridDim.x * STPB)
         next_status[i] = 0;
     const int tile = blockIdx.x;
     const int32_t base = tile * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
@@ -266,7 +271,7 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
     uint64_t cnt2 = wave_sum(((uint64_t)pop << 32) | (uint64_t)__popc(nib));
     if (lane_id() == 0) s_cnt[threadIdx.x >> 6] = cnt2;
     uint64_t total;
-    uint64_t excl = block_exclusive_scan(mine, &total, lds4);
+    uint64_t excl = block_exclusive_scan<STPB>(mine, &total, lds4);
     if (threadIdx.x < WAVE) {
         uint64_t prefix = 0;
         if (threadIdx.x == 0) {
@@ -275,7 +280,7 @@ __global__ __launch_bounds__(TPB) void k_scan(const uint32_t *__restrict__ xmask
             // one) also sees their counts
             uint64_t c = 0;
 #pragma unroll
-            for (int i = 0; i < TPB / WAVE; ++i) c += s_cnt[i];
+            for (int i = 0; i < STPB / WAVE; ++i) c += s_cnt[i];
             if ((uint32_t)c) atomicAdd(&counters[C_NZACC], (int32_t)(uint32_t)c);
             if (c >> 32) atomicAdd(&counters[C_XPOP], (int32_t)(c >> 32));
             __threadfence();
@@ -1574,12 +1579,16 @@ __global__ __launch_bounds__(TPB) void k_rows(MainArgs a)
 // (its popcount enters the tile scan and the look-back); the rows are then
 // written in 32 rounds where thread t handles row t + 256 r of the tile, so
 // consecutive lanes touch consecutive accumulators and output slots.
+#ifndef FINALIZE_TPB
+#define FINALIZE_TPB 1024
+#endif
+constexpr int FTPB = FINALIZE_TPB;                 // threads per compaction workgroup
 constexpr int FIN_WORDS = FINALIZE_WORDS;
-constexpr int FIN_ROUNDS = FIN_WORDS * 32 / TPB;  // rows per thread
-static_assert(FIN_WORDS <= TPB && FIN_ROUNDS >= 1, "finalize tile");
+constexpr int FIN_ROUNDS = FIN_WORDS * 32 / FTPB;  // rows per thread
+static_assert(FIN_WORDS <= FTPB && FIN_ROUNDS >= 1, "finalize tile");
 
 template <int MODE>
-__global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, int32_t nywords,
+__global__ __launch_bounds__(FTPB) void k_finalize(uint32_t *__restrict__ ybits, int32_t nywords,
                                                   double *__restrict__ yacc, int32_t m,
                                                   int32_t *__restrict__ y_idx, void *__restrict__ y_val,
                                                   int32_t *__restrict__ y_nnz,
@@ -1589,15 +1598,15 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
                                                   const int32_t *__restrict__ x_idx, int32_t k,
                                                   int32_t n)
 {
-    __shared__ uint64_t lds4[TPB / WAVE];
+    __shared__ uint64_t lds4[FTPB / WAVE];
     __shared__ uint64_t s_prefix;
     __shared__ uint32_t s_word[FIN_WORDS];
     __shared__ uint32_t s_wpos[FIN_WORDS];
-    for (int32_t i = blockIdx.x * TPB + threadIdx.x; i < n_status; i += gridDim.x * TPB)
+    for (int32_t i = blockIdx.x * FTPB + threadIdx.x; i < n_status; i += gridDim.x * FTPB)
         next_status[i] = 0;
     // clear the blk_x_mask words this call's x indices touched, and put the
     // absent-entry marker back into the densified x
-    for (int32_t t = blockIdx.x * TPB + threadIdx.x; t < k; t += gridDim.x * TPB) {
+    for (int32_t t = blockIdx.x * FTPB + threadIdx.x; t < k; t += gridDim.x * FTPB) {
         const int32_t j = x_idx[t];
         if (j >= 0 && j < n) {
             xmask[j >> 5] = 0u;
@@ -1609,7 +1618,7 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
     const int32_t w = tile * FIN_WORDS + threadIdx.x;
     const uint32_t word = ((int)threadIdx.x < FIN_WORDS && w < nywords) ? ybits[w] : 0u;
     uint64_t total;
-    const uint64_t excl = block_exclusive_scan((uint64_t)__popc(word), &total, lds4);
+    const uint64_t excl = block_exclusive_scan<FTPB>((uint64_t)__popc(word), &total, lds4);
     if ((int)threadIdx.x < FIN_WORDS) {
         s_word[threadIdx.x] = word;
         s_wpos[threadIdx.x] = (uint32_t)excl;
@@ -1636,7 +1645,7 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
         uint32_t hm = 0;
 #pragma unroll
         for (int u = 0; u < FB; ++u) {
-            const int lr = (r0 + u) * TPB + threadIdx.x;  // row within the tile
+            const int lr = (r0 + u) * FTPB + threadIdx.x;  // row within the tile
             const uint32_t wd = s_word[lr >> 5];
             const bool h = (wd >> (lr & 31)) & 1u;
             hm |= (h ? 1u : 0u) << u;
@@ -1645,7 +1654,7 @@ __global__ __launch_bounds__(TPB) void k_finalize(uint32_t *__restrict__ ybits, 
 #pragma unroll
         for (int u = 0; u < FB; ++u) {
             if (!((hm >> u) & 1u)) continue;
-            const int lr = (r0 + u) * TPB + threadIdx.x;
+            const int lr = (r0 + u) * FTPB + threadIdx.x;
             const uint32_t wd = s_word[lr >> 5];
             const uint32_t bit = lr & 31;
             const int64_t pos = base_pos + s_wpos[lr >> 5] + __popc(wd & ((1u << bit) - 1u));
@@ -1918,7 +1927,7 @@ hipError_t launch_ballot(const DevMatrix &A, const DevCtx &C, int mode, const vo
 
 hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th3, hipStream_t s)
 {
-    dim3 g(grid_for(A.nbc, SCAN_TILE, INT_MAX)), b(TPB);
+    dim3 g(grid_for(A.nbc, SCAN_TILE, INT_MAX)), b(STPB);
     const int p = C.scan_parity;
     hipLaunchKernelGGL(k_scan, g, b, 0, s, C.xmask, A.cb_ptr, A.nbc, C.items,
                        C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3);
@@ -1980,7 +1989,7 @@ hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_i
                            int32_t *y_nnz, const int32_t *x_idx, int32_t k, hipStream_t s)
 {
     int32_t nyw = (A.nbr + 1) / 2;
-    dim3 g(grid_for(nyw, FIN_WORDS, INT_MAX)), b(TPB);
+    dim3 g(grid_for(nyw, FIN_WORDS, INT_MAX)), b(FTPB);
     const int p = C.fin_parity;
     uint64_t *st = C.st_fin[p], *nx = C.st_fin[1 - p];
     const int32_t ns = C.n_st_fin;

@@ -65,7 +65,7 @@ static_assert(HV_CHUNK >= 1 && HV_CHUNK <= 16, "chunk size");
 #define SCAN_ITEMS_PER_THREAD 4
 #endif
 #ifndef FINALIZE_WORDS
-#define FINALIZE_WORDS 64
+#define FINALIZE_WORDS 128
 #endif
 int32_t scan_tiles(int32_t nbc);      // workgroups (and status words) of the scan
 int32_t finalize_tiles(int32_t nbr);  // workgroups (and status words) of the compaction
