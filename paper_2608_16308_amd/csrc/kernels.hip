@@ -226,7 +226,12 @@ __global__ __launch_bounds__(TPB) void k_ballot(const void *__restrict__ x, int3
 // so that task t of item a visits block-CSC position pbase + t.  The last
 // tile fixes N_nzblk (counted by the blocker), the task totals and the
 // global path: push iff N_nzblk < th3 N_blk (Sec. 3.3.1).
-__global__ __launch_bounds__(STPB) void k_scan(const uint32_t *__restrict__ xmask,
+// DX (dense activation, MODE fp32 or fp16, n a multiple of 16, x 16-byte
+// aligned): the blocker is folded into the scan's front end -- each thread
+// reads the x of its vector blocks, writes their densified copy and masks.
+template <bool DX, int MODE>
+__global__ __launch_bounds__(STPB) void k_scan(uint32_t *__restrict__ xmask, const void *__restrict__ xdense,
+                                              void *__restrict__ xd,
                                               const int32_t *__restrict__ cb_ptr, int32_t nbc,
                                               int4 *__restrict__ items,
                                               uint32_t *__restrict__ xbits,
@@ -247,10 +252,59 @@ __global__ __launch_bounds__(STPB) void k_scan(const uint32_t *__restrict__ xmas
     uint64_t mine = 0;
     uint32_t nib = 0;  // activity of this thread's 4 vector blocks
     uint32_t pop = 0;  // stored x entries in them
+    uint32_t amk[SCAN_ITEMS];
+    if constexpr (DX) {
+        // 16 entries per vector block: the marker for zeros, the canonical
+        // NaN for an entry equal to the marker
+        constexpr int PER = MODE == M_F16 ? 8 : 4;  // entries per 16 bytes
+#pragma unroll
+        for (int k = 0; k < SCAN_ITEMS; ++k) {
+            const int32_t J = base + k;
+            uint32_t msk = 0;
+            if (J < nbc) {
+                const uint4 *src = (const uint4 *)xdense + (int64_t)J * (16 / PER);
+                uint4 *dst = (uint4 *)xd + (int64_t)J * (16 / PER);
+#pragma unroll
+                for (int q = 0; q < 16 / PER; ++q) {
+                    const uint4 v = src[q];
+                    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if constexpr (MODE == M_F16) {
+#pragma unroll
+                            for (int h = 0; h < 2; ++h) {
+                                const uint32_t hv = (w[e] >> (16 * h)) & 0xFFFFu;
+                                const bool nz = (hv & 0x7FFFu) != 0;
+                                const uint32_t o = !nz ? 0xFFFFu : hv == 0xFFFFu ? 0x7E00u : hv;
+                                w[e] = (w[e] & ~(0xFFFFu << (16 * h))) | (o << (16 * h));
+                                msk |= (nz ? 1u : 0u) << (q * 8 + e * 2 + h);
+                            }
+                        } else {
+                            const bool nz = (w[e] & 0x7FFFFFFFu) != 0;
+                            msk |= (nz ? 1u : 0u) << (q * 4 + e);
+                            w[e] = !nz ? 0xFFFFFFFFu : w[e] == 0xFFFFFFFFu ? 0x7FC00000u : w[e];
+                        }
+                    }
+                    dst[q] = make_uint4(w[0], w[1], w[2], w[3]);
+                }
+            }
+            amk[k] = msk;
+        }
+        // the masks of two consecutive vector blocks share a word
+#pragma unroll
+        for (int k = 0; k < SCAN_ITEMS; k += 2)
+            if (base + k < nbc) xmask[(base + k) >> 1] = amk[k] | (base + k + 1 < nbc ? amk[k + 1] << 16 : 0u);
+    } else {
+#pragma unroll
+        for (int k = 0; k < SCAN_ITEMS; ++k) {
+            const int32_t J = base + k;
+            amk[k] = J < nbc ? mask16(xmask, J) : 0u;
+        }
+    }
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
         const int32_t J = base + k;
-        const uint32_t am = J < nbc ? mask16(xmask, J) : 0u;
+        const uint32_t am = amk[k];
         nib |= (am ? 1u : 0u) << k;
         pop += __popc(am);
         start[k] = am ? cb_ptr[J] : 0;
@@ -1930,8 +1984,29 @@ hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th
 {
     dim3 g(grid_for(A.nbc, SCAN_TILE, INT_MAX)), b(STPB);
     const int p = C.scan_parity;
-    hipLaunchKernelGGL(k_scan, g, b, 0, s, C.xmask, A.cb_ptr, A.nbc, C.items,
+    hipLaunchKernelGGL((k_scan<false, 0>), g, b, 0, s, C.xmask, nullptr, nullptr, A.cb_ptr, A.nbc, C.items,
                        C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) C.scan_parity = 1 - p;
+    return e;
+}
+
+bool scan_takes_dense(const DevMatrix &A, const void *x_dense)
+{
+    return A.n % 16 == 0 && ((uintptr_t)x_dense & 15u) == 0 && SCAN_ITEMS % 2 == 0;
+}
+
+hipError_t launch_scan_dense(const DevMatrix &A, DevCtx &C, int mode, const void *x_dense, int forced_path,
+                             double th3, hipStream_t s)
+{
+    dim3 g(grid_for(A.nbc, SCAN_TILE, INT_MAX)), b(STPB);
+    const int p = C.scan_parity;
+    if (mode == M_F16)
+        hipLaunchKernelGGL((k_scan<true, M_F16>), g, b, 0, s, C.xmask, x_dense, C.xd, A.cb_ptr, A.nbc, C.items,
+                           C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3);
+    else
+        hipLaunchKernelGGL((k_scan<true, M_F32>), g, b, 0, s, C.xmask, x_dense, C.xd, A.cb_ptr, A.nbc, C.items,
+                           C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) C.scan_parity = 1 - p;
     return e;

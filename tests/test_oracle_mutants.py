@@ -5,8 +5,10 @@ dropped term, a wrong sign, a wrong index or bound, a skipped sort, a broken
 mask test), compiled with gcc into a temporary library on the CPU.  The pin
 suite of ``oracle_pins.py`` is then run against it and has to fail.
 """
+import json
 import os
 import subprocess
+import sys
 
 import pytest
 
@@ -35,6 +37,23 @@ MUTANTS = {
 }
 
 
+# The pins run against a mutant in a child process: a mutant may write out of
+# bounds, and its damage must not reach the test process.  A child that dies
+# (a mutant that crashes) has failed the pins as well.
+_CHILD = """
+import json, sys
+sys.path[:0] = [{tests!r}, {root!r}]
+import oracle_pins as pins
+caught = []
+for check in pins.ALL_CHECKS:
+    try:
+        check(lib_path={lib!r})
+    except (AssertionError, ValueError, IndexError) as e:
+        caught.append([check.__name__, type(e).__name__])
+print(json.dumps(caught), flush=True)
+"""
+
+
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_mutant_is_caught(name, tmp_path):
     old, new = MUTANTS[name]
@@ -45,11 +64,12 @@ def test_mutant_is_caught(name, tmp_path):
     msrc.write_text(mutated)
     lib = str(tmp_path / f"liboracle_{name}.so")
     subprocess.run(["gcc", "-O1", "-std=c11", "-fPIC", "-shared", "-o", lib, str(msrc)], check=True)
-    caught = []
-    for check in pins.ALL_CHECKS:
-        try:
-            check(lib_path=lib)
-        except (AssertionError, ValueError, IndexError) as e:  # noqa: PERF203
-            caught.append((check.__name__, type(e).__name__))
+    here = os.path.dirname(os.path.abspath(__file__))
+    code = _CHILD.format(tests=here, root=os.path.dirname(here), lib=lib)
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    if r.returncode == 0:
+        caught = json.loads(r.stdout.strip().splitlines()[-1])
+    else:
+        caught = [["child", f"exit status {r.returncode}"]]
     assert caught, f"mutant {name} survived every pin"
     os.remove(lib)
