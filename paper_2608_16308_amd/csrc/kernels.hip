@@ -493,22 +493,19 @@ __device__ __forceinline__ uint32_t inline_cd(uint64_t d, int e, uint32_t vb)
 }
 
 
-// Header of a 16-group record (the 16-bit row masks, or column masks for
-// ForceCSC, then the 8-bit group starts), read by every lane with three
-// 16-byte loads (records of these formats are 16-byte aligned).
-struct Hdr16 {
+// The 16 group masks at the head of a Dense, ForceCSR, ForceCSC or patched-CSR
+// record (row masks; column masks for ForceCSC), read with two 16-byte loads
+// (records of these formats are 16-byte aligned).
+struct Masks16 {
     uint32_t m[8];
-    uint32_t s[4];
 };
-__device__ __forceinline__ Hdr16 load_hdr(const uint8_t *rec)
+__device__ __forceinline__ Masks16 load_masks(const uint8_t *rec)
 {
     const uint4 a = ((const uint4 *)(rec + HDR_MASK))[0], b = ((const uint4 *)(rec + HDR_MASK))[1];
-    const uint4 c = *(const uint4 *)(rec + HDR_START);
-    return Hdr16{{a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w}, {c.x, c.y, c.z, c.w}};
+    return Masks16{{a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w}};
 }
 // (t is a constant after unrolling: no dynamic register indexing)
-__device__ __forceinline__ uint32_t hdr_mask(const Hdr16 &h, int t) { return (h.m[t >> 1] >> ((t & 1) * 16)) & 0xFFFFu; }
-__device__ __forceinline__ uint32_t hdr_start(const Hdr16 &h, int t) { return (h.s[t >> 2] >> ((t & 3) * 8)) & 0xFFu; }
+__device__ __forceinline__ uint32_t mask_at(const Masks16 &h, int t) { return (h.m[t >> 1] >> ((t & 1) * 16)) & 0xFFFFu; }
 
 // Position of the k-th (0-based) set bit of a 16-bit v, by halving.
 __device__ __forceinline__ uint32_t nth_bit16(uint32_t v, uint32_t k)
@@ -526,57 +523,57 @@ __device__ __forceinline__ uint32_t nth_bit16(uint32_t v, uint32_t k)
     return pos;
 }
 
-// Entry e of a 16-group record: its group (the last group starting at or
-// before e; empty groups start where the next one does) and its position
-// inside the group's mask.
-__device__ __forceinline__ void hdr_locate(const Hdr16 &h, uint32_t e, uint32_t &g, uint32_t &other)
+// Group t's mask restricted to the entries one push task has to multiply
+// (Sec. 3.3.3: the block's structure against blk_x_mask): entries whose column
+// is active in the vector-block mask mx and whose row is admitted (am).  The
+// groups of the row view are rows (bits: columns); ForceCSC groups are columns
+// (bits: rows).
+__device__ __forceinline__ uint32_t group_live(uint32_t type, int t, uint32_t gm, uint32_t mx, uint32_t am)
 {
-    uint32_t gg = 0, gs = 0, gm = 0;
-#pragma unroll
-    for (int t = 0; t < 16; ++t) {
-        const uint32_t st = hdr_start(h, t);
-        if (st <= e) {
-            gg = (uint32_t)t;
-            gs = st;
-            gm = hdr_mask(h, t);
-        }
-    }
-    g = gg;
-    other = nth_bit16(gm, e - gs);
+    if (type == T_FCSC) return ((mx >> t) & 1u) ? (gm & am) : 0u;
+    return ((am >> t) & 1u) ? (gm & mx) : 0u;
 }
 
-// Entry e (row-major; column-major for ForceCSC) of a Dense, ForceCSR,
-// ForceCSC or patched-CSR record: its local row and column and the index of
-// its value in the record's value array.  Dense records hold 16 row masks and
-// all 256 values; the row starts are the prefix sums of the row popcounts.
-__device__ __forceinline__ void hdr_entry(const uint8_t *rec, uint32_t type, uint32_t e, uint32_t &r,
-                                          uint32_t &c, uint32_t &vi)
+// Number of live entries of a record with the given masks.
+__device__ __forceinline__ uint32_t live_count(const Masks16 &h, uint32_t type, uint32_t mx, uint32_t am)
 {
-    Hdr16 h;
-    const uint4 m0 = ((const uint4 *)(rec + HDR_MASK))[0], m1 = ((const uint4 *)(rec + HDR_MASK))[1];
-    h.m[0] = m0.x; h.m[1] = m0.y; h.m[2] = m0.z; h.m[3] = m0.w;
-    h.m[4] = m1.x; h.m[5] = m1.y; h.m[6] = m1.z; h.m[7] = m1.w;
-    if (type == T_DENSE) {
-        uint32_t acc = 0;
+    uint32_t n = 0;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            uint32_t wv = 0;
+    for (int t = 0; t < 16; ++t) n += __popc(group_live(type, t, mask_at(h, t), mx, am));
+    return n;
+}
+
+// Live entry e (in record order: row-major, column-major for ForceCSC) of a
+// Dense, ForceCSR, ForceCSC or patched-CSR record: its local row and column
+// and the index of its value in the record's value array (Dense: r * 16 + c
+// over all 256 values; the others: the group's start plus the entry's rank in
+// the group's stored mask).
+__device__ __forceinline__ void live_entry(const uint8_t *rec, uint32_t type, uint32_t e, uint32_t mx, uint32_t am,
+                                           uint32_t &r, uint32_t &c, uint32_t &vi)
+{
+    const Masks16 h = load_masks(rec);
+    const uint4 st = *(const uint4 *)(rec + HDR_START);  // group starts (not read for Dense)
+    uint32_t before = 0, g = 0, gb = 0, gl = 0, gm = 0;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                wv |= acc << (8 * u);
-                acc += __popc(hdr_mask(h, 4 * t + u));
-            }
-            h.s[t] = wv;
+    for (int t = 0; t < 16; ++t) {
+        const uint32_t m = mask_at(h, t), l = group_live(type, t, m, mx, am);
+        if (l != 0u && before <= e) {
+            g = (uint32_t)t;
+            gb = before;
+            gl = l;
+            gm = m;
         }
-    } else {
-        const uint4 st = *(const uint4 *)(rec + HDR_START);
-        h.s[0] = st.x; h.s[1] = st.y; h.s[2] = st.z; h.s[3] = st.w;
+        before += __popc(l);
     }
-    uint32_t g, o;
-    hdr_locate(h, e, g, o);
+    const uint32_t o = nth_bit16(gl, e - gb);
     r = type == T_FCSC ? o : g;
     c = type == T_FCSC ? g : o;
-    vi = type == T_DENSE ? r * BS + c : e;
+    if (type == T_DENSE) {
+        vi = r * BS + c;
+    } else {
+        const uint32_t w = g < 8u ? (g < 4u ? st.x : st.y) : (g < 12u ? st.z : st.w);
+        vi = ((w >> ((g & 3u) * 8u)) & 0xFFu) + __popc(gm & ((1u << o) - 1u));
+    }
 }
 
 template <int MODE>
@@ -785,10 +782,11 @@ __device__ __forceinline__ FlatEntries flat_issue(const MainArgs &a, HeavyStage<
             cd = valid ? a.pay[off + (uint64_t)a.vb * nnz + e] : 0u;
             if constexpr (valued<MODE>()) f.val[j] = valid ? VT<MODE>::load(a.pay + off, e) : 0.f;
         } else if constexpr (ANYTYPE) {
-            // the other formats: locate the entry from the record header
+            // the other formats: the e-th live entry, located from the header
             if (valid) {
                 uint32_t r, c, vi;
-                hdr_entry(a.pay + off, type, e, r, c, vi);
+                const uint32_t ma = hs->mxam[o];
+                live_entry(a.pay + off, type, e, ma & 0xFFFFu, ma >> 16, r, c, vi);
                 cd = (r << 4) | c;
                 if constexpr (valued<MODE>()) f.val[j] = VT<MODE>::load(a.pay + off + values_at(type, nnz), vi);
             }
@@ -810,7 +808,10 @@ __device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> 
 #pragma unroll
     for (int j = 0; j < FLAT_E; ++j) {
         const uint32_t o = (f.ocd[j] >> 8) & 0xFFu, r = (f.ocd[j] >> 4) & 15u, c = f.ocd[j] & 15u;
-        const bool adm = (f.ocd[j] >> 31) && ((hs->mxam[o] >> (16 + r)) & 1u);
+        // with the vector-block mask staged, an entry whose column it lacks
+        // needs no gather
+        const bool adm = (f.ocd[j] >> 31) && ((hs->mxam[o] >> (16 + r)) & 1u) &&
+                         (!MXK || ((hs->mxam[o] >> c) & 1u));
         raw[j] = (adm && !known) ? x_gather<MODE>(a, hs->J[o] & 0x0FFFFFFF, c) : 0u;
         if (!adm) f.ocd[j] = 0u;
     }
@@ -1517,10 +1518,14 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
                 hit[k] = inline_block_push<MODE>(a.vb, d[k], J[k], R[k], mx[k], am[k], a.xd, a.yacc, a.parent);
             // every block with a payload record (stored COO and the other
             // formats) goes to the entry-parallel pass; the block column
-            // carries the format in its top bits there
+            // carries the format in its top bits there.  A COO record is
+            // walked whole; of the others only the live entries, counted
+            // from the record's masks
             const bool flat = act[k] && !desc_inline(d[k]);
             cnt[k] = flat ? desc_nnz(d[k]) : 0u;
-            if (flat)
+            if (flat && desc_type(d[k]) != T_COO)
+                cnt[k] = live_count(load_masks(a.pay + desc_off(d[k])), desc_type(d[k]), mx[k], am[k]);
+            if (cnt[k])
                 hs->stage(k * WAVE + lane, d[k], J[k] | (int32_t)(desc_type(d[k]) << 28), mx[k], am[k], R[k]);
         }
         if (ballot(cnt[0] | cnt[1] | cnt[2] | cnt[3])) {
