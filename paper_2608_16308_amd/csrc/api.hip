@@ -333,11 +333,14 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
         (st = dev_zeros(ctx->allocs, (size_t)c.n_st_scan, &c.st_scan[0])) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.n_st_scan, &c.st_scan[1])) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.n_st_fin, &c.st_fin[0])) != DBS_OK ||
-        (st = dev_zeros(ctx->allocs, (size_t)c.n_st_fin, &c.st_fin[1])) != DBS_OK) {
+        (st = dev_zeros(ctx->allocs, (size_t)c.n_st_fin, &c.st_fin[1])) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)compact_list_entries(sizing->d.nseg), &c.clist)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)compact_list_regions(), &c.ccount)) != DBS_OK) {
         free_all(ctx->allocs);
         delete ctx;
         return st;
     }
+    c.clist_cap = compact_list_entries(sizing->d.nseg);
     c.xd = xd;
     c.xmask = xmask;
     c.ybits = ybits;

@@ -613,6 +613,10 @@ struct MainArgs {
     int64_t ystride;        // batched pull: accumulators between consecutive vectors
     uint32_t *ybits;        // y structure; BFS: next-frontier bitmap
     int32_t *parent;        // BFS only
+    int32_t *clist;         // compacted pull: per-wave regions of active slot ids (NULL: not used)
+    uint32_t *ccount;       // compacted pull: entries per region
+    int64_t clist_cap;      // entries the list holds
+    int32_t nreg;           // compacted pull: regions (waves of the second kernel's grid)
 };
 
 // Independent work units per lane and loop iteration: four segments per
@@ -799,10 +803,11 @@ __device__ __forceinline__ FlatEntries flat_issue(const MainArgs &a, HeavyStage<
 // Gathers x for the entries and adds their products (see flat_pass).  MXK:
 // the staged word holds the block's vector-block mask, which then answers
 // the boolean modes' presence test without a gather.
-template <int MODE, bool PUSH, bool MXK>
+template <int MODE, bool PUSH, bool MXK, bool RUNS>
 __device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> *hs, FlatEntries f,
                                             float *sy, int32_t *sp)
 {
+    static_assert(!RUNS || PUSH, "the run destination uses the staged block rows");
     constexpr bool known = MXK && !valued<MODE>();
     uint32_t raw[FLAT_E];
 #pragma unroll
@@ -822,7 +827,12 @@ __device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> 
         const bool present = known ? ((hs->mxam[o] >> c) & 1u) != 0 : x_present<MODE>(raw[j], J, c);
         if ((f.ocd[j] >> 31) && present) {
             const int ko = (int)(o >> 6), lo = (int)(o & (WAVE - 1));
-            if constexpr (PUSH) {
+            if constexpr (RUNS) {
+                const int at = hs->R[o] * 16 + (int)r;
+                if constexpr (valued<MODE>()) atomicAdd(&sy[at], f.val[j] * x_value<MODE>(raw[j]));
+                if constexpr (MODE == M_BFS) atomicMin(&sp[at], J * BS + (int32_t)c);
+                atomicOr(&hs->hitw[o], 1u << r);
+            } else if constexpr (PUSH) {
                 const int64_t row = (int64_t)hs->R[o] * BS + r;
                 if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], (double)(f.val[j] * x_value<MODE>(raw[j])));
                 if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], J * BS + (int32_t)c);
@@ -850,7 +860,9 @@ __device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> 
 //         collected per slot quarter in hitw[slot * 4 + quarter].
 //   push: products go straight to the fp64 accumulators of the owner's
 //         block row; rows hit are collected per block in hitw[entry].
-template <int MODE, bool PUSH, bool MXK, bool ANYTYPE, class Between>
+//   runs (compacted pull): the staged row word is the owner's run; products
+//         go to the run's LDS rows, rows hit per block in hitw[entry].
+template <int MODE, bool PUSH, bool MXK, bool ANYTYPE, bool RUNS, class Between>
 __device__ void flat_pass(const MainArgs &a, HeavyStage<PUSH> *hs, const uint32_t (&cnt)[SLOTS],
                           const uint64_t (&d)[SLOTS], float *sy, int32_t *sp, Between &&between)
 {
@@ -877,10 +889,10 @@ __device__ void flat_pass(const MainArgs &a, HeavyStage<PUSH> *hs, const uint32_
     // caller's inline products are formed
     FlatEntries f = flat_issue<MODE, PUSH, ANYTYPE>(a, hs, cnt, excl, tot, 0u, carry);
     between();
-    flat_finish<MODE, PUSH, MXK>(a, hs, f, sy, sp);
+    flat_finish<MODE, PUSH, MXK, RUNS>(a, hs, f, sy, sp);
     for (uint32_t base = FLAT_W; base < tot; base += FLAT_W) {
         f = flat_issue<MODE, PUSH, ANYTYPE>(a, hs, cnt, excl, tot, base, carry);
-        flat_finish<MODE, PUSH, MXK>(a, hs, f, sy, sp);
+        flat_finish<MODE, PUSH, MXK, RUNS>(a, hs, f, sy, sp);
     }
     wave_lds_sync();
 }
@@ -1352,7 +1364,7 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
         };
         if (ballot(cnt[0] | cnt[1] | cnt[2] | cnt[3])) {
             wave_lds_sync();
-            flat_pass<MODE, false, !LDSBITS, false>(a, hs, cnt, d, sy, sp, inline_products);
+            flat_pass<MODE, false, !LDSBITS, false, false>(a, hs, cnt, d, sy, sp, inline_products);
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k) hit[k] |= hs->hitw[k * 4 + q];
         } else {
@@ -1394,6 +1406,90 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             if constexpr (MODE == M_BFS) sp[k * WAVE + lane] = INT_MAX;
         }
         wave_lds_sync();
+    }
+}
+
+// Compacted pull.  Below an activity threshold most slots of a segment have
+// nothing to multiply, and the segment loop pays its full chain of dependent
+// loads for a few useful lanes.  Instead, one kernel compacts the slots with
+// work into a list (k_pull_compact), and a second one (k_pull_active) runs
+// the same block work over the list, 256 active slots per wave and round,
+// with the products summed per run of one block row in LDS before the
+// commit; the pull kernel then takes only the non-COO blocks.  Used while
+// N_nzblk / N_blk is below PULL_COMPACT_PERMILLE / 1000 (the slot activity
+// roughly follows it).
+#ifndef PULL_COMPACT_PERMILLE
+#define PULL_COMPACT_PERMILLE 400
+#endif
+// Region r (wave r of k_pull_compact fills it, wave r of k_pull_active walks
+// it) covers spw consecutive segments and holds up to 16 spw entries.  False when the list is absent
+// or too small.
+__device__ __forceinline__ bool compact_pull(const MainArgs &a, int32_t N, int64_t &spw)
+{
+    const int nw = a.nreg;
+    spw = (a.nseg + nw - 1) / nw;
+    return a.clist != nullptr && a.nseg > 0 && (int64_t)N * 1000 < (int64_t)a.nbc * PULL_COMPACT_PERMILLE &&
+           (int64_t)nw * spw * 16 <= a.clist_cap;
+}
+
+// First half: wave gw takes segments [gw spw, (gw + 1) spw), one segment per
+// lane and round (its 16 block columns by four 16-byte loads), and appends
+// the slots that hold work -- a COO block (the listed non-COO blocks carry
+// the sign bit) whose vector block is active, in an admitted block row -- to
+// its own region, in slot order.  The region's entry count goes to
+// ccount[gw].  The activity bitmap is copied into LDS when it fits.
+template <bool LDSBITS>
+__device__ void pull_compact(const MainArgs &a, int gw, int64_t spw)
+{
+    const int lane = lane_id();
+    const int64_t s0 = (int64_t)gw * spw;
+    const int64_t s1 = min(a.nseg, s0 + spw);
+    int32_t *out = a.clist + s0 * 16;
+    uint32_t n = 0;
+    for (int64_t base = s0; base < s1; base += WAVE) {
+        const int64_t sid = base + lane;
+        uint32_t f = 0;
+        if (sid < s1) {
+            const int4 *p = (const int4 *)(a.sl_col + sid * 16);
+            const int4 c0 = p[0], c1 = p[1], c2 = p[2], c3 = p[3];
+            const uint32_t am = row_admit(a, (int32_t)(a.seg_rs[sid] & 0x7FFFFFFFu));
+            const int32_t col[16] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w,
+                                     c2.x, c2.y, c2.z, c2.w, c3.x, c3.y, c3.z, c3.w};
+            if (am) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    bool on = col[i] >= 0;
+                    if constexpr (LDSBITS) on = on && block_active(col[i]);
+                    else on = on && mask16(a.xmask, col[i]) != 0u;
+                    f |= (on ? 1u : 0u) << i;
+                }
+            }
+        }
+        const uint32_t cnt = __popc(f), incl = wave_incl_add(cnt);
+        uint32_t pos = n + incl - cnt;
+        while (f) {
+            const int i = ctz32(f);
+            f &= f - 1;
+            out[pos++] = (int32_t)(sid * 16 + i);
+        }
+        n += readlane_u32(incl, WAVE - 1);
+    }
+    if (lane == 0) a.ccount[gw] = n;
+}
+
+__global__ __launch_bounds__(TPB) void k_pull_compact(MainArgs a)
+{
+    const int32_t N = a.counters[C_NZBLK];
+    int64_t spw;
+    if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, spw)) return;
+    const int gw = blockIdx.x * (TPB / WAVE) + (threadIdx.x >> 6);
+    const int32_t nwords = (a.nbc + 31) >> 5;
+    if (nwords <= LDS_BITMAP_WORDS) {
+        for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
+        __syncthreads();
+        if (gw < a.nreg) pull_compact<true>(a, gw, spw);
+    } else {
+        if (gw < a.nreg) pull_compact<false>(a, gw, spw);
     }
 }
 
@@ -1530,7 +1626,7 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
         }
         if (ballot(cnt[0] | cnt[1] | cnt[2] | cnt[3])) {
             wave_lds_sync();
-            flat_pass<MODE, true, true, true>(a, hs, cnt, d, sy, sp, [] {});
+            flat_pass<MODE, true, true, true, false>(a, hs, cnt, d, sy, sp, [] {});
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k) if (cnt[k]) hit[k] |= hs->hitw[k * WAVE + lane];
             wave_lds_sync();
@@ -1592,20 +1688,171 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(Mai
         // columns (measured: a quarter was 1.5% slower at 1% uniform x)
         const bool spec = (int64_t)N * 8 >= (int64_t)a.nbc;
         const int32_t nwords = (a.nbc + 31) >> 5;
+        // below the compaction threshold this kernel takes only the non-COO
+        // blocks; k_pull_compact and k_pull_active take the segments
+        int64_t spw;
+        const bool compact = a.nreg > 0 && compact_pull(a, N, spw);
         if (nwords <= LDS_BITMAP_WORDS) {
             for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
             __syncthreads();
             // the non-COO pass stages its headers over the wave's whole LDS slice
             pull_rows<MODE, true>(a, (uint32_t *)lds_raw);
-            init_acc();
-            wave_lds_sync();
-            pull_loop<MODE, true>(a, gw, nw, sy, sp, &L.hs, spec);
+            if (!compact) {
+                init_acc();
+                wave_lds_sync();
+                pull_loop<MODE, true>(a, gw, nw, sy, sp, &L.hs, spec);
+            }
         } else {
             pull_rows<MODE, false>(a, (uint32_t *)lds_raw);
-            init_acc();
-            wave_lds_sync();
-            pull_loop<MODE, false>(a, gw, nw, sy, sp, &L.hs, spec);
+            if (!compact) {
+                init_acc();
+                wave_lds_sync();
+                pull_loop<MODE, false>(a, gw, nw, sy, sp, &L.hs, spec);
+            }
         }
+    }
+}
+
+// Second half of the compacted pull (launched with one wave per region, a
+// grid that is resident at once: wave gw walks region gw).  A round takes the next 256 entries, entry
+// base + 64 k + lane in slot k of a lane, and numbers the runs of one block
+// row among them (the list is in slot order, so block rows do not
+// decrease); a round ends early at the first entry of run RUN_CAP.  Inline
+// COO blocks are taken by their lane, stored COO blocks entry-parallel
+// (flat_pass), both adding into the run's 16 LDS rows; then every run's rows
+// hit are committed with one fp64 atomic each (grouped: the 16 lanes of a
+// run cover one block row).
+constexpr int RUN_CAP = 32;
+struct ActiveLds {
+    uint32_t acc[RUN_CAP * 16];  // per run: 16 row sums (fp32) or BFS minimum parents
+    uint32_t hm[RUN_CAP];        // rows hit per run
+    int32_t runR[RUN_CAP];       // block row of each run
+    HeavyStage<true> hs;
+};
+
+template <int MODE>
+__global__ __launch_bounds__(TPB) void k_pull_active(MainArgs a)
+{
+    __shared__ ActiveLds lds[TPB / WAVE];
+    const int32_t N = a.counters[C_NZBLK];
+    int64_t spw;
+    if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, spw)) return;
+    const int w = threadIdx.x >> 6, lane = lane_id(), gw = blockIdx.x * (TPB / WAVE) + w;
+    if (gw >= a.nreg) return;
+    ActiveLds &L = lds[w];
+    float *sy = (float *)L.acc;
+    int32_t *sp = (int32_t *)L.acc;
+    constexpr uint32_t ACC0 = MODE == M_BFS ? (uint32_t)INT_MAX : 0u;
+    for (int t = lane; t < RUN_CAP * 16; t += WAVE) L.acc[t] = ACC0;
+    if (lane < RUN_CAP) L.hm[lane] = 0u;
+    wave_lds_sync();
+    const uint32_t cnt = a.ccount[gw];
+    const int32_t *list = a.clist + (int64_t)gw * spw * 16;
+    constexpr int IM = inline_max<MODE>();
+    for (uint32_t base = 0; base < cnt;) {
+        bool v[SLOTS];
+        int32_t slot[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            const uint32_t e = base + (uint32_t)(k * WAVE + lane);
+            v[k] = e < cnt;
+            slot[k] = v[k] ? list[e] : 0;
+        }
+        int32_t J[SLOTS], R[SLOTS];
+        uint64_t d[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            J[k] = v[k] ? a.sl_col[slot[k]] : -1;
+            d[k] = v[k] ? a.sl_desc[slot[k]] : 0ull;
+            R[k] = v[k] ? (int32_t)(a.seg_rs[slot[k] >> 4] & 0x7FFFFFFFu) : -1;
+        }
+        // runs of one block row, in entry order (k major)
+        uint32_t run[SLOTS];
+        uint32_t nr = 0;
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            const uint32_t last = k ? readlane_u32((uint32_t)R[k - 1], WAVE - 1) : 0xFFFFFFFFu;
+            uint32_t prev = wave_shr1((uint32_t)R[k]);
+            if (lane == 0) prev = last;
+            const uint32_t fl = (v[k] && (uint32_t)R[k] != prev) ? 1u : 0u;
+            const uint32_t inc = wave_incl_add(fl);
+            run[k] = nr + inc - 1u;
+            nr += readlane_u32(inc, WAVE - 1);
+            // the first entry of each run records the run's block row
+            if (fl && run[k] < (uint32_t)RUN_CAP) L.runR[run[k]] = R[k];
+        }
+        // the round ends before the first entry of run RUN_CAP
+        uint32_t cut = SLOTS * WAVE;
+#pragma unroll
+        for (int k = SLOTS - 1; k >= 0; --k) {
+            const uint64_t b = ballot(v[k] && run[k] >= (uint32_t)RUN_CAP);
+            if (b) cut = (uint32_t)(k * WAVE + ctz64(b));
+        }
+        uint32_t am[SLOTS];
+        bool act[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            v[k] = v[k] && (uint32_t)(k * WAVE + lane) < cut;
+            am[k] = v[k] ? row_admit(a, R[k]) : 0u;
+            act[k] = v[k] && am[k] != 0u && J[k] >= 0;
+        }
+        const uint32_t nruns = nr < (uint32_t)RUN_CAP ? nr : (uint32_t)RUN_CAP;
+        uint32_t xr[SLOTS][IM];
+        uint32_t cnf[SLOTS];
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) {
+            const bool inl = act[k] && desc_inline(d[k]);
+            const uint32_t nnz = desc_nnz(d[k]);
+#pragma unroll
+            for (int e = 0; e < IM; ++e)
+                xr[k][e] = (inl && (uint32_t)e < nnz)
+                               ? x_gather<MODE>(a, J[k], valued<MODE>() ? (inline_cd(d[k], e, a.vb) & 15u) : 0u)
+                               : 0u;
+            const bool flat = act[k] && flat_coo(d[k]);
+            cnf[k] = flat ? nnz : 0u;
+            if (flat) L.hs.stage(k * WAVE + lane, d[k], J[k], 0u, am[k], (int32_t)run[k]);
+        }
+        auto inline_products = [&]() {
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k) {
+                if (act[k] && desc_inline(d[k])) {
+                    const uint32_t h = inline_block<MODE>(a, d[k], J[k], am[k], xr[k], sy + run[k] * 16,
+                                                          sp + run[k] * 16);
+                    if (h) atomicOr(&L.hm[run[k]], h);
+                }
+            }
+        };
+        if (ballot(cnf[0] | cnf[1] | cnf[2] | cnf[3])) {
+            wave_lds_sync();
+            flat_pass<MODE, true, false, false, true>(a, &L.hs, cnf, d, sy, sp, inline_products);
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k) {
+                const uint32_t h = cnf[k] ? L.hs.hitw[k * WAVE + lane] : 0u;
+                if (h) atomicOr(&L.hm[run[k]], h);
+            }
+        } else {
+            inline_products();
+        }
+        wave_lds_sync();
+        // commit: four runs at a time, lane i of a run's 16 lanes takes row i
+        for (uint32_t rb = 0; rb < nruns; rb += 4) {
+            const uint32_t r = rb + (uint32_t)(lane >> 4), i = (uint32_t)(lane & 15);
+            if (r < nruns) {
+                const uint32_t h = L.hm[r];
+                const int32_t Rr = L.runR[r];
+                if ((h >> i) & 1u) {
+                    const int64_t row = (int64_t)Rr * BS + i;
+                    if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], (double)sy[r * 16 + i]);
+                    if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], sp[r * 16 + i]);
+                }
+                if (i == 0 && h) or_mask16(a.ybits, Rr, h);
+                L.acc[r * 16 + i] = ACC0;
+            }
+        }
+        wave_lds_sync();
+        if (lane < RUN_CAP) L.hm[lane] = 0u;
+        wave_lds_sync();
+        base += cut;
     }
 }
 
@@ -1949,7 +2196,33 @@ static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStre
     int g = grid_for(waves, TPB / WAVE, MAX_MAIN_GRID);
     const int cap = resident_grid<MODE, PATH>(dyn);
     if (g > cap) g = cap;
-    hipLaunchKernelGGL((k_traverse<MODE, PATH>), dim3(g), dim3(TPB), dyn, s, a);
+    // compacted pull: as many regions as the second kernel keeps resident,
+    // and no more than the pull kernel has waves
+    MainArgs b = a;
+    b.nreg = 0;
+    if (PATH == PATH_PULL && a.clist && a.nseg > 0) {
+        static int g2 = 0;
+        if (g2 == 0) {
+            int dev = 0, cus = 0, per_cu = 0;
+            g2 = -1;
+            if (hipGetDevice(&dev) == hipSuccess &&
+                hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+                hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_pull_active<MODE>, TPB, 0) == hipSuccess &&
+                cus > 0 && per_cu > 0)
+                g2 = cus * per_cu;
+        }
+        if (g2 > 0) b.nreg = min(g2, g) * (TPB / WAVE);
+    }
+    hipLaunchKernelGGL((k_traverse<MODE, PATH>), dim3(g), dim3(TPB), dyn, s, b);
+    // the compacted pull's kernels (they return at once above the threshold)
+    if (b.nreg > 0) {
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_pull_compact, dim3(b.nreg / (TPB / WAVE)), dim3(TPB), dyn, s, b);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k_pull_active<MODE>), dim3(b.nreg / (TPB / WAVE)), dim3(TPB), 0, s, b);
+    }
     return hipGetLastError();
 }
 
@@ -2047,7 +2320,17 @@ static void fill_main_args(const DevMatrix &A, const DevCtx &C, int mode, const 
     a.parent = parent;
     a.xstride = 0;
     a.ystride = 0;
+    // slot ids are int32
+    const bool fits = C.clist && (A.nseg + 4 * MAX_MAIN_GRID) * 16 <= C.clist_cap &&
+                      A.nseg * 16 < (int64_t)INT32_MAX;
+    a.clist = fits ? C.clist : nullptr;
+    a.ccount = C.ccount;
+    a.clist_cap = C.clist_cap;
+    a.nreg = 0;
 }
+
+int64_t compact_list_entries(int64_t nseg) { return (nseg + 4 * MAX_MAIN_GRID) * 16; }
+int32_t compact_list_regions() { return 4 * MAX_MAIN_GRID; }
 
 hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
                        const uint32_t *omask, int complement, int32_t *parent, int forced_path,

@@ -97,7 +97,16 @@ struct DevCtx {
     uint64_t *st_fin[2] = {nullptr, nullptr};   // y compaction
     int32_t n_st_fin = 0;
     int scan_parity = 0, fin_parity = 0;
+    // Compacted pull (moderate x activity): per-wave regions of active slot
+    // ids and their counts; written and read within one call.
+    int32_t *clist = nullptr;
+    int64_t clist_cap = 0;
+    uint32_t *ccount = nullptr;
 };
+// Entries and regions of the compacted pull's list for a matrix of nseg
+// pull segments.
+int64_t compact_list_entries(int64_t nseg);
+int32_t compact_list_regions();
 
 enum Mode : int { M_F32 = 0, M_F16 = 1, M_BOOL = 2, M_BFS = 3 };
 
