@@ -560,7 +560,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"rmat{args.scale}_spmspv_density_sweep", "scale": args.scale,
                    "edge_factor": 16, "n": a.n, "nnz": a.nnz, "densities": DENSITIES, "x_kinds": KINDS,
-                   "calls_per_step": len(points), "semiring": "plus_times", "path": "auto", "th3": 0.05,
+                   "calls_per_step": len(points), "semiring": "plus_times", "path": "auto", "th3": 0.01,
                    "nblk": info["nblk"], "db_build_s": round(build_s, 2),
                    "useful_GFLOPs": round(2 * step_useful * args.steps / elapsed / 1e9, 2)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

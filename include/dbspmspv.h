@@ -53,11 +53,11 @@ typedef enum { DBS_PLUS_TIMES = 0, DBS_OR_AND = 1 } dbs_semiring;
 typedef enum { DBS_PATH_AUTO = 0, DBS_PATH_PUSH = 1, DBS_PATH_PULL = 2 } dbs_path;
 
 /* Global selector threshold (Sec. 3.3.1): AUTO takes push iff
- * N_nzblk < th3 * N_blk.  The paper sets th3 = 0.01 on its GPUs; on MI355X
- * the measured push/pull crossover of these kernels lies near s_b = 0.05 for
- * uniform and clustered x on R-MAT graphs (bench.py --ablation), which is
- * the default here.  Pass th3 = DBS_TH3_PAPER for the paper's value.      */
-#define DBS_TH3_DEFAULT 0.05f
+ * N_nzblk < th3 * N_blk.  The paper sets th3 = 0.01 on its GPUs; on MI355X,
+ * over R-MAT graphs with uniform and clustered x (bench.py --ablation), the
+ * same value gives the smallest summed time of these kernels' automatic
+ * choices, so it is the default here too.                                  */
+#define DBS_TH3_DEFAULT 0.01f
 #define DBS_TH3_PAPER 0.01f
 
 /* Low-level block formats (Sec. 3.2.1). */

@@ -126,14 +126,17 @@ def test_empty_x_and_threshold(torch):
     log("empty x")
     st = check_spmspv(ctx, A, om, a, np.zeros(0, np.int32), np.zeros(0, np.float32), label="empty x")
     assert st["y_nnz"] == 0 and st["n_nzblk"] == 0
-    # N_blk = 25, one active block: with the paper's th3 = 0.01 push needs
-    # N_nzblk < 0.25 (never); the default th3 (0.05) gives N_nzblk < 1.25.
+    # N_blk = 25, one active block: with the paper's th3 = 0.01 (also the
+    # default) push needs N_nzblk < 0.25 (never); th3 = 0.05 gives
+    # N_nzblk < 1.25.
     xi = np.array([5, 6], dtype=np.int32)
     xv = np.array([0.5, -2.0], dtype=np.float32)
     log("threshold paper value")
     check_spmspv(ctx, A, om, a, xi, xv, expect_path="pull", label="th 0.01", th3=0.01)
     log("threshold default")
-    st = check_spmspv(ctx, A, om, a, xi, xv, expect_path="push", label="th default")
+    check_spmspv(ctx, A, om, a, xi, xv, expect_path="pull", label="th default")
+    log("threshold 0.05")
+    st = check_spmspv(ctx, A, om, a, xi, xv, expect_path="push", label="th 0.05", th3=0.05)
     assert st["n_nzblk"] == 1 and st["n_blk"] == 25
     # exact boundary: 2 active blocks, th3 = 0.08 -> 2 < 2.0 is false -> pull
     xi2 = np.array([5, 200], dtype=np.int32)
