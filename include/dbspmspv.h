@@ -56,9 +56,18 @@ typedef enum { DBS_PATH_AUTO = 0, DBS_PATH_PUSH = 1, DBS_PATH_PULL = 2 } dbs_pat
  * N_nzblk < th3 * N_blk.  The paper sets th3 = 0.01 on its GPUs; on MI355X,
  * over R-MAT graphs with uniform and clustered x (bench.py --ablation), the
  * same value gives the smallest summed time of these kernels' automatic
- * choices, so it is the default here too.                                  */
+ * choices, so it is the default here too.
+ * With the default (a th3 argument <= 0) the selector also takes push when x
+ * is spread -- fewer than two of its indices per nonzero vector block -- and
+ * N_nzblk < DBS_TH3_SPREAD * N_blk: push then visits blocks that mostly hold
+ * one matching column, which measured faster than pull up to about that
+ * activity, while clustered x (up to 16 indices per vector block) favours
+ * pull from the paper's threshold on.  An explicit th3 > 0 gives the
+ * paper's rule alone, and so does dbs_bfs (a spread frontier's pull is
+ * cheap once the visited rows are masked out).                            */
 #define DBS_TH3_DEFAULT 0.01f
 #define DBS_TH3_PAPER 0.01f
+#define DBS_TH3_SPREAD 0.12f
 
 /* Low-level block formats (Sec. 3.2.1). */
 typedef enum {
@@ -221,7 +230,8 @@ typedef struct {
  *                      = 0 only rows whose bit is set may appear in y, with
  *                      complement_mask = 1 only rows whose bit is clear.
  *   path               AUTO: push iff N_nzblk < th3 N_blk (Sec. 3.3.1); or forced
- *   th3                <= 0 selects DBS_TH3_DEFAULT
+ *   th3                <= 0 selects DBS_TH3_DEFAULT with the spread rule
+ *                      (see DBS_TH3_SPREAD); > 0 the paper's rule with it
  *   d_y_idx            capacity m: the structural pattern of y ascending
  *                      (every row with a stored A[i][j] at a listed j that the
  *                      mask admits, including entries that sum to 0)

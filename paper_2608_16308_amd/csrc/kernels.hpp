@@ -114,13 +114,14 @@ hipError_t launch_scatter(const DevMatrix &A, const DevCtx &C, int mode, int32_t
                           const int32_t *x_idx, const void *x_val, hipStream_t s);
 hipError_t launch_ballot(const DevMatrix &A, const DevCtx &C, int mode, const void *x_dense,
                          hipStream_t s);
-hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th3,
+// th3s > 0: the spread rule as well (see k_scan)
+hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th3, double th3s,
                        hipStream_t s);
 // Dense activation with n a multiple of 16 and a 16-byte aligned x: the
 // blocker runs inside the scan (one launch fewer).
 bool scan_takes_dense(const DevMatrix &A, const void *x_dense);
 hipError_t launch_scan_dense(const DevMatrix &A, DevCtx &C, int mode, const void *x_dense, int forced_path,
-                             double th3, hipStream_t s);
+                             double th3, double th3s, hipStream_t s);
 // Launches the traversal: the push and the pull kernel for an automatic path
 // (each returns at once unless the scan chose it), or only the forced one.
 hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
