@@ -186,3 +186,25 @@ def test_error_flags(torch):
     Ap = gpu_matrix(pat)
     with pytest.raises(dbs.DbsError):
         ctx.spmspv(Ap, to_dev(np.array([1], np.int32)), to_dev(np.ones(1, np.float32)))
+
+
+def test_spread_rule(torch):
+    """The default selector's spread rule: push when x has under two indices
+    per nonzero vector block and N_nzblk < 0.12 N_blk; otherwise, and for an
+    explicit th3, the paper's rule."""
+    a = wl.random_csr(2000, 3200, 0.01, key=(39, 0))  # N_blk = 200
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    rng = wl.rng_for(wl.W_RAND, 40, 0)
+    blocks = np.sort(rng.choice(200, 40, replace=False))
+    spread10 = (blocks[:10] * 16 + 3).astype(np.int32)             # s_b = 0.05, one index per block
+    spread30 = (blocks[:30] * 16 + 7).astype(np.int32)             # s_b = 0.15
+    clustered10 = np.concatenate([np.arange(b * 16, b * 16 + 16) for b in blocks[:10]]).astype(np.int32)
+    pairs10 = np.concatenate([[b * 16 + 1, b * 16 + 9] for b in blocks[:10]]).astype(np.int32)  # two per block
+    cases = [(spread10, 0.0, "push"), (spread10, 0.01, "pull"), (spread30, 0.0, "pull"),
+             (clustered10, 0.0, "pull"), (pairs10, 0.0, "pull")]
+    for xi, th3, want in cases:
+        xv = wl._nonzero_uniform(wl.rng_for(wl.W_RAND, 41, xi.size), -1.0, 1.0, xi.size)
+        label = f"spread rule k={xi.size} th3={th3} -> {want}"
+        log(label)
+        check_spmspv(ctx, A, om, a, xi, xv, expect_path=want, label=label, th3=th3)
