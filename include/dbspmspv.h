@@ -196,8 +196,59 @@ dbs_status dbs_matrix_build_csr(int32_t m, int32_t n, int64_t nnz, const int64_t
                                 const int32_t *col_idx, const void *vals, dbs_dtype vt,
                                 const dbs_build_opts *opts, dbs_matrix **out);
 
+/* GPU-side conversion (the offline step of Sec. 3.1, 3.2.1 and 3.3.2 run on
+ * the device; for weights that are already in device memory, as decoding
+ * loads them, Sec. 4.3).  d_w holds a dense m x n matrix, row-major with a
+ * leading dimension of ld >= n elements, float (DBS_F32) or IEEE binary16
+ * bits (DBS_F16); an entry is stored iff its value is nonzero (-0 is zero,
+ * NaN is stored).  The result equals, array for array and byte for byte,
+ * dbs_matrix_build_csr of the CSR of those entries with the same opts.
+ * Kernels and copies run on `stream` (a hipStream_t, NULL = the default
+ * stream); the call returns after they finish.  Temporary device memory:
+ * 20 bytes per 16x16 tile plus O(m/16 + n/16).  d_w stays the caller's.
+ * Errors: DBS_ERR_ARG for a bad shape, ld, dtype or opts; DBS_ERR_UNSUPPORTED
+ * for n >= 2^26 or the limits of dbs_host_build_csr; DBS_ERR_DEVICE.       */
+dbs_status dbs_matrix_build_dense(int32_t m, int32_t n, const void *d_w, int64_t ld, dbs_dtype vt,
+                                  const dbs_build_opts *opts, void *stream, dbs_matrix **out);
+
 dbs_status dbs_matrix_info_get(const dbs_matrix *A, dbs_matrix_info *out);
 void dbs_matrix_destroy(dbs_matrix *A);
+
+/* Sizes of the device arrays of a matrix (element counts). */
+typedef struct {
+    int64_t nslots;        /* 16 nseg: pull-segment slots */
+    int64_t nseg;          /* segment words */
+    int64_t nblk;          /* block-CSC positions */
+    int32_t nbc;           /* block columns (block-CSC pointer has nbc + 1) */
+    int32_t reserved;
+    int64_t nheavy;        /* non-COO list entries */
+    int64_t nchunk;        /* non-COO chunks (chunk starts have nchunk + 1) */
+    int64_t payload_bytes; /* block payload */
+} dbs_matrix_layout;
+
+/* Host buffers for a copy of the device arrays (any member may be NULL to
+ * skip that array), each at least as long as dbs_matrix_layout says:
+ * slot block columns (-1 padding, sign bit: non-COO block) and descriptors,
+ * segment words (block row | 1 << 31 for a plain-store row), the block-CSC
+ * pointer, rows and descriptors, the non-COO list's block columns,
+ * descriptors, chunk starts and chunk block rows, and the payload.         */
+typedef struct {
+    int32_t *sl_col;
+    uint64_t *sl_desc;
+    uint32_t *seg_rs;
+    int32_t *cb_ptr;
+    int32_t *csc_row;
+    uint64_t *csc_desc;
+    int32_t *hv_col;
+    uint64_t *hv_desc;
+    int32_t *hv_cstart;
+    int32_t *hv_crow;
+    uint8_t *payload;
+} dbs_matrix_arrays;
+
+dbs_status dbs_matrix_layout_get(const dbs_matrix *A, dbs_matrix_layout *out);
+/* Copies the device arrays into the caller's host buffers (synchronous).    */
+dbs_status dbs_matrix_download(const dbs_matrix *A, dbs_matrix_arrays *out);
 
 /* ---------------------------------------------------------------------- */
 /* Per-stream context: scratch masks, lists, dense x and y accumulators.  */

@@ -133,10 +133,50 @@ class Matrix:
     def from_csr(cls, m, n, row_ptr, col_idx, vals=None, opts=None):
         return cls.upload(HostMatrix.from_csr(m, n, row_ptr, col_idx, vals, opts))
 
+    @classmethod
+    def from_dense(cls, w, opts=None, stream=None):
+        """GPU-side conversion of a dense 2-D torch tensor on the device
+        (float32 or float16, unit column stride): entries are stored iff
+        nonzero.  Runs on `stream` (a torch stream; default: the current one)
+        and returns when done."""
+        import torch
+        if w.dim() != 2 or not w.is_cuda or w.stride(1) != 1:
+            raise ValueError("from_dense takes a 2-D device tensor with unit column stride")
+        if w.dtype == torch.float32:
+            code = DBS_F32
+        elif w.dtype == torch.float16:
+            code = DBS_F16
+        else:
+            raise ValueError(f"from_dense takes float32 or float16, not {w.dtype}")
+        st = torch.cuda.current_stream(w.device) if stream is None else stream
+        out = ctypes.c_void_p()
+        m, n = w.shape
+        check(lib().dbs_matrix_build_dense(m, n, ctypes.c_void_p(w.data_ptr()), w.stride(0) if m > 0 else n, code,
+                                           ctypes.byref(opts) if opts is not None else None,
+                                           ctypes.c_void_p(st.cuda_stream), ctypes.byref(out)))
+        return cls(out.value)
+
     def info(self) -> dict:
         info = _lib.MatrixInfo()
         check(lib().dbs_matrix_info_get(self._h, ctypes.byref(info)))
         return _info_dict(info)
+
+    def download(self) -> dict:
+        """Host copies of the device arrays (for inspection and tests)."""
+        lay = _lib.MatrixLayout()
+        check(lib().dbs_matrix_layout_get(self._h, ctypes.byref(lay)))
+        arr = {
+            "sl_col": np.empty(lay.nslots, np.int32), "sl_desc": np.empty(lay.nslots, np.uint64),
+            "seg_rs": np.empty(lay.nseg, np.uint32), "cb_ptr": np.empty(lay.nbc + 1, np.int32),
+            "csc_row": np.empty(lay.nblk, np.int32), "csc_desc": np.empty(lay.nblk, np.uint64),
+            "hv_col": np.empty(lay.nheavy, np.int32), "hv_desc": np.empty(lay.nheavy, np.uint64),
+            "hv_cstart": np.empty(lay.nchunk + 1, np.int32), "hv_crow": np.empty(lay.nchunk, np.int32),
+            "payload": np.empty(lay.payload_bytes, np.uint8),
+        }
+        ptrs = _lib.MatrixArrays(**{k: (v.ctypes.data_as(ctypes.c_void_p) if v.size else None)
+                                    for k, v in arr.items()})
+        check(lib().dbs_matrix_download(self._h, ctypes.byref(ptrs)))
+        return arr
 
     @property
     def shape(self):

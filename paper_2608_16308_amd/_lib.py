@@ -26,7 +26,7 @@ EXPORTED = [
     "dbs_matrix_info_get", "dbs_matrix_destroy", "dbs_ctx_create", "dbs_ctx_set_stream",
     "dbs_ctx_destroy", "dbs_spmspv", "dbs_spmspv_dense", "dbs_spmm_dense", "dbs_bfs", "dbs_ctx_enable_timing",
     "dbs_ctx_read_timing", "dbs_last_error", "dbs_version", "dbs_basic_build", "dbs_basic_destroy",
-    "dbs_basic_spmspv",
+    "dbs_basic_spmspv", "dbs_matrix_build_dense", "dbs_matrix_layout_get", "dbs_matrix_download",
 ]
 
 
@@ -51,6 +51,19 @@ class HostArrays(ctypes.Structure):
                 ("csc2csr", ctypes.POINTER(ctypes.c_int32)), ("desc", ctypes.POINTER(ctypes.c_uint64)),
                 ("payload", ctypes.POINTER(ctypes.c_uint8)), ("payload_bytes", ctypes.c_int64),
                 ("seg", ctypes.POINTER(ctypes.c_uint64)), ("nseg", ctypes.c_int64)]
+
+
+class MatrixLayout(ctypes.Structure):
+    _fields_ = [("nslots", ctypes.c_int64), ("nseg", ctypes.c_int64), ("nblk", ctypes.c_int64),
+                ("nbc", ctypes.c_int32), ("reserved", ctypes.c_int32), ("nheavy", ctypes.c_int64),
+                ("nchunk", ctypes.c_int64), ("payload_bytes", ctypes.c_int64)]
+
+
+class MatrixArrays(ctypes.Structure):
+    _fields_ = [("sl_col", ctypes.c_void_p), ("sl_desc", ctypes.c_void_p), ("seg_rs", ctypes.c_void_p),
+                ("cb_ptr", ctypes.c_void_p), ("csc_row", ctypes.c_void_p), ("csc_desc", ctypes.c_void_p),
+                ("hv_col", ctypes.c_void_p), ("hv_desc", ctypes.c_void_p), ("hv_cstart", ctypes.c_void_p),
+                ("hv_crow", ctypes.c_void_p), ("payload", ctypes.c_void_p)]
 
 
 class CallStats(ctypes.Structure):
@@ -105,6 +118,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dbs_matrix_upload": (ctypes.c_int, [vp, P(vp)]),
         "dbs_matrix_build_csr": (ctypes.c_int, [i32, i32, i64, vp, vp, vp, ctypes.c_int, P(BuildOpts), P(vp)]),
         "dbs_matrix_info_get": (ctypes.c_int, [vp, P(MatrixInfo)]),
+        "dbs_matrix_build_dense": (ctypes.c_int, [i32, i32, vp, i64, ctypes.c_int, P(BuildOpts), vp, P(vp)]),
+        "dbs_matrix_layout_get": (ctypes.c_int, [vp, P(MatrixLayout)]),
+        "dbs_matrix_download": (ctypes.c_int, [vp, P(MatrixArrays)]),
         "dbs_matrix_destroy": (None, [vp]),
         "dbs_ctx_create": (ctypes.c_int, [vp, vp, P(vp)]),
         "dbs_ctx_set_stream": (ctypes.c_int, [vp, vp]),

@@ -25,7 +25,7 @@ HIP_FLAGS = [
 ]
 CXX_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-pthread"]
 
-HIP_SOURCES = ["kernels.hip", "api.hip", "basic.hip"]
+HIP_SOURCES = ["kernels.hip", "api.hip", "basic.hip", "convert.hip"]
 CXX_SOURCES = ["builder.cpp"]
 
 

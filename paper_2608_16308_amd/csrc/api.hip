@@ -10,6 +10,7 @@
 
 #include "internal.hpp"
 #include "kernels.hpp"
+#include "matrix.hpp"
 
 using namespace dbs;
 
@@ -71,11 +72,6 @@ dbs_status dev_zeros(std::vector<void *> &allocs, size_t count, T **out, int byt
 
 }  // namespace
 
-struct dbs_matrix {
-    DevMatrix d;
-    dbs_matrix_info info{};
-    std::vector<void *> allocs;
-};
 
 struct TimedLaunch {
     int cls;
@@ -282,6 +278,43 @@ extern "C" dbs_status dbs_matrix_info_get(const dbs_matrix *A, dbs_matrix_info *
 {
     if (!A || !out) return dbs_fail(DBS_ERR_ARG, "dbs_matrix_info_get: NULL argument");
     *out = A->info;
+    return DBS_OK;
+}
+
+extern "C" dbs_status dbs_matrix_layout_get(const dbs_matrix *A, dbs_matrix_layout *out)
+{
+    if (!A || !out) return dbs_fail(DBS_ERR_ARG, "dbs_matrix_layout_get: NULL argument");
+    std::memset(out, 0, sizeof *out);
+    out->nslots = 16 * A->d.nseg;
+    out->nseg = A->d.nseg;
+    out->nblk = A->d.nblk;
+    out->nbc = A->d.nbc;
+    out->nheavy = A->d.nheavy;
+    out->nchunk = A->d.nchunk;
+    out->payload_bytes = A->info.payload_bytes;
+    return DBS_OK;
+}
+
+extern "C" dbs_status dbs_matrix_download(const dbs_matrix *A, dbs_matrix_arrays *out)
+{
+    if (!A || !out) return dbs_fail(DBS_ERR_ARG, "dbs_matrix_download: NULL argument");
+    const DevMatrix &d = A->d;
+    auto get = [](void *dst, const void *src, size_t bytes) -> hipError_t {
+        if (!dst || !bytes) return hipSuccess;
+        return hipMemcpy(dst, src, bytes, hipMemcpyDeviceToHost);
+    };
+    const size_t ns = (size_t)(16 * d.nseg), nb = (size_t)d.nblk, nh = (size_t)d.nheavy, nc = (size_t)d.nchunk;
+    HIP_TRY(get(out->sl_col, d.sl_col, ns * 4), "hipMemcpy (slots)");
+    HIP_TRY(get(out->sl_desc, d.sl_desc, ns * 8), "hipMemcpy (slots)");
+    HIP_TRY(get(out->seg_rs, d.seg_rs, (size_t)d.nseg * 4), "hipMemcpy (segments)");
+    HIP_TRY(get(out->cb_ptr, d.cb_ptr, ((size_t)d.nbc + 1) * 4), "hipMemcpy (block-CSC)");
+    HIP_TRY(get(out->csc_row, d.csc_row, nb * 4), "hipMemcpy (block-CSC)");
+    HIP_TRY(get(out->csc_desc, d.csc_desc, nb * 8), "hipMemcpy (block-CSC)");
+    HIP_TRY(get(out->hv_col, d.hv_col, nh * 4), "hipMemcpy (non-COO list)");
+    HIP_TRY(get(out->hv_desc, d.hv_desc, nh * 8), "hipMemcpy (non-COO list)");
+    HIP_TRY(get(out->hv_cstart, d.hv_cstart, (nc + 1) * 4), "hipMemcpy (non-COO list)");
+    HIP_TRY(get(out->hv_crow, d.hv_crow, nc * 4), "hipMemcpy (non-COO list)");
+    HIP_TRY(get(out->payload, d.pay, (size_t)A->info.payload_bytes), "hipMemcpy (payload)");
     return DBS_OK;
 }
 
