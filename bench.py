@@ -121,7 +121,8 @@ def other_configs(args, torch, dbs, wl, dev, flush):
     """Mesh-like SpMSpV (126^3 7-point stencil, relabelled, 5% random
     entries; x from BFS balls at 0.1%, 1%, 10%) and the two sparse decode
     layers (fp16, 50% kept, 10% dense activation, dense fp16 y), warm and
-    cold, in the units of the main sweep; the decode layers also beside a
+    cold, in the units of the main sweep (and their model-load time: GPU-side
+    conversion against host build plus upload); the decode layers also beside a
     dense fp16 F.linear of the same weights (the paper's PyTorch baseline)."""
     from paper_2608_16308_amd.bytes_model import BytesModel
     out = {}
@@ -184,6 +185,21 @@ def other_configs(args, torch, dbs, wl, dev, flush):
         lin = lambda: F.linear(xr, wd)
         lin_us = _time_call(torch, lin, reps)
         lin_cold = _cold_us(torch, lin, reps, flush)[0]
+        # model load: the GPU-side conversion of the dense device weights,
+        # beside the host build from CSR plus its upload (best of 3 each)
+        def _load_ms(fn):
+            best = None
+            for _ in range(3):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                M = fn()
+                torch.cuda.synchronize()
+                dt = (time.perf_counter() - t0) * 1e3
+                del M
+                best = dt if best is None else min(best, dt)
+            return round(best, 2)
+        conv_ms = _load_ms(lambda: dbs.Matrix.from_dense(wd))
+        host_ms = _load_ms(lambda: dbs.Matrix.from_csr(w.m, w.n, w.row_ptr, w.col_idx, w.vals))
         # batched decoding (several tokens per pass): warm us per call at nb
         # activations, beside a dense F.linear of the same batch
         batched = {}
@@ -201,7 +217,8 @@ def other_configs(args, torch, dbs, wl, dev, flush):
                        "cold_GBs": round(mod["bytes_total"] / (cold * 1e-6) / 1e9, 1),
                        "cold_traversal_GBs": round(mod["bytes_main"] / (cold_trav * 1e-6) / 1e9, 1),
                        "dense_f16_linear_us": round(lin_us, 2), "dense_f16_linear_cold_us": round(lin_cold, 2),
-                       "speedup_vs_dense_cold": round(lin_cold / cold, 2), "batched": batched})
+                       "speedup_vs_dense_cold": round(lin_cold / cold, 2), "batched": batched,
+                       "load_gpu_convert_ms": conv_ms, "load_host_build_upload_ms": host_ms})
         log(f"[bench] decode {layers[-1]}")
         del ctx, A, wd
         torch.cuda.empty_cache()
