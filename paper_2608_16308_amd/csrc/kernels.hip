@@ -623,6 +623,7 @@ struct MainArgs {
     uint32_t *ccount;       // compacted pull: entries per region
     int64_t clist_cap;      // entries the list holds
     int32_t nreg;           // compacted pull: regions (waves of the second kernel's grid)
+    int32_t cpw;            // non-COO pass: chunks per workgroup round (1..16)
 };
 
 // Independent work units per lane and loop iteration: four segments per
@@ -923,9 +924,9 @@ __device__ __forceinline__ bool block_active(int32_t J) { return (lds_bits[J >> 
 
 // Pull: the non-COO blocks (Dense, ForceCSR, ForceCSC, patched CSR), listed
 // at upload in block-CSR order and cut into chunks of at most HV_CHUNK
-// consecutive blocks of one block row, taken 16 chunks per workgroup and
-// round ahead of the segment loop:
-//  1. thread t (chunk t / 16, block t % 16 of it) loads its block's metadata
+// consecutive blocks of one block row, taken a.cpw (at most 16) chunks per
+// workgroup and round ahead of the segment loop:
+//  1. thread t (chunk t / 16 if below a.cpw, block t % 16 of it) loads its block's metadata
 //     (block column, activity, descriptor), then its record header (row
 //     masks and starts, or column masks and starts for ForceCSC) and its
 //     vector-block mask into LDS; the active blocks of the round are listed
@@ -1025,10 +1026,10 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *L)
     uint8_t *items = (uint8_t *)(L + Y::IT);
     uint8_t *qvals = (uint8_t *)(L + Y::VB) + cs * HV_VAL_BYTES;
     constexpr int VW = MODE == M_F16 ? 8 : 16;
-    for (int64_t c0 = (int64_t)blockIdx.x * Y::NQ; c0 < a.nchunk; c0 += (int64_t)gridDim.x * Y::NQ) {
+    for (int64_t c0 = (int64_t)blockIdx.x * a.cpw; c0 < a.nchunk; c0 += (int64_t)gridDim.x * a.cpw) {
         // 1. metadata, headers and x masks of the round's blocks; the list of the active ones
         const int64_t ch = c0 + cs;
-        const bool valid = ch < a.nchunk;
+        const bool valid = cs < a.cpw && ch < a.nchunk;
         const int32_t h0 = valid ? a.hv_cstart[ch] : 0;
         const int32_t h1 = valid ? a.hv_cstart[ch + 1] : 0;
         const int32_t R = valid ? a.hv_crow[ch] : 0;
@@ -1864,9 +1865,10 @@ __global__ __launch_bounds__(TPB) void k_pull_active(MainArgs a)
 
 // Pull for a matrix without COO blocks (every block is in the non-COO list,
 // as in a decode layer): the non-COO pass alone, in a kernel of its own so
-// that its registers do not compete with the segment loop's; one workgroup
-// per round of 16 chunks (the grid is sized to the chunks, not to
-// residency).
+// that its registers do not compete with the segment loop's; one round per
+// workgroup, of as few chunks as keep the grid within one resident round
+// (fewer chunks per round leave fewer listed blocks per quarter-wave, hence
+// shorter chains of dependent loads).
 template <int MODE, int NB>
 __global__ __launch_bounds__(TPB) void k_rows(MainArgs a)
 {
@@ -2189,6 +2191,27 @@ static int resident_grid(size_t dyn_lds)
     return grid;
 }
 
+// Chunks per round for k_rows: the fewest (at most 16) that keep its grid
+// within one round of resident workgroups.
+template <int MODE, int NB>
+static int32_t rows_cpw(int64_t nchunk, size_t dyn)
+{
+    static int resident[2] = {0, 0};
+    const int slot = dyn ? 1 : 0;
+    if (resident[slot] == 0) {
+        int dev = 0, cus = 0, per_cu = 0;
+        resident[slot] = -1;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_rows<MODE, NB>, TPB, dyn) == hipSuccess &&
+            cus > 0 && per_cu > 0)
+            resident[slot] = cus * per_cu;
+    }
+    if (resident[slot] <= 0) return TPB / 16;
+    const int64_t c = (nchunk + resident[slot] - 1) / resident[slot];
+    return (int32_t)std::max<int64_t>(1, std::min<int64_t>(c, TPB / 16));
+}
+
 template <int MODE, int PATH>
 static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStream_t s)
 {
@@ -2196,7 +2219,9 @@ static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStre
     const int32_t nwords = (A.nbc + 31) >> 5;
     const size_t dyn = (PATH == PATH_PULL && nwords <= LDS_BITMAP_WORDS) ? (size_t)nwords * 4 : 0;
     if (PATH == PATH_PULL && A.nblk > 0 && A.nheavy == A.nblk) {
-        hipLaunchKernelGGL((k_rows<MODE, 1>), dim3(grid_for(A.nchunk, 4 * (TPB / WAVE), INT_MAX)), dim3(TPB), dyn, s, a);
+        MainArgs b = a;
+        b.cpw = rows_cpw<MODE, 1>(A.nchunk, dyn);
+        hipLaunchKernelGGL((k_rows<MODE, 1>), dim3(grid_for(A.nchunk, b.cpw, INT_MAX)), dim3(TPB), dyn, s, b);
         return hipGetLastError();
     }
     int g = grid_for(waves, TPB / WAVE, MAX_MAIN_GRID);
@@ -2333,6 +2358,7 @@ static void fill_main_args(const DevMatrix &A, const DevCtx &C, int mode, const 
     a.ccount = C.ccount;
     a.clist_cap = C.clist_cap;
     a.nreg = 0;
+    a.cpw = TPB / 16;
 }
 
 int64_t compact_list_entries(int64_t nseg) { return (nseg + 4 * MAX_MAIN_GRID) * 16; }
@@ -2404,7 +2430,9 @@ static hipError_t launch_rows_nb(const DevMatrix &A, const MainArgs &a, hipStrea
 {
     const int32_t nwords = (A.nbc + 31) >> 5;
     const size_t dyn = nwords <= LDS_BITMAP_WORDS ? (size_t)nwords * 4 : 0;
-    hipLaunchKernelGGL((k_rows<MODE, NB>), dim3(grid_for(A.nchunk, 4 * (TPB / WAVE), INT_MAX)), dim3(TPB), dyn, s, a);
+    MainArgs b = a;
+    b.cpw = rows_cpw<MODE, NB>(A.nchunk, dyn);
+    hipLaunchKernelGGL((k_rows<MODE, NB>), dim3(grid_for(A.nchunk, b.cpw, INT_MAX)), dim3(TPB), dyn, s, b);
     return hipGetLastError();
 }
 
