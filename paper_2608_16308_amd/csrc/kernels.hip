@@ -624,6 +624,7 @@ struct MainArgs {
     int64_t clist_cap;      // entries the list holds
     int32_t nreg;           // compacted pull: regions (waves of the second kernel's grid)
     int32_t cpw;            // non-COO pass: chunks per workgroup round (1..16)
+    int32_t cpm;            // compacted pull below N_nzblk / N_blk = cpm / 1000
 };
 
 // Independent work units per lane and loop iteration: four segments per
@@ -1424,10 +1425,18 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
 // with the products summed per run of one block row in LDS before the
 // commit; the pull kernel then takes only the non-COO blocks.  Used while
 // N_nzblk / N_blk is below PULL_COMPACT_PERMILLE / 1000 (the slot activity
-// roughly follows it).
+// roughly follows it; PULL_COMPACT_PERMILLE_BOOL for the Boolean modes).
 #ifndef PULL_COMPACT_PERMILLE
 #define PULL_COMPACT_PERMILLE 400
 #endif
+// Boolean modes (BFS levels) do less per active slot, so the segment loop
+// stays ahead of the list down to a lower activity
+#ifndef PULL_COMPACT_PERMILLE_BOOL
+#define PULL_COMPACT_PERMILLE_BOOL 150
+#endif
+// The compaction tests activity in an LDS copy of the bitmap; without one
+// (more vector blocks than this many bits) the segment loop is used.
+constexpr int32_t COMPACT_BITMAP_WORDS = 8192;
 // Region r (wave r of k_pull_compact fills it, wave r of k_pull_active walks
 // it) covers spw consecutive segments and holds up to 16 spw entries.  False when the list is absent
 // or too small.
@@ -1435,8 +1444,8 @@ __device__ __forceinline__ bool compact_pull(const MainArgs &a, int32_t N, int64
 {
     const int nw = a.nreg;
     spw = (a.nseg + nw - 1) / nw;
-    return a.clist != nullptr && a.nseg > 0 && (int64_t)N * 1000 < (int64_t)a.nbc * PULL_COMPACT_PERMILLE &&
-           (int64_t)nw * spw * 16 <= a.clist_cap;
+    return a.clist != nullptr && a.nseg > 0 && (int64_t)N * 1000 < (int64_t)a.nbc * a.cpm &&
+           ((a.nbc + 31) >> 5) <= COMPACT_BITMAP_WORDS && (int64_t)nw * spw * 16 <= a.clist_cap;
 }
 
 // First half: wave gw takes segments [gw spw, (gw + 1) spw), one segment per
@@ -1491,7 +1500,7 @@ __global__ __launch_bounds__(TPB) void k_pull_compact(MainArgs a)
     if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, spw)) return;
     const int gw = blockIdx.x * (TPB / WAVE) + (threadIdx.x >> 6);
     const int32_t nwords = (a.nbc + 31) >> 5;
-    if (nwords <= LDS_BITMAP_WORDS) {
+    if (nwords <= COMPACT_BITMAP_WORDS) {  // (always, by compact_pull)
         for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
         __syncthreads();
         if (gw < a.nreg) pull_compact<true>(a, gw, spw);
@@ -2231,6 +2240,7 @@ static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStre
     // and no more than the pull kernel has waves
     MainArgs b = a;
     b.nreg = 0;
+    b.cpm = valued<MODE>() ? PULL_COMPACT_PERMILLE : PULL_COMPACT_PERMILLE_BOOL;
     if (PATH == PATH_PULL && a.clist && a.nseg > 0) {
         static int g2 = 0;
         if (g2 == 0) {
@@ -2249,7 +2259,9 @@ static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStre
     if (b.nreg > 0) {
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(k_pull_compact, dim3(b.nreg / (TPB / WAVE)), dim3(TPB), dyn, s, b);
+        const int32_t nwords = (A.nbc + 31) >> 5;
+        const size_t dync = nwords <= COMPACT_BITMAP_WORDS ? (size_t)nwords * 4 : 0;
+        hipLaunchKernelGGL(k_pull_compact, dim3(b.nreg / (TPB / WAVE)), dim3(TPB), dync, s, b);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL((k_pull_active<MODE>), dim3(b.nreg / (TPB / WAVE)), dim3(TPB), 0, s, b);
@@ -2359,6 +2371,7 @@ static void fill_main_args(const DevMatrix &A, const DevCtx &C, int mode, const 
     a.clist_cap = C.clist_cap;
     a.nreg = 0;
     a.cpw = TPB / 16;
+    a.cpm = 0;
 }
 
 int64_t compact_list_entries(int64_t nseg) { return (nseg + 4 * MAX_MAIN_GRID) * 16; }
