@@ -1493,8 +1493,12 @@ __device__ void pull_compact(const MainArgs &a, int gw, int64_t spw)
     if (lane == 0) a.ccount[gw] = n;
 }
 
+// The compaction kernel also takes the non-COO blocks (pull_rows), so that
+// their chains overlap the compaction instead of preceding it.
+template <int MODE>
 __global__ __launch_bounds__(TPB) void k_pull_compact(MainArgs a)
 {
+    __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE, 1>::WORDS];
     const int32_t N = a.counters[C_NZBLK];
     int64_t spw;
     if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, spw)) return;
@@ -1503,8 +1507,10 @@ __global__ __launch_bounds__(TPB) void k_pull_compact(MainArgs a)
     if (nwords <= COMPACT_BITMAP_WORDS) {  // (always, by compact_pull)
         for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
         __syncthreads();
+        pull_rows<MODE, true>(a, rows_lds);
         if (gw < a.nreg) pull_compact<true>(a, gw, spw);
     } else {
+        pull_rows<MODE, false>(a, rows_lds);
         if (gw < a.nreg) pull_compact<false>(a, gw, spw);
     }
 }
@@ -1704,27 +1710,23 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(Mai
         // columns (measured: a quarter was 1.5% slower at 1% uniform x)
         const bool spec = (int64_t)N * 8 >= (int64_t)a.nbc;
         const int32_t nwords = (a.nbc + 31) >> 5;
-        // below the compaction threshold this kernel takes only the non-COO
-        // blocks; k_pull_compact and k_pull_active take the segments
+        // below the compaction threshold k_pull_compact takes the non-COO
+        // blocks and compacts the segments, k_pull_active walks them
         int64_t spw;
-        const bool compact = a.nreg > 0 && compact_pull(a, N, spw);
+        if (a.nreg > 0 && compact_pull(a, N, spw)) return;
         if (nwords <= LDS_BITMAP_WORDS) {
             for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
             __syncthreads();
             // the non-COO pass stages its headers over the wave's whole LDS slice
             pull_rows<MODE, true>(a, (uint32_t *)lds_raw);
-            if (!compact) {
-                init_acc();
-                wave_lds_sync();
-                pull_loop<MODE, true>(a, gw, nw, sy, sp, &L.hs, spec);
-            }
+            init_acc();
+            wave_lds_sync();
+            pull_loop<MODE, true>(a, gw, nw, sy, sp, &L.hs, spec);
         } else {
             pull_rows<MODE, false>(a, (uint32_t *)lds_raw);
-            if (!compact) {
-                init_acc();
-                wave_lds_sync();
-                pull_loop<MODE, false>(a, gw, nw, sy, sp, &L.hs, spec);
-            }
+            init_acc();
+            wave_lds_sync();
+            pull_loop<MODE, false>(a, gw, nw, sy, sp, &L.hs, spec);
         }
     }
 }
@@ -2261,7 +2263,7 @@ static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStre
         if (e != hipSuccess) return e;
         const int32_t nwords = (A.nbc + 31) >> 5;
         const size_t dync = nwords <= COMPACT_BITMAP_WORDS ? (size_t)nwords * 4 : 0;
-        hipLaunchKernelGGL(k_pull_compact, dim3(b.nreg / (TPB / WAVE)), dim3(TPB), dync, s, b);
+        hipLaunchKernelGGL((k_pull_compact<MODE>), dim3(b.nreg / (TPB / WAVE)), dim3(TPB), dync, s, b);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL((k_pull_active<MODE>), dim3(b.nreg / (TPB / WAVE)), dim3(TPB), 0, s, b);
