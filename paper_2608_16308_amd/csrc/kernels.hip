@@ -1419,11 +1419,12 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
 
 // Compacted pull.  Below an activity threshold most slots of a segment have
 // nothing to multiply, and the segment loop pays its full chain of dependent
-// loads for a few useful lanes.  Instead, one kernel compacts the slots with
-// work into a list (k_pull_compact), and a second one (k_pull_active) runs
-// the same block work over the list, 256 active slots per wave and round,
-// with the products summed per run of one block row in LDS before the
-// commit; the pull kernel then takes only the non-COO blocks.  Used while
+// loads for a few useful lanes.  Instead, the pull kernel compacts the slots
+// with work into a list (pull_compact; k_pull_compact when the bitmap is too
+// large for the pull kernel's LDS copy) alongside the non-COO blocks, and the
+// push kernel runs the same block work over the list (pull_active), 256
+// active slots per wave and round, with the products summed per run of one
+// block row in LDS before the commit.  Used while
 // N_nzblk / N_blk is below PULL_COMPACT_PERMILLE / 1000 (the slot activity
 // roughly follows it; PULL_COMPACT_PERMILLE_BOOL for the Boolean modes).
 #ifndef PULL_COMPACT_PERMILLE
@@ -1437,9 +1438,9 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
 // The compaction tests activity in an LDS copy of the bitmap; without one
 // (more vector blocks than this many bits) the segment loop is used.
 constexpr int32_t COMPACT_BITMAP_WORDS = 8192;
-// Region r (wave r of k_pull_compact fills it, wave r of k_pull_active walks
-// it) covers spw consecutive segments and holds up to 16 spw entries.  False when the list is absent
-// or too small.
+// Region r (wave r of the compaction fills it, wave r of the walk takes it)
+// covers spw consecutive segments and holds up to 16 spw entries.  False when
+// the list is absent or too small.
 __device__ __forceinline__ bool compact_pull(const MainArgs &a, int32_t N, int64_t &spw)
 {
     const int nw = a.nreg;
@@ -1493,8 +1494,10 @@ __device__ void pull_compact(const MainArgs &a, int gw, int64_t spw)
     if (lane == 0) a.ccount[gw] = n;
 }
 
-// The compaction kernel also takes the non-COO blocks (pull_rows), so that
-// their chains overlap the compaction instead of preceding it.
+// The compaction as a kernel of its own, for activity bitmaps of more than
+// LDS_BITMAP_WORDS words (the pull kernel then returns at once): it also
+// takes the non-COO blocks (pull_rows), so that their chains overlap the
+// compaction instead of preceding it.
 template <int MODE>
 __global__ __launch_bounds__(TPB) void k_pull_compact(MainArgs a)
 {
@@ -1659,81 +1662,9 @@ __device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
     }
 }
 
-// LDS of one wave: per-slot row accumulators and the staged whole-wave blocks.
-template <bool PUSH>
-struct WaveLds {
-    uint32_t acc[SLOTS * WAVE];  // row accumulators: fp32 sums, or BFS minimum parents
-    HeavyStage<PUSH> hs;
-};
-
-// LDS of a traversal kernel: the waves' slices, or (pull, before the
-// segment loop) the non-COO pass's layout over the same bytes
-template <int MODE, int PATH>
-constexpr size_t traverse_lds_bytes()
-{
-    const size_t waves = (TPB / WAVE) * sizeof(WaveLds<PATH == PATH_PUSH>);
-    const size_t rows = PATH == PATH_PULL ? RowsLds<MODE>::WORDS * sizeof(uint32_t) : 0;
-    return waves > rows ? waves : rows;
-}
-
-
-// The traversal kernels (one per path).  Both are launched for an automatic
-// path choice; each reads the choice the scan made on the device and the
-// other one returns at once.
-// Pull is held to 96 registers (five waves per SIMD; a few spill), which
-// measured faster than four waves without spills; push keeps its registers.
-template <int MODE, int PATH>
-__global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(MainArgs a)
-{
-    __shared__ __align__(16) uint8_t lds_raw[traverse_lds_bytes<MODE, PATH>()];
-    WaveLds<PATH == PATH_PUSH> *lds = (WaveLds<PATH == PATH_PUSH> *)lds_raw;
-    // BFS: the host has read the frontier size of this level; restart the count
-    if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
-    const int32_t N = a.counters[C_NZBLK];
-    if (N == 0 || a.counters[C_PATH] != PATH) return;
-    const int w = threadIdx.x >> 6, lane = lane_id();
-    WaveLds<PATH == PATH_PUSH> &L = lds[w];
-    float *sy = (float *)L.acc;
-    int32_t *sp = (int32_t *)L.acc;
-    auto init_acc = [&]() {
-#pragma unroll
-        for (int k = 0; k < SLOTS; ++k) L.acc[k * WAVE + lane] = MODE == M_BFS ? (uint32_t)INT_MAX : 0u;
-    };
-    const int gw = blockIdx.x * (TPB / WAVE) + w, nw = gridDim.x * (TPB / WAVE);
-    if constexpr (PATH == PATH_PUSH) {
-        init_acc();
-        wave_lds_sync();
-        push_loop<MODE>(a, gw, nw, sy, sp, &L.hs);
-    } else {
-        // with an eighth or more of the vector blocks active, enough visited
-        // blocks are used to load their descriptors together with their block
-        // columns (measured: a quarter was 1.5% slower at 1% uniform x)
-        const bool spec = (int64_t)N * 8 >= (int64_t)a.nbc;
-        const int32_t nwords = (a.nbc + 31) >> 5;
-        // below the compaction threshold k_pull_compact takes the non-COO
-        // blocks and compacts the segments, k_pull_active walks them
-        int64_t spw;
-        if (a.nreg > 0 && compact_pull(a, N, spw)) return;
-        if (nwords <= LDS_BITMAP_WORDS) {
-            for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
-            __syncthreads();
-            // the non-COO pass stages its headers over the wave's whole LDS slice
-            pull_rows<MODE, true>(a, (uint32_t *)lds_raw);
-            init_acc();
-            wave_lds_sync();
-            pull_loop<MODE, true>(a, gw, nw, sy, sp, &L.hs, spec);
-        } else {
-            pull_rows<MODE, false>(a, (uint32_t *)lds_raw);
-            init_acc();
-            wave_lds_sync();
-            pull_loop<MODE, false>(a, gw, nw, sy, sp, &L.hs, spec);
-        }
-    }
-}
-
-// Second half of the compacted pull (launched with one wave per region, a
-// grid that is resident at once: wave gw walks region gw).  A round takes the next 256 entries, entry
-// base + 64 k + lane in slot k of a lane, and numbers the runs of one block
+// Second half of the compacted pull (run by the push kernel, whose grid has
+// a wave per region: wave gw walks region gw).  A round takes the next 256
+// entries, entry base + 64 k + lane in slot k of a lane, and numbers the runs of one block
 // row among them (the list is in slot order, so block rows do not
 // decrease); a round ends early at the first entry of run RUN_CAP.  Inline
 // COO blocks are taken by their lane, stored COO blocks entry-parallel
@@ -1749,15 +1680,9 @@ struct ActiveLds {
 };
 
 template <int MODE>
-__global__ __launch_bounds__(TPB) void k_pull_active(MainArgs a)
+__device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t spw)
 {
-    __shared__ ActiveLds lds[TPB / WAVE];
-    const int32_t N = a.counters[C_NZBLK];
-    int64_t spw;
-    if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, spw)) return;
-    const int w = threadIdx.x >> 6, lane = lane_id(), gw = blockIdx.x * (TPB / WAVE) + w;
-    if (gw >= a.nreg) return;
-    ActiveLds &L = lds[w];
+    const int lane = lane_id();
     float *sy = (float *)L.acc;
     int32_t *sp = (int32_t *)L.acc;
     constexpr uint32_t ACC0 = MODE == M_BFS ? (uint32_t)INT_MAX : 0u;
@@ -1871,6 +1796,109 @@ __global__ __launch_bounds__(TPB) void k_pull_active(MainArgs a)
         if (lane < RUN_CAP) L.hm[lane] = 0u;
         wave_lds_sync();
         base += cut;
+    }
+}
+
+// LDS of one wave: per-slot row accumulators and the staged whole-wave blocks.
+template <bool PUSH>
+struct WaveLds {
+    uint32_t acc[SLOTS * WAVE];  // row accumulators: fp32 sums, or BFS minimum parents
+    HeavyStage<PUSH> hs;
+};
+
+// LDS of a traversal kernel: the waves' slices, or (pull, before the
+// segment loop) the non-COO pass's layout over the same bytes
+template <int MODE, int PATH>
+constexpr size_t traverse_lds_bytes()
+{
+    const size_t waves = (TPB / WAVE) * sizeof(WaveLds<PATH == PATH_PUSH>);
+    const size_t other = PATH == PATH_PULL ? RowsLds<MODE>::WORDS * sizeof(uint32_t)
+                                           : (TPB / WAVE) * sizeof(ActiveLds);
+    return waves > other ? waves : other;
+}
+
+
+// The traversal kernels, launched pull kernel first.  Each reads the path
+// the scan chose on the device and returns at once when it has no part in it:
+//   pull kernel: above the compaction threshold the non-COO pass and the
+//                segment loop; below it the non-COO pass and the compaction
+//                of the COO segments (k_pull_compact instead, when the
+//                activity bitmap exceeds this kernel's LDS copy)
+//   push kernel: push, or the compacted pull's walk of the regions -- one
+//                launch for the two, so that an automatic path choice costs
+//                two traversal launches, not four.
+// Pull is held to 96 registers (five waves per SIMD; a few spill), which
+// measured faster than four waves without spills; push keeps its registers.
+// In the Boolean modes the compaction inside the pull kernel pushes its
+// arrays out to scratch memory under that limit, so there k_pull_compact
+// always takes it.
+template <int MODE> constexpr bool pull_takes_compaction() { return valued<MODE>(); }
+
+template <int MODE, int PATH>
+__global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(MainArgs a)
+{
+    __shared__ __align__(16) uint8_t lds_raw[traverse_lds_bytes<MODE, PATH>()];
+    WaveLds<PATH == PATH_PUSH> *lds = (WaveLds<PATH == PATH_PUSH> *)lds_raw;
+    // BFS: the host has read the frontier size of this level; restart the count
+    if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
+    const int32_t N = a.counters[C_NZBLK];
+    const int32_t path = a.counters[C_PATH];
+    if (N == 0) return;
+    const int w = threadIdx.x >> 6, lane = lane_id();
+    if constexpr (PATH == PATH_PUSH) {
+        if (path == PATH_PULL) {
+            int64_t spw;
+            const int gw = blockIdx.x * (TPB / WAVE) + w;
+            if (a.nreg > 0 && compact_pull(a, N, spw) && gw < a.nreg)
+                pull_active<MODE>(a, ((ActiveLds *)lds_raw)[w], gw, spw);
+            return;
+        }
+    }
+    if (path != PATH) return;
+    WaveLds<PATH == PATH_PUSH> &L = lds[w];
+    float *sy = (float *)L.acc;
+    int32_t *sp = (int32_t *)L.acc;
+    auto init_acc = [&]() {
+#pragma unroll
+        for (int k = 0; k < SLOTS; ++k) L.acc[k * WAVE + lane] = MODE == M_BFS ? (uint32_t)INT_MAX : 0u;
+    };
+    const int gw = blockIdx.x * (TPB / WAVE) + w, nw = gridDim.x * (TPB / WAVE);
+    if constexpr (PATH == PATH_PUSH) {
+        init_acc();
+        wave_lds_sync();
+        push_loop<MODE>(a, gw, nw, sy, sp, &L.hs);
+    } else {
+        // with an eighth or more of the vector blocks active, enough visited
+        // blocks are used to load their descriptors together with their block
+        // columns (measured: a quarter was 1.5% slower at 1% uniform x)
+        const bool spec = (int64_t)N * 8 >= (int64_t)a.nbc;
+        const int32_t nwords = (a.nbc + 31) >> 5;
+        // below the compaction threshold: the non-COO blocks and the
+        // compaction of the segments (the push kernel walks the regions)
+        int64_t spw;
+        const bool compact = a.nreg > 0 && compact_pull(a, N, spw);
+        if (!pull_takes_compaction<MODE>() && compact) return;  // k_pull_compact
+        if (nwords <= LDS_BITMAP_WORDS) {
+            for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
+            __syncthreads();
+            // the non-COO pass stages its headers over the wave's whole LDS slice
+            pull_rows<MODE, true>(a, (uint32_t *)lds_raw);
+            if constexpr (pull_takes_compaction<MODE>()) {
+                if (compact) {
+                    if (gw < a.nreg) pull_compact<true>(a, gw, spw);
+                    return;
+                }
+            }
+            init_acc();
+            wave_lds_sync();
+            pull_loop<MODE, true>(a, gw, nw, sy, sp, &L.hs, spec);
+        } else {
+            if (compact) return;  // k_pull_compact
+            pull_rows<MODE, false>(a, (uint32_t *)lds_raw);
+            init_acc();
+            wave_lds_sync();
+            pull_loop<MODE, false>(a, gw, nw, sy, sp, &L.hs, spec);
+        }
     }
 }
 
@@ -2223,61 +2251,47 @@ static int32_t rows_cpw(int64_t nchunk, size_t dyn)
     return (int32_t)std::max<int64_t>(1, std::min<int64_t>(c, TPB / 16));
 }
 
-template <int MODE, int PATH>
-static hipError_t launch_traverse(const DevMatrix &A, const MainArgs &a, hipStream_t s)
-{
-    const int64_t waves = PATH == PATH_PULL ? (A.nseg + 3) / 4 : (A.nblk + WAVE - 1) / WAVE;
-    const int32_t nwords = (A.nbc + 31) >> 5;
-    const size_t dyn = (PATH == PATH_PULL && nwords <= LDS_BITMAP_WORDS) ? (size_t)nwords * 4 : 0;
-    if (PATH == PATH_PULL && A.nblk > 0 && A.nheavy == A.nblk) {
-        MainArgs b = a;
-        b.cpw = rows_cpw<MODE, 1>(A.nchunk, dyn);
-        hipLaunchKernelGGL((k_rows<MODE, 1>), dim3(grid_for(A.nchunk, b.cpw, INT_MAX)), dim3(TPB), dyn, s, b);
-        return hipGetLastError();
-    }
-    int g = grid_for(waves, TPB / WAVE, MAX_MAIN_GRID);
-    const int cap = resident_grid<MODE, PATH>(dyn);
-    if (g > cap) g = cap;
-    // compacted pull: as many regions as the second kernel keeps resident,
-    // and no more than the pull kernel has waves
-    MainArgs b = a;
-    b.nreg = 0;
-    b.cpm = valued<MODE>() ? PULL_COMPACT_PERMILLE : PULL_COMPACT_PERMILLE_BOOL;
-    if (PATH == PATH_PULL && a.clist && a.nseg > 0) {
-        static int g2 = 0;
-        if (g2 == 0) {
-            int dev = 0, cus = 0, per_cu = 0;
-            g2 = -1;
-            if (hipGetDevice(&dev) == hipSuccess &&
-                hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-                hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_pull_active<MODE>, TPB, 0) == hipSuccess &&
-                cus > 0 && per_cu > 0)
-                g2 = cus * per_cu;
-        }
-        if (g2 > 0) b.nreg = min(g2, g) * (TPB / WAVE);
-    }
-    hipLaunchKernelGGL((k_traverse<MODE, PATH>), dim3(g), dim3(TPB), dyn, s, b);
-    // the compacted pull's kernels (they return at once above the threshold)
-    if (b.nreg > 0) {
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        const int32_t nwords = (A.nbc + 31) >> 5;
-        const size_t dync = nwords <= COMPACT_BITMAP_WORDS ? (size_t)nwords * 4 : 0;
-        hipLaunchKernelGGL((k_pull_compact<MODE>), dim3(b.nreg / (TPB / WAVE)), dim3(TPB), dync, s, b);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL((k_pull_active<MODE>), dim3(b.nreg / (TPB / WAVE)), dim3(TPB), 0, s, b);
-    }
-    return hipGetLastError();
-}
-
+// Launch order: the pull kernel (and k_pull_compact when the bitmap does not
+// fit the pull kernel's LDS copy), then the push kernel, which also walks the
+// compacted pull's regions.  `forced` is the path known on the host (BFS, a
+// forced path, or a choice that the number of x entries already settles);
+// 0 launches both, and the device choice makes one of them return at once.
 template <int MODE>
 static hipError_t launch_paths(const DevMatrix &A, const MainArgs &a, int forced, hipStream_t s)
 {
+    const bool pull = forced != PATH_PUSH, push = forced != PATH_PULL;
+    const int32_t nwords = (A.nbc + 31) >> 5;
+    const size_t dyn = nwords <= LDS_BITMAP_WORDS ? (size_t)nwords * 4 : 0;
+    MainArgs b = a;
+    b.nreg = 0;
+    b.cpm = valued<MODE>() ? PULL_COMPACT_PERMILLE : PULL_COMPACT_PERMILLE_BOOL;
     hipError_t e = hipSuccess;
-    if (forced != PATH_PULL) e = launch_traverse<MODE, PATH_PUSH>(A, a, s);
-    if (e == hipSuccess && forced != PATH_PUSH) e = launch_traverse<MODE, PATH_PULL>(A, a, s);
-    return e;
+    if (pull && A.nblk > 0 && A.nheavy == A.nblk) {
+        // no COO blocks: the non-COO pass alone
+        MainArgs r = b;
+        r.cpw = rows_cpw<MODE, 1>(A.nchunk, dyn);
+        hipLaunchKernelGGL((k_rows<MODE, 1>), dim3(grid_for(A.nchunk, r.cpw, INT_MAX)), dim3(TPB), dyn, s, r);
+        e = hipGetLastError();
+    } else if (pull) {
+        int g = grid_for((A.nseg + 3) / 4, TPB / WAVE, MAX_MAIN_GRID);
+        g = min(g, resident_grid<MODE, PATH_PULL>(dyn));
+        // compacted pull: as many regions as the push kernel keeps resident,
+        // and no more than the pull kernel has waves
+        if (a.clist && a.nseg > 0) b.nreg = min(resident_grid<MODE, PATH_PUSH>(0), g) * (TPB / WAVE);
+        hipLaunchKernelGGL((k_traverse<MODE, PATH_PULL>), dim3(g), dim3(TPB), dyn, s, b);
+        e = hipGetLastError();
+        if (e == hipSuccess && b.nreg > 0 && (dyn == 0 || !pull_takes_compaction<MODE>())) {
+            const size_t dync = nwords <= COMPACT_BITMAP_WORDS ? (size_t)nwords * 4 : 0;
+            hipLaunchKernelGGL((k_pull_compact<MODE>), dim3(b.nreg / (TPB / WAVE)), dim3(TPB), dync, s, b);
+            e = hipGetLastError();
+        }
+    }
+    if (e != hipSuccess || !(push || b.nreg > 0)) return e;
+    int g = push ? grid_for((A.nblk + WAVE - 1) / WAVE, TPB / WAVE, MAX_MAIN_GRID) : 1;
+    g = min(g, resident_grid<MODE, PATH_PUSH>(0));
+    g = max(g, b.nreg / (TPB / WAVE));
+    hipLaunchKernelGGL((k_traverse<MODE, PATH_PUSH>), dim3(g), dim3(TPB), 0, s, b);
+    return hipGetLastError();
 }
 
 hipError_t launch_scatter(const DevMatrix &A, const DevCtx &C, int mode, int32_t k,
