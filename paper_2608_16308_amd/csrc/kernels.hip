@@ -255,6 +255,11 @@ __global__ __launch_bounds__(STPB) void k_scan(uint32_t *__restrict__ xmask, con
     uint32_t nib = 0;  // activity of this thread's 4 vector blocks
     uint32_t pop = 0;  // stored x entries in them
     uint32_t amk[SCAN_ITEMS];
+    // the block-column pointers of all the thread's vector blocks, active or
+    // not, go out with the masks (a dependent load would add a round trip)
+    int32_t cbv[SCAN_ITEMS + 1];
+#pragma unroll
+    for (int k = 0; k <= SCAN_ITEMS; ++k) cbv[k] = base + k <= nbc ? cb_ptr[base + k] : 0;
     if constexpr (DX) {
         // 16 entries per vector block: the marker for zeros, the canonical
         // NaN for an entry equal to the marker
@@ -305,12 +310,11 @@ __global__ __launch_bounds__(STPB) void k_scan(uint32_t *__restrict__ xmask, con
     }
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
-        const int32_t J = base + k;
         const uint32_t am = amk[k];
         nib |= (am ? 1u : 0u) << k;
         pop += __popc(am);
-        start[k] = am ? cb_ptr[J] : 0;
-        len[k] = am ? (uint32_t)(cb_ptr[J + 1] - start[k]) : 0u;
+        start[k] = am ? cbv[k] : 0;
+        len[k] = am ? (uint32_t)(cbv[k + 1] - cbv[k]) : 0u;
         if (len[k]) mine += (1ull << 34) + len[k];
     }
     // one activity bit per vector block: 32 / SCAN_ITEMS threads form a word
