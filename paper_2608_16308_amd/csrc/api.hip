@@ -487,8 +487,14 @@ extern "C" dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring
         if ((double)x_nnz < lim) launch_path = DBS_PATH_PUSH;
         else if ((double)((x_nnz + 15) / 16) >= lim_any) launch_path = DBS_PATH_PULL;
     }
-    LAUNCH(ctx, DBS_K_SCATTER, launch_scatter(A->d, ctx->c, mode, x_nnz, d_x_idx, d_x_val, s));
-    LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, launch_path, (double)norm_th3(th3), spread_th3(th3), s));
+    if (small_x_fits(A->d, (int32_t)x_nnz)) {
+        // a short index list: blocker and scan in one workgroup
+        LAUNCH(ctx, DBS_K_SCAN, launch_small_x(A->d, ctx->c, mode, (int32_t)x_nnz, d_x_idx, d_x_val, launch_path,
+                                               (double)norm_th3(th3), spread_th3(th3), s));
+    } else {
+        LAUNCH(ctx, DBS_K_SCATTER, launch_scatter(A->d, ctx->c, mode, x_nnz, d_x_idx, d_x_val, s));
+        LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, launch_path, (double)norm_th3(th3), spread_th3(th3), s));
+    }
     LAUNCH(ctx, DBS_K_MAIN,
            launch_main(A->d, ctx->c, mode, ctx->c.xd, d_mask, complement_mask ? 1 : 0, nullptr, launch_path, s));
     LAUNCH(ctx, DBS_K_FINALIZE,

@@ -387,6 +387,148 @@ __global__ __launch_bounds__(STPB) void k_scan(uint32_t *__restrict__ xmask, con
     }
 }
 
+// Blocker and scan in one workgroup for a short index list (k <= SMALL_X_MAX
+// and an activity bitmap of at most SMALL_X_WORDS words), in place of
+// k_scatter + k_scan, whose grid walks every vector block and whose tiles
+// wait on each other's look-back status.  Each thread takes up to two
+// indices: the value goes into the dense scratch and the index's mask bit is
+// set with a returning atomic, whose old word tells whether the index was
+// already stored (the distinct indices are counted from that).  The vector
+// blocks are deduplicated in an LDS hash table (after runs of equal blocks
+// in consecutive lanes); each first occurrence loads
+// its block-column extent, sets its bit in an LDS copy of the activity
+// bitmap, and becomes a push work item (in hash-arrival order, not ascending
+// J: push needs only increasing first tasks).  The counters, the path choice
+// and the whole bitmap are then written as k_scan writes them.
+constexpr int SX_TPB = 1024;
+constexpr int SX_PER = SMALL_X_MAX / SX_TPB;   // indices per thread
+constexpr int SX_HASH_LOG = 12;
+constexpr int SX_HASH = 1 << SX_HASH_LOG;      // hash slots: twice the indices
+static_assert(SX_PER * SX_TPB == SMALL_X_MAX && SX_HASH == 2 * SMALL_X_MAX, "small-x tile");
+
+__device__ __forceinline__ bool sx_insert(uint32_t *tab, uint32_t key)
+{
+    // multiplicative hashing, linear probing; the table is never more than
+    // half full, so a free slot is always found
+    uint32_t h = (key * 2654435761u) >> (32 - SX_HASH_LOG);
+    for (;;) {
+        const uint32_t old = atomicCAS(&tab[h], 0xFFFFFFFFu, key);
+        if (old == 0xFFFFFFFFu) return true;
+        if (old == key) return false;
+        h = (h + 1u) & (uint32_t)(SX_HASH - 1);
+    }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(SX_TPB) void k_small_x(const int32_t *__restrict__ xi, const void *__restrict__ xv,
+                                                   int32_t k, int32_t n, void *__restrict__ xd,
+                                                   uint32_t *__restrict__ xmask,
+                                                   const int32_t *__restrict__ cb_ptr, int32_t nbc,
+                                                   int4 *__restrict__ items, uint32_t *__restrict__ xbits,
+                                                   int32_t *__restrict__ counters, int32_t forced_path,
+                                                   double th3, double th3s)
+{
+    __shared__ uint32_t s_hash[SX_HASH];
+    __shared__ uint32_t s_bits[SMALL_X_WORDS];
+    __shared__ uint64_t lds4[SX_TPB / WAVE];
+    const int t = threadIdx.x;
+    const int32_t nwords = (nbc + 31) >> 5;
+    int32_t j[SX_PER];
+    uint32_t v[SX_PER];
+#pragma unroll
+    for (int e = 0; e < SX_PER; ++e) {
+        const int32_t i = e * SX_TPB + t;
+        j[e] = i < k ? xi[i] : -1;
+        v[e] = 0;
+        if constexpr (MODE == M_F32) v[e] = i < k ? ((const uint32_t *)xv)[i] : 0u;
+        if constexpr (MODE == M_F16) v[e] = i < k ? ((const uint16_t *)xv)[i] : 0u;
+    }
+    for (int32_t i = t; i < SX_HASH; i += SX_TPB) s_hash[i] = 0xFFFFFFFFu;
+    for (int32_t i = t; i < nwords; i += SX_TPB) s_bits[i] = 0u;
+    __syncthreads();
+    const int lane = lane_id();
+    uint32_t bad = 0, pop = 0, own = 0;
+    int32_t cs[SX_PER], ce[SX_PER];
+#pragma unroll
+    for (int e = 0; e < SX_PER; ++e) {
+        const int32_t i = e * SX_TPB + t;
+        const bool valid = i < k && j[e] >= 0 && j[e] < n;
+        if (i < k && !valid) ++bad;
+        cs[e] = ce[e] = 0;
+        // an input equal to the absent-entry marker becomes the canonical NaN
+        if (valid) {
+            if constexpr (MODE == M_F32) ((uint32_t *)xd)[j[e]] = v[e] == 0xFFFFFFFFu ? 0x7FC00000u : v[e];
+            if constexpr (MODE == M_F16)
+                ((uint16_t *)xd)[j[e]] = v[e] == 0xFFFFu ? (uint16_t)0x7E00u : (uint16_t)v[e];
+        }
+        // runs of lanes with one mask word (sorted or clustered indices) are
+        // merged first: one returning atomic per run, whose old word tells
+        // which of the run's bits were already stored
+        const int32_t w = valid ? j[e] >> 5 : -1;
+        uint32_t bits = valid ? 1u << (j[e] & 31) : 0u;
+#pragma unroll
+        for (int o = 1; o < WAVE; o <<= 1) {
+            const uint32_t vb = (uint32_t)__shfl_up((int)bits, o, WAVE);
+            const int32_t vw = __shfl_up(w, o, WAVE);
+            if (lane >= o && vw == w) bits |= vb;
+        }
+        const int32_t nextw = __shfl_down(w, 1, WAVE);
+        if (w >= 0 && (lane == WAVE - 1 || nextw != w)) pop += __popc(bits & ~atomicOr(&xmask[w], bits));
+        // likewise the vector blocks: the first lane of a run inserts
+        const int32_t J = valid ? j[e] >> 4 : -1;
+        const int32_t prevJ = __shfl_up(J, 1, WAVE);
+        if (valid && (lane == 0 || prevJ != J) && sx_insert(s_hash, (uint32_t)J)) {
+            own |= 1u << e;
+            cs[e] = cb_ptr[J];
+            ce[e] = cb_ptr[J + 1];
+            atomicOr(&s_bits[J >> 5], 1u << (J & 31));
+        }
+    }
+    uint64_t mine = 0;
+#pragma unroll
+    for (int e = 0; e < SX_PER; ++e) {
+        const uint32_t len = (uint32_t)(ce[e] - cs[e]);
+        if (((own >> e) & 1u) && len) mine += (1ull << 34) + len;
+    }
+    uint64_t total, ctot;
+    const uint64_t excl = block_exclusive_scan<SX_TPB>(mine, &total, lds4);
+    // block totals of (distinct indices, bad indices, distinct vector blocks)
+    block_exclusive_scan<SX_TPB>(((uint64_t)pop << 32) | ((uint64_t)bad << 16) | (uint64_t)__popc(own), &ctot,
+                                 lds4);
+    int64_t idx = (int64_t)(excl >> 34);
+    int64_t off = (int64_t)(excl & ((1ull << 34) - 1));
+#pragma unroll
+    for (int e = 0; e < SX_PER; ++e) {
+        const int32_t len = ce[e] - cs[e];
+        if (((own >> e) & 1u) && len) {
+            items[idx] = make_int4((int32_t)off, j[e] >> 4, cs[e] - (int32_t)off, 0);
+            ++idx;
+            off += len;
+        }
+    }
+    // (the scans' barriers have completed the LDS bitmap)
+    for (int32_t i = t; i < nwords; i += SX_TPB) xbits[i] = s_bits[i];
+    if (t == 0) {
+        const int32_t NT = (int32_t)(total >> 34);
+        const int32_t T = (int32_t)(total & ((1ull << 34) - 1));
+        const int32_t N = (int32_t)(ctot & 0xFFFFu);
+        const int32_t nbad = (int32_t)((ctot >> 16) & 0xFFFFu);
+        const int32_t npop = (int32_t)(ctot >> 32);
+        items[NT] = make_int4(T, 0, 0, 0);
+        counters[C_NZBLK] = N;
+        counters[C_NTB] = NT;
+        counters[C_TASKS] = T;
+        if (npop) atomicAdd(&counters[C_XPOP], npop);
+        if (nbad) atomicAdd(&counters[C_XBAD], nbad);
+        int path = forced_path;
+        if (path == 0) {
+            const bool spread = th3s > 0.0 && (int64_t)npop < 2 * (int64_t)N && (double)N < th3s * (double)nbc;
+            path = ((double)N < th3 * (double)nbc || spread) ? PATH_PUSH : PATH_PULL;
+        }
+        counters[C_PATH] = path;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // block microkernels
 // ---------------------------------------------------------------------------
@@ -2335,6 +2477,27 @@ hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th
 bool scan_takes_dense(const DevMatrix &A, const void *x_dense)
 {
     return A.n % 16 == 0 && ((uintptr_t)x_dense & 15u) == 0 && SCAN_ITEMS % 2 == 0;
+}
+
+hipError_t launch_small_x(const DevMatrix &A, const DevCtx &C, int mode, int32_t k, const int32_t *x_idx,
+                          const void *x_val, int forced_path, double th3, double th3s, hipStream_t s)
+{
+    // (the look-back status words of the next k_scan stay zero: none used)
+    if (!small_x_fits(A, k)) return hipErrorInvalidValue;
+#define SX_ARGS x_idx, x_val, k, A.n, C.xd, C.xmask, A.cb_ptr, A.nbc, C.items, C.xbits, C.counters, \
+                forced_path, th3, th3s
+    switch (mode) {
+    case M_F32: hipLaunchKernelGGL(k_small_x<M_F32>, dim3(1), dim3(SX_TPB), 0, s, SX_ARGS); break;
+    case M_F16: hipLaunchKernelGGL(k_small_x<M_F16>, dim3(1), dim3(SX_TPB), 0, s, SX_ARGS); break;
+    default: hipLaunchKernelGGL(k_small_x<M_BOOL>, dim3(1), dim3(SX_TPB), 0, s, SX_ARGS); break;
+    }
+#undef SX_ARGS
+    return hipGetLastError();
+}
+
+bool small_x_fits(const DevMatrix &A, int32_t k)
+{
+    return k >= 0 && k <= SMALL_X_MAX && ((int64_t)A.nbc + 31) / 32 <= SMALL_X_WORDS;
 }
 
 hipError_t launch_scan_dense(const DevMatrix &A, DevCtx &C, int mode, const void *x_dense, int forced_path,

@@ -117,6 +117,14 @@ hipError_t launch_ballot(const DevMatrix &A, const DevCtx &C, int mode, const vo
 // th3s > 0: the spread rule as well (see k_scan)
 hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th3, double th3s,
                        hipStream_t s);
+// Blocker and scan as one single-workgroup kernel, for up to SMALL_X_MAX
+// indices and an activity bitmap of up to SMALL_X_WORDS words (small_x_fits);
+// otherwise launch_scatter + launch_scan.
+constexpr int32_t SMALL_X_MAX = 2048;
+constexpr int32_t SMALL_X_WORDS = 8192;
+bool small_x_fits(const DevMatrix &A, int32_t k);
+hipError_t launch_small_x(const DevMatrix &A, const DevCtx &C, int mode, int32_t k, const int32_t *x_idx,
+                          const void *x_val, int forced_path, double th3, double th3s, hipStream_t s);
 // Dense activation with n a multiple of 16 and a 16-byte aligned x: the
 // blocker runs inside the scan (one launch fewer).
 bool scan_takes_dense(const DevMatrix &A, const void *x_dense);

@@ -3,9 +3,10 @@ masks, every block format) against the CPU oracle, through the C ABI."""
 import numpy as np
 import pytest
 
+import oracle
 import paper_2608_16308_amd as dbs
 import workloads as wl
-from gpu_helpers import check_spmspv, gpu_matrix, log, mask_words, oracle_matrix, to_dev, torch_mod
+from gpu_helpers import REL_TOL, check_spmspv, gpu_matrix, log, mask_words, oracle_matrix, to_dev, torch_mod
 
 pytestmark = pytest.mark.gpu
 
@@ -208,3 +209,41 @@ def test_spread_rule(torch):
         label = f"spread rule k={xi.size} th3={th3} -> {want}"
         log(label)
         check_spmspv(ctx, A, om, a, xi, xv, expect_path=want, label=label, th3=th3)
+
+
+@pytest.mark.parametrize("kind", ["uniform", "clustered"])
+def test_small_x_route_boundary(torch, kind):
+    """Up to 2048 indices take the one-workgroup blocker and scan, more take
+    the grid-wide pair: both sides of the boundary, every path, against the
+    oracle; the same x with one repeated entry (2049 indices, the wide route)
+    gives the same y and statistics, with the duplicate flagged."""
+    a = wl.random_csr(3000, 40000, 0.002, key=(41, 0))
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    rng = wl.rng_for(wl.W_RAND, 42, 0 if kind == "uniform" else 1)
+    if kind == "uniform":
+        idx = np.sort(rng.choice(a.n, 2049, replace=False))
+    else:
+        starts = np.sort(rng.choice(a.n // 64 - 1, 33, replace=False)) * 64
+        idx = np.unique(np.concatenate([np.arange(s, s + 64) for s in starts]))[:2049]
+    idx = idx.astype(np.int32)
+    vals = wl._nonzero_uniform(wl.rng_for(wl.W_RAND, 43, 0), -1.0, 1.0, idx.size)
+    stats = {}
+    for k in (1, 2, 17, 2047, 2048, 2049):
+        for p in PATHS:
+            label = f"{kind} k={k} path={p}"
+            log(label)
+            stats[(k, p)] = check_spmspv(ctx, A, om, a, idx[:k], vals[:k], path=p, label=label)
+    # 2048 distinct entries plus a repeat of the first: the wide route
+    xi = np.concatenate([idx[:2048], idx[:1]])
+    xv = np.concatenate([vals[:2048], vals[:1]])
+    for p in PATHS:
+        log(f"{kind} duplicate k=2049 path={p}")
+        y_idx, y_val, st = ctx.spmspv(A, to_dev(xi), to_dev(xv), path=p, stats=True)
+        torch.cuda.synchronize()
+        ref = stats[(2048, p)]
+        assert st["error_flags"] & 2
+        assert st["n_nzblk"] == ref["n_nzblk"] and st["y_nnz"] == ref["y_nnz"] and st["path"] == ref["path"]
+        ri, rv, rs = om.spmspv(idx[:2048], vals[:2048].astype(np.float64))
+        assert np.array_equal(y_idx.cpu().numpy(), ri)
+        assert oracle.within_tol(y_val.cpu().numpy(), rv, rs, REL_TOL).all()
