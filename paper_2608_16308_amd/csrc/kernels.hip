@@ -1451,15 +1451,17 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
         bool vs[SLOTS], act[SLOTS];
         int32_t b[SLOTS], J[SLOTS];
         uint32_t am[SLOTS], mx[SLOTS];
-        // segment word, block column and (spec) descriptor: independent loads
+        // segment word, block column and (spec) descriptor: independent
+        // loads, non-temporal (each slot is read once per call), so that the
+        // stream does not push x out of the L2
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
             const int64_t sid = u * 4 * spq + q * spq + k;
             vs[k] = k < spq && sid < a.nseg;
-            s[k] = vs[k] ? a.seg_rs[sid] : 0u;
+            s[k] = vs[k] ? __builtin_nontemporal_load(&a.seg_rs[sid]) : 0u;
             b[k] = (int32_t)(sid * 16 + i);
-            J[k] = vs[k] ? a.sl_col[b[k]] : -1;
-            d[k] = (vs[k] && spec) ? a.sl_desc[b[k]] : 0ull;
+            J[k] = vs[k] ? __builtin_nontemporal_load(&a.sl_col[b[k]]) : -1;
+            d[k] = (vs[k] && spec) ? __builtin_nontemporal_load(&a.sl_desc[b[k]]) : 0ull;
         }
         // block activity: the LDS bitmap when it fits, else the vector-block
         // mask (gathered here then, and kept for the whole-wave blocks)
@@ -1478,7 +1480,7 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
         }
         if (!spec) {
 #pragma unroll
-            for (int k = 0; k < SLOTS; ++k) d[k] = act[k] ? a.sl_desc[b[k]] : 0ull;
+            for (int k = 0; k < SLOTS; ++k) d[k] = act[k] ? __builtin_nontemporal_load(&a.sl_desc[b[k]]) : 0ull;
         }
         // nothing to multiply anywhere in the wave: the LDS rows are untouched
         if (!ballot(act[0] || act[1] || act[2] || act[3])) continue;
