@@ -1183,11 +1183,14 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *L)
         const uint32_t am = valid ? row_admit(a, R) : 0u;
         const int32_t h = h0 + (int32_t)r;
         bool act = h < h1 && am != 0;
+        // block column and descriptor together (one round trip)
         const int32_t J = act ? a.hv_col[h] : 0;
+        const uint64_t d = act ? a.hv_desc[h] : 0ull;
         if constexpr (LDSBITS) act = act && block_active(J);
         const uint32_t mx = act ? mask16(a.xmask, J) : 0u;
-        const uint64_t d = act ? a.hv_desc[h] : 0ull;
-        act = act && mx != 0;
+        // with the activity bitmap in LDS an active block's mask is nonzero,
+        // so its header loads go out with the mask's
+        if constexpr (!LDSBITS) act = act && mx != 0;
         if (act) {
             const uint4 *hp = (const uint4 *)(a.pay + desc_off(d));
             const uint4 m0 = hp[0], m1 = hp[1];
