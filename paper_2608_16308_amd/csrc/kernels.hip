@@ -332,18 +332,21 @@ __global__ __launch_bounds__(STPB) void k_scan(uint32_t *__restrict__ xmask, con
     if (lane_id() == 0) s_cnt[threadIdx.x >> 6] = cnt2;
     uint64_t total;
     uint64_t excl = block_exclusive_scan<STPB>(mine, &total, lds4);
+    // the tile's counts (thread 0; a single tile keeps them for itself)
+    uint64_t c = 0;
     if (threadIdx.x < WAVE) {
         uint64_t prefix = 0;
         if (threadIdx.x == 0) {
-            // counted before the tile's status is published: a tile that has
-            // seen every earlier status (directly or through an inclusive
-            // one) also sees their counts
-            uint64_t c = 0;
 #pragma unroll
             for (int i = 0; i < STPB / WAVE; ++i) c += s_cnt[i];
-            if ((uint32_t)c) atomicAdd(&counters[C_NZACC], (int32_t)(uint32_t)c);
-            if (c >> 32) atomicAdd(&counters[C_XPOP], (int32_t)(c >> 32));
-            __threadfence();
+            // counted before the tile's status is published: a tile that
+            // has seen every earlier status (directly or through an
+            // inclusive one) also sees their counts
+            if (gridDim.x > 1) {
+                if ((uint32_t)c) atomicAdd(&counters[C_NZACC], (int32_t)(uint32_t)c);
+                if (c >> 32) atomicAdd(&counters[C_XPOP], (int32_t)(c >> 32));
+                __threadfence();
+            }
         }
         if (tile == 0) {
             if (threadIdx.x == 0) st_store(&status[0], ST_INC | total);
@@ -370,14 +373,23 @@ __global__ __launch_bounds__(STPB) void k_scan(uint32_t *__restrict__ xmask, con
         const uint64_t all = s_prefix + total;
         const int32_t NT = (int32_t)(all >> 34);
         const int32_t T = (int32_t)(all & ((1ull << 34) - 1));
-        __threadfence();
-        const int32_t N = __hip_atomic_load(&counters[C_NZACC], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        counters[C_NZACC] = 0;
+        int32_t N, pop;
+        if (gridDim.x > 1) {
+            __threadfence();
+            N = __hip_atomic_load(&counters[C_NZACC], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            counters[C_NZACC] = 0;
+            pop = __hip_atomic_load(&counters[C_XPOP], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            // one tile: no other counts to wait for (the distinct-index total
+            // still goes to the counter, where the compaction reads it)
+            N = (int32_t)(uint32_t)c;
+            pop = (int32_t)(c >> 32);
+            counters[C_XPOP] = pop;
+        }
         counters[C_NZBLK] = N;
         counters[C_NTB] = NT;
         counters[C_TASKS] = T;
         items[NT] = make_int4(T, 0, 0, 0);
-        const int32_t pop = __hip_atomic_load(&counters[C_XPOP], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         int path = forced_path;
         if (path == 0) {
             const bool spread = th3s > 0.0 && (int64_t)pop < 2 * (int64_t)N && (double)N < th3s * (double)nbc;
