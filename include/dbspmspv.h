@@ -390,7 +390,8 @@ dbs_status dbs_basic_spmspv(dbs_basic_matrix *B, dbs_path path, int32_t x_nnz, c
 /* Kernel classes timed with HIP events on the context's stream. */
 typedef enum {
     DBS_K_SCATTER = 0,   /* vector blocker: scatter x or ballot a dense x     */
-    DBS_K_SCAN = 1,      /* active vector-block list, task offsets, selector  */
+    DBS_K_SCAN = 1,      /* active vector-block list, task offsets, selector
+                            (with the blocker too for up to 2048 x indices)   */
     DBS_K_MAIN = 2,      /* push or pull traversal with block microkernels    */
     DBS_K_FINALIZE = 3,  /* compaction / conversion of y, scratch reset       */
     DBS_K_BFS_UPDATE = 4,/* BFS level, visited and frontier update            */
