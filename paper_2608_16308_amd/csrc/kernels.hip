@@ -1,18 +1,24 @@
 // gfx950 kernels of the dual-view blocked SpMSpV (DB-SpMSpV).
 //
-// One call of y = A x runs four kernels on the context's stream:
+// One call of y = A x runs these kernels on the context's stream:
 //   k_scatter / k_ballot  vector blocker (Sec. 3.2.2, 4.1): dense x values and
 //                         the 16-bit blk_x_mask of every 16-element vector block
 //   k_scan                single-pass look-back scan over vector blocks: the
-//                         ascending list of nonzero vector blocks, N_nzblk, the
-//                         push task offsets, and the global push/pull choice
+//                         list of nonzero vector blocks, N_nzblk, the push
+//                         task offsets, and the global push/pull choice
 //                         s_b = N_nzblk / N_blk < th3 (Sec. 3.3.1)
-//   k_traverse            push (block tasks flattened over the block-CSC lists
-//                         of the active column blocks, fetched grid-stride) or
-//                         pull (weighted row-block segments), with a per-block
-//                         microkernel chosen from the block format and the
-//                         vector-block mask (Sec. 3.3.2, 3.3.3, Alg. 2-5) and
-//                         hierarchical writeback through LDS (Sec. 3.3.3)
+//   (k_small_x            both of the above in one workgroup, for short index
+//                         lists)
+//   k_traverse            pull (weighted row-block segments, or below an
+//                         activity threshold a compaction of the segments'
+//                         active slots), then push (block tasks flattened over
+//                         the block-CSC lists of the active column blocks,
+//                         fetched grid-stride; or the walk of the compacted
+//                         slots), with a per-block microkernel chosen from the
+//                         block format and the vector-block mask (Sec. 3.3.2,
+//                         3.3.3, Alg. 2-5) and hierarchical writeback through
+//                         LDS (Sec. 3.3.3); the kernel the device choice does
+//                         not need returns at once
 //   k_finalize            look-back compaction of the touched rows into an
 //                         ascending sparse y, and reset of the scratch it used
 //

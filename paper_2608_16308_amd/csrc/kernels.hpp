@@ -130,8 +130,10 @@ hipError_t launch_small_x(const DevMatrix &A, const DevCtx &C, int mode, int32_t
 bool scan_takes_dense(const DevMatrix &A, const void *x_dense);
 hipError_t launch_scan_dense(const DevMatrix &A, DevCtx &C, int mode, const void *x_dense, int forced_path,
                              double th3, double th3s, hipStream_t s);
-// Launches the traversal: the push and the pull kernel for an automatic path
-// (each returns at once unless the scan chose it), or only the forced one.
+// Launches the traversal: the pull kernel then the push kernel for an
+// automatic path (the one the scan did not choose returns at once; the push
+// kernel also walks the compacted pull's list), or only what the forced path
+// needs.
 hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
                        const uint32_t *omask, int complement, int32_t *parent, int forced_path,
                        hipStream_t s);
