@@ -247,3 +247,37 @@ def test_small_x_route_boundary(torch, kind):
         ri, rv, rs = om.spmspv(idx[:2048], vals[:2048].astype(np.float64))
         assert np.array_equal(y_idx.cpu().numpy(), ri)
         assert oracle.within_tol(y_val.cpu().numpy(), rv, rs, REL_TOL).all()
+
+
+def test_single_scan_tile_counts(torch):
+    """More than 2048 indices on a matrix of at most 1024 vector blocks: the
+    grid-wide blocker and a scan of one tile, which keeps its counts itself.
+    Distinct indices against the oracle on every path; a repeated index and
+    an out-of-range index are flagged, and leave y as without them."""
+    a = wl.random_csr(1500, 12000, 0.004, key=(44, 0))   # N_blk = 750
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    rng = wl.rng_for(wl.W_RAND, 45, 0)
+    idx = np.sort(rng.choice(a.n, 3000, replace=False)).astype(np.int32)
+    vals = wl._nonzero_uniform(wl.rng_for(wl.W_RAND, 46, 0), -1.0, 1.0, idx.size)
+    ref = {}
+    for p in PATHS:
+        label = f"one scan tile k=3000 path={p}"
+        log(label)
+        ref[p] = check_spmspv(ctx, A, om, a, idx, vals, path=p, label=label)
+        assert ref[p]["n_nzblk"] == np.unique(idx >> 4).size
+    ri, rv, rs = om.spmspv(idx, vals.astype(np.float64))
+    for what, xi, xv, flag in (("repeat", np.concatenate([idx, idx[5:6]]), np.concatenate([vals, vals[5:6]]), 2),
+                               ("out of range", np.concatenate([idx, [a.n]]).astype(np.int32),
+                                np.concatenate([vals, [1.0]]).astype(np.float32), 1)):
+        for p in PATHS:
+            log(f"one scan tile {what} path={p}")
+            y_idx, y_val, st = ctx.spmspv(A, to_dev(xi.astype(np.int32)), to_dev(xv.astype(np.float32)), path=p,
+                                          stats=True)
+            torch.cuda.synchronize()
+            assert st["error_flags"] & flag, (what, p, st)
+            assert st["n_nzblk"] == ref[p]["n_nzblk"] and st["path"] == ref[p]["path"]
+            assert np.array_equal(y_idx.cpu().numpy(), ri)
+            assert oracle.within_tol(y_val.cpu().numpy(), rv, rs, REL_TOL).all()
+    log("one scan tile clean call after the flagged ones")
+    check_spmspv(ctx, A, om, a, idx, vals, label="one scan tile after errors")
