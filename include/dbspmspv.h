@@ -83,7 +83,7 @@ typedef enum {
  * th2 = 2.0 (Sec. 3.2.1, taken from CB-SpMV) and a pull segment closes once
  * its accumulated format weight reaches 16 (Sec. 3.3.2).  force_type = -1
  * classifies each block; 0..4 stores every block in that one format (the
- * format ablation of Sec. 5.3).                                             */
+ * format ablation of Sec. 5.4).                                             */
 typedef struct {
     int32_t th0;        /* nnz < th0            -> COO   */
     int32_t th1;        /* nnz > th1            -> Dense */
@@ -116,7 +116,7 @@ typedef struct dbs_matrix dbs_matrix;            /* DB format resident on the GP
 typedef struct dbs_ctx dbs_ctx;                  /* per-stream workspace              */
 
 /* ---------------------------------------------------------------------- */
-/* Offline conversion (Sec. 3.1, 3.2.1; done once and reused, Sec. 5.4).  */
+/* Offline conversion (Sec. 3.1, 3.2.1; done once and reused, Sec. 5.5).  */
 /* ---------------------------------------------------------------------- */
 
 /* Converts a host CSR matrix into the DB format in host memory.

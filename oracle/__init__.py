@@ -240,6 +240,29 @@ def decode_linear(W: OracleMatrix, a_f16: np.ndarray):
 
 
 def within_tol(y_gpu, y_ref, S, rel: float = 1e-5) -> np.ndarray:
-    """Elementwise |y_gpu - y_ref| <= rel * S (S == 0 demands equality)."""
-    y_gpu = np.asarray(y_gpu, dtype=np.float64)
-    return np.abs(y_gpu - np.asarray(y_ref, dtype=np.float64)) <= rel * np.asarray(S, dtype=np.float64)
+    """Element-wise acceptance of computed values against the oracle's.
+
+    The method reaches the plain sum of products, but accumulates it in a
+    different order and precision than the oracle's fp64 sum, so a value is
+    accepted iff |y_gpu - y_ref| <= rel * S, S = sum_j |a_ij x_j| of its row:
+    the rounding error of any summation order is bounded by that sum.  Hence
+
+    * S == 0 demands an exact match (a row whose every product is zero);
+    * the bound applies only to a finite reference: an infinite one (an
+      infinite input) demands the same infinity;
+    * a NaN result is accepted only where the reference is NaN too (a NaN
+      input value reaches every row it multiplies), and a NaN reference
+      demands a NaN result;
+    * equal values are accepted (infinities of one sign);
+    * the three arrays must have one shape; the result has that shape.
+    """
+    g = np.asarray(y_gpu, dtype=np.float64)
+    r = np.asarray(y_ref, dtype=np.float64)
+    s = np.asarray(S, dtype=np.float64)
+    if g.shape != r.shape or g.shape != s.shape:
+        raise ValueError(f"within_tol: shapes differ {g.shape} {r.shape} {s.shape}")
+    with np.errstate(invalid="ignore"):
+        close = np.isfinite(r) & (np.abs(g - r) <= rel * s)
+        same = g == r
+    both_nan = np.isnan(g) & np.isnan(r)
+    return close | same | both_nan

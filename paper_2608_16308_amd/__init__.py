@@ -122,6 +122,9 @@ class Matrix:
 
     def __init__(self, handle):
         self._h = ctypes.c_void_p(handle)
+        info = _lib.MatrixInfo()
+        check(lib().dbs_matrix_info_get(self._h, ctypes.byref(info)))
+        self.m, self.n, self.dtype = int(info.m), int(info.n), int(info.dtype)
 
     @classmethod
     def upload(cls, hm: HostMatrix):
@@ -180,8 +183,7 @@ class Matrix:
 
     @property
     def shape(self):
-        i = self.info()
-        return i["m"], i["n"]
+        return self.m, self.n
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -192,6 +194,104 @@ class Matrix:
 
 def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+# ---------------------------------------------------------------------------
+# Argument checks.  The C ABI takes raw device pointers and trusts the sizes
+# and element types it is given, so every tensor is checked here before its
+# address is passed on: its device, contiguity, element type and length.  A
+# failed check raises DbsError(DBS_ERR_ARG) and nothing is launched.
+# ---------------------------------------------------------------------------
+def _arg_error(msg):
+    return DbsError(_lib.DBS_ERR_ARG, msg)
+
+
+def _value_dtype(torch, code):
+    return {DBS_F32: torch.float32, DBS_F16: torch.float16}.get(code)
+
+
+def _check_tensor(t, name, dtypes, min_numel, device, ndim=None):
+    """One tensor argument: on `device`, contiguous, of one of `dtypes`, with
+    at least `min_numel` elements (and `ndim` dimensions if given)."""
+    if t is None:
+        raise _arg_error(f"{name} is required")
+    if t.device != device:
+        raise _arg_error(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise _arg_error(f"{name} must be contiguous")
+    if t.dtype not in dtypes:
+        raise _arg_error(f"{name} has dtype {t.dtype}, expected {' or '.join(str(d) for d in dtypes)}")
+    if ndim is not None and t.dim() != ndim:
+        raise _arg_error(f"{name} must have {ndim} dimension(s), not {t.dim()}")
+    if t.numel() < min_numel:
+        raise _arg_error(f"{name} holds {t.numel()} elements, needs at least {min_numel}")
+
+
+def _mask_dtypes(torch):
+    return tuple(d for d in (torch.int32, getattr(torch, "uint32", None)) if d is not None)
+
+
+def validate_spmspv(torch, m, n, dtype, semiring, device, x_idx, x_val, mask, y_idx, y_val, y_nnz):
+    """Checks the tensors of one dbs_spmspv call (see Context.spmspv_raw)."""
+    if semiring == DBS_PLUS_TIMES and dtype == DBS_PATTERN:
+        raise _arg_error("a pattern matrix takes only the OR-AND semiring")
+    k = 0
+    if x_idx is not None:
+        _check_tensor(x_idx, "x_idx", (torch.int32,), 0, device, ndim=1)
+        k = x_idx.numel()
+    if semiring == DBS_PLUS_TIMES:
+        if k:
+            _check_tensor(x_val, "x_val", (_value_dtype(torch, dtype),), k, device, ndim=1)
+            if x_val.numel() != k:
+                raise _arg_error(f"x_val holds {x_val.numel()} values for {k} indices")
+        _check_tensor(y_val, "y_val", (_value_dtype(torch, dtype),), m, device)
+    if mask is not None:
+        _check_tensor(mask, "mask", _mask_dtypes(torch), (m + 31) // 32, device)
+    _check_tensor(y_idx, "y_idx", (torch.int32,), m, device)
+    _check_tensor(y_nnz, "y_nnz", (torch.int32,), 1, device)
+    return k
+
+
+def validate_dense(torch, m, n, dtype, device, x, y, y32):
+    """Checks the tensors of one dbs_spmspv_dense call."""
+    vdt = _value_dtype(torch, dtype)
+    if vdt is None:
+        raise _arg_error("a dense activation needs an fp32 or fp16 matrix")
+    _check_tensor(x, "x", (vdt,), n, device)
+    _check_tensor(y, "y", (vdt,), m, device)
+    if y32 is not None:
+        _check_tensor(y32, "y32", (torch.float32,), m, device)
+
+
+def validate_spmm(torch, m, n, dtype, device, X, Y, Y32):
+    """Checks the tensors of one dbs_spmm_dense call: X is [nb, n] and Y (and
+    Y32) [nb, m], row-major."""
+    vdt = _value_dtype(torch, dtype)
+    if vdt is None:
+        raise _arg_error("a dense activation needs an fp32 or fp16 matrix")
+    _check_tensor(X, "X", (vdt,), 0, device, ndim=2)
+    nb = int(X.shape[0])
+    if not 1 <= nb <= _lib.DBS_MAX_BATCH:
+        raise _arg_error(f"batch of {nb} activations, supported 1..{_lib.DBS_MAX_BATCH}")
+    if int(X.shape[1]) != n:
+        raise _arg_error(f"X has {X.shape[1]} columns, the matrix {n}")
+    for t, name, dt in ((Y, "Y", vdt), (Y32, "Y32", torch.float32)):
+        if t is None and name == "Y32":
+            continue
+        _check_tensor(t, name, (dt,), nb * m, device, ndim=2)
+        if m and (int(t.shape[0]) != nb or int(t.shape[1]) != m):
+            raise _arg_error(f"{name} has shape {tuple(t.shape)}, expected ({nb}, {m})")
+    return nb
+
+
+def validate_bfs(torch, m, n, device, source, level, parent):
+    """Checks the tensors of one dbs_bfs call."""
+    if m != n:
+        raise _arg_error("BFS needs a square matrix")
+    if not 0 <= int(source) < n:
+        raise _arg_error(f"source {source} outside [0, {n})")
+    _check_tensor(level, "level", (torch.int32,), n, device)
+    _check_tensor(parent, "parent", (torch.int32,), n, device)
 
 
 class BasicMatrix:
@@ -212,7 +312,15 @@ class BasicMatrix:
         """Dense fp32 y[m] = A x by "push" or "pull" (torch CUDA tensors)."""
         import torch
         s = (stream or torch.cuda.current_stream()).cuda_stream
-        k = 0 if x_idx is None else int(x_idx.numel())
+        dev = y.device if y is not None else torch.device("cuda", torch.cuda.current_device())
+        if dev.type != "cuda":
+            raise _arg_error("y must be a device tensor")
+        k = 0
+        if x_idx is not None:
+            _check_tensor(x_idx, "x_idx", (torch.int32,), 0, dev, ndim=1)
+            k = int(x_idx.numel())
+            _check_tensor(x_val, "x_val", (torch.float32,), k, dev, ndim=1)
+        _check_tensor(y, "y", (torch.float32,), self.m, dev)
         check(lib().dbs_basic_spmspv(self._h, PATHS[path], k, _ptr(x_idx), _ptr(x_val), _ptr(y),
                                      ctypes.c_void_p(s)))
         return y
@@ -237,6 +345,11 @@ class Context:
         check(lib().dbs_ctx_create(sizing._h, ctypes.c_void_p(stream.cuda_stream), ctypes.byref(out)))
         self._h = out
         self.m, self.n = sizing.shape
+        self.device = torch.device("cuda", torch.cuda.current_device())
+
+    def _check_matrix(self, A):
+        if A.m > self.m or A.n > self.n:
+            raise _arg_error(f"matrix {A.m}x{A.n} exceeds the context's sizing {self.m}x{self.n}")
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -256,9 +369,15 @@ class Context:
     # -- y = A x
     def spmspv_raw(self, A: Matrix, x_idx, x_val, y_idx, y_val, y_nnz, semiring=DBS_PLUS_TIMES,
                    mask=None, complement=False, path="auto", th3=0.0, stats=False):
-        """All arguments are preallocated torch CUDA tensors (or None)."""
+        """All arguments are preallocated torch CUDA tensors on the context's
+        device (or None): x_idx int32 [k], x_val [k] in A's value type (None
+        for OR-AND), mask int32/uint32 of at least ceil(m/32) words, y_idx
+        int32 and y_val (A's value type; None for OR-AND) of at least m
+        entries, y_nnz int32 [1]."""
+        self._check_matrix(A)
+        k = validate_spmspv(self._torch, A.m, A.n, A.dtype, semiring, self.device, x_idx, x_val, mask,
+                            y_idx, y_val, y_nnz)
         st = _lib.CallStats() if stats else None
-        k = 0 if x_idx is None else int(x_idx.numel())
         check(lib().dbs_spmspv(self._h, A._h, semiring, k, _ptr(x_idx), _ptr(x_val), _ptr(mask),
                                1 if complement else 0, PATHS[path], float(th3), _ptr(y_idx),
                                _ptr(y_val), _ptr(y_nnz), ctypes.byref(st) if st is not None else None))
@@ -268,14 +387,13 @@ class Context:
                complement=False, path="auto", th3=0.0, stats=False):
         """Returns (y_idx, y_val or None[, stats]) as CUDA tensors trimmed to nnz(y)."""
         torch = self._torch
-        m, _ = A.shape
-        info_dtype = A.info()["dtype"]
+        m = A.m
         sr = DBS_OR_AND if semiring in ("or_and", DBS_OR_AND) else DBS_PLUS_TIMES
-        dev = x_idx.device
+        dev = self.device
         y_idx = torch.empty(max(m, 1), dtype=torch.int32, device=dev)
         y_val = None
         if sr == DBS_PLUS_TIMES:
-            y_val = torch.empty(max(m, 1), dtype=torch.float16 if info_dtype == DBS_F16 else torch.float32,
+            y_val = torch.empty(max(m, 1), dtype=torch.float16 if A.dtype == DBS_F16 else torch.float32,
                                 device=dev)
         y_nnz = torch.zeros(1, dtype=torch.int32, device=dev)
         st = self.spmspv_raw(A, x_idx, x_val, y_idx, y_val, y_nnz, sr, mask, complement, path, th3, stats)
@@ -286,9 +404,11 @@ class Context:
     def spmspv_dense(self, A: Matrix, x, path="auto", th3=0.0, y=None, y32=None, stats=False):
         """Dense activation (active iff nonzero); returns y (and y32 if given)."""
         torch = self._torch
-        m, _ = A.shape
-        if y is None:
+        self._check_matrix(A)
+        m = A.m
+        if y is None and x is not None:
             y = torch.empty(max(m, 1), dtype=x.dtype, device=x.device)
+        validate_dense(torch, m, A.n, A.dtype, self.device, x, y, y32)
         st = _lib.CallStats() if stats else None
         check(lib().dbs_spmspv_dense(self._h, A._h, _ptr(x), PATHS[path], float(th3), _ptr(y), _ptr(y32),
                                      ctypes.byref(st) if st is not None else None))
@@ -297,10 +417,11 @@ class Context:
     def spmm_dense(self, A: Matrix, X, Y=None, Y32=None, stats=False):
         """Batched dense activations X [nb, n] (active iff nonzero); returns Y [nb, m]."""
         torch = self._torch
+        self._check_matrix(A)
         m, n = A.shape
-        nb = int(X.shape[0])
-        if Y is None:
-            Y = torch.empty((nb, max(m, 1)), dtype=X.dtype, device=X.device)
+        if Y is None and X is not None and X.dim() == 2:
+            Y = torch.empty((int(X.shape[0]), max(m, 1)), dtype=X.dtype, device=X.device)
+        nb = validate_spmm(torch, m, n, A.dtype, self.device, X, Y, Y32)
         st = _lib.CallStats() if stats else None
         check(lib().dbs_spmm_dense(self._h, A._h, nb, _ptr(X), _ptr(Y), _ptr(Y32),
                                    ctypes.byref(st) if st is not None else None))
@@ -308,12 +429,14 @@ class Context:
 
     def bfs(self, A: Matrix, source: int, policy="auto", th3=0.0, level=None, parent=None, stats=False):
         torch = self._torch
+        self._check_matrix(A)
         m, n = A.shape
-        dev = torch.device("cuda", torch.cuda.current_device())
+        dev = self.device
         if level is None:
             level = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
         if parent is None:
             parent = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+        validate_bfs(torch, m, n, dev, source, level, parent)
         st = _lib.BfsStats() if stats else None
         check(lib().dbs_bfs(self._h, A._h, int(source), _ptr(level), _ptr(parent), PATHS[policy],
                             float(th3), ctypes.byref(st) if st is not None else None))

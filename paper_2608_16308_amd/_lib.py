@@ -19,6 +19,7 @@ DBS_BLK_COO, DBS_BLK_DENSE, DBS_BLK_FCSR, DBS_BLK_FCSC, DBS_BLK_CSR = range(5)
 BLOCK_TYPE_NAMES = ["coo", "dense", "fcsr", "fcsc", "csr"]
 DBS_K_NAMES = ["scatter", "scan", "main", "finalize", "bfs_update", "other"]
 DBS_BFS_MAX_LEVEL_STATS = 64
+DBS_MAX_BATCH = 8
 
 EXPORTED = [
     "dbs_build_opts_default", "dbs_host_build_csr", "dbs_host_info", "dbs_host_arrays_get",

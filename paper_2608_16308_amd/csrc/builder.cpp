@@ -1,6 +1,6 @@
 // Offline CSR -> dual-view blocked (DB) conversion on the host (Sec. 3.1,
 // 3.2.1, 3.3.2).  Runs once per matrix; the result is reused across SpMSpV
-// calls, BFS levels and decoding tokens (Sec. 5.4).
+// calls, BFS levels and decoding tokens (Sec. 5.5).
 //
 // Steps, all O(nnz log(entries per block row)):
 //  1. per 16-row block row, gather the entries, sort them by

@@ -54,6 +54,16 @@ def f16_ulp_dist(a16: np.ndarray, b16: np.ndarray) -> np.ndarray:
     return np.abs(key(a16) - key(b16))
 
 
+def check_f16(g16: np.ndarray, ref64: np.ndarray, label: str):
+    """fp16 outputs: NaN exactly where the fp64 reference is NaN, elsewhere
+    within one fp16 ulp of its round-to-nearest-even."""
+    r16 = np.asarray(ref64, dtype=np.float64).astype(np.float16)
+    gn, rn = np.isnan(g16), np.isnan(r16)
+    assert np.array_equal(gn, rn), f"{label}: NaN positions differ ({gn.sum()} vs {rn.sum()})"
+    d = f16_ulp_dist(g16[~gn], r16[~rn])
+    assert d.max(initial=0) <= 1, f"{label}: fp16 y off by {d.max()} ulp"
+
+
 def check_spmspv(ctx, A, om, a: wl.CSR, x_idx, x_val, path="auto", mask=None, complement=False,
                  semiring="plus_times", expect_path=None, label="", th3=0.0):
     """Runs one SpMSpV on the GPU and checks it against the oracle."""
@@ -76,8 +86,7 @@ def check_spmspv(ctx, A, om, a: wl.CSR, x_idx, x_val, path="auto", mask=None, co
     if semiring == "plus_times":
         gv = y_val.cpu().numpy()
         if gv.dtype == np.float16:
-            d = f16_ulp_dist(gv, rv.astype(np.float16))
-            assert d.max(initial=0) <= 1, f"{label}: fp16 y off by {d.max()} ulp"
+            check_f16(gv, rv, label)
         else:
             ok = oracle.within_tol(gv, rv, rs, REL_TOL)
             if not ok.all():
@@ -88,4 +97,20 @@ def check_spmspv(ctx, A, om, a: wl.CSR, x_idx, x_val, path="auto", mask=None, co
     assert st["error_flags"] == 0
     if expect_path is not None:
         assert st["path"] == expect_path, (label, st)
+    return st
+
+
+def check_decode_dense(ctx, A, om, a16, path, label):
+    """One dense-activation call (decode layer) against the oracle: the fp16
+    output within one ulp of the fp64 sum's rounding (NaN where it is NaN),
+    the fp32 sums within the tolerance."""
+    torch = torch_mod()
+    x = to_dev(a16)
+    y32 = torch.empty(om.m, dtype=torch.float32, device="cuda:0")
+    y, st = ctx.spmspv_dense(A, x, path=path, y32=y32, stats=True)
+    torch.cuda.synchronize()
+    y64, S, _ = oracle.decode_linear(om, a16)
+    check_f16(y.cpu().numpy(), y64, label)
+    ok = oracle.within_tol(y32.cpu().numpy(), y64, S, REL_TOL)
+    assert ok.all(), f"{label}: {np.sum(~ok)} fp32 sums out of tolerance"
     return st

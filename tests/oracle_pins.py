@@ -341,5 +341,67 @@ def check_fp16_rounding(lib_path=None):
     assert y64[0] == 1 + 2 ** -11 and float(y16[0]) == 1.0
 
 
+def check_within_tol(fn=None):
+    """The acceptance rule of every value comparison against the oracle.
+
+    Values with exact binary forms put each case exactly on, or one double
+    beyond, the bound rel * S, so that a strict comparison, a dropped abs, a
+    bound of rel + S or rel * |y_ref|, or a NaN accepted against a number each
+    flips at least one verdict.
+    """
+    fn = fn or oracle.within_tol
+    tol1 = 1e-5 * 1.0  # the bound for S = 1 at the default rel, as the rule computes it
+    up = np.nextafter
+    cases = [
+        # (y_gpu, y_ref, S, accept)
+        (tol1, 0.0, 1.0, True),                       # exactly on the bound
+        (-tol1, 0.0, 1.0, True),                      # below the reference by the bound
+        (up(tol1, np.inf), 0.0, 1.0, False),          # one double beyond
+        (-up(tol1, np.inf), 0.0, 1.0, False),
+        (-2.0 * tol1, 0.0, 1.0, False),               # far below (a dropped abs accepts it)
+        (0.0, 0.0, 0.0, True),                        # S = 0: exact equality only
+        (5e-324, 0.0, 0.0, False),                    # smallest subnormal off
+        (1e-6, 0.0, 0.0, False),
+        (0.5 + 5e-4, 0.5, 100.0, True),               # cancellation: S >> |y_ref|
+        (0.5 + 2e-3, 0.5, 100.0, False),
+        (1e30 * (1 + 0.5e-5), 1e30, 1e30, True),      # relative at large scale
+        (1e30 * (1 + 2e-5), 1e30, 1e30, False),
+        (np.nan, 1.0, 1.0, False),                    # NaN result, number expected
+        (1.0, np.nan, np.nan, False),                 # number result, NaN expected
+        (np.nan, np.nan, np.nan, True),               # NaN where the reference is NaN
+        (np.inf, np.inf, np.inf, True),
+        (-np.inf, np.inf, np.inf, False),
+        (1.0, np.inf, np.inf, False),                 # an infinite reference demands it exactly
+        (np.inf, 1.0, 1.0, False),
+        (-0.0, 0.0, 0.0, True),                       # the sign of an exact zero sum is free
+    ]
+    g = np.array([c[0] for c in cases], dtype=np.float64)
+    r = np.array([c[1] for c in cases], dtype=np.float64)
+    s = np.array([c[2] for c in cases], dtype=np.float64)
+    want = np.array([c[3] for c in cases])
+    got = np.asarray(fn(g, r, s))
+    assert got.shape == want.shape, ("within_tol shape", got.shape)
+    bad = np.nonzero(got != want)[0]
+    assert bad.size == 0, ("within_tol verdicts", [cases[i] for i in bad])
+    # element-wise: one verdict per element, in order, for float32 inputs too
+    g32 = np.array([1.0, 1.5, 2.0], dtype=np.float32)
+    r64 = np.array([1.0, 1.0, 2.0 + 1e-9], dtype=np.float64)
+    s64 = np.array([1.0, 1.0, 1.0], dtype=np.float64)
+    assert np.array_equal(np.asarray(fn(g32, r64, s64)), [True, False, True])
+    # another rel scales the bound; with rel and S powers of two the bound
+    # 2^-17 * 8 = 2^-14 is exact at any magnitude of the reference
+    assert np.array_equal(np.asarray(fn(np.array([1.0 + 2.0 ** -14, up(1.0 + 2.0 ** -14, 2.0), 1.0 - 2.0 ** -14]),
+                                        np.ones(3), np.full(3, 8.0), 2.0 ** -17)), [True, False, True])
+    assert np.array_equal(np.asarray(fn(np.array([1e-3, 2e-3]), np.zeros(2), np.ones(2), 1e-3)), [True, False])
+    # arrays of different shapes are an error, not a broadcast
+    for shapes in (((3,), (2,), (2,)), ((3,), (1,), (1,)), ((3,), (3,), ())):
+        try:
+            fn(*(np.zeros(sh) for sh in shapes))
+        except ValueError:
+            pass
+        else:
+            raise AssertionError(f"within_tol accepted arrays of shapes {shapes}")
+
+
 ALL_CHECKS = [check_fp16_rounding, check_dense_matvec, check_bool, check_special_cases, check_masks,
               check_bfs_bruteforce, check_bfs_closed_forms, check_decode]

@@ -7,7 +7,7 @@ import oracle
 import oracle_pins
 import paper_2608_16308_amd as dbs
 import workloads as wl
-from gpu_helpers import REL_TOL, check_spmspv, f16_ulp_dist, gpu_matrix, log, oracle_matrix, to_dev, torch_mod
+from gpu_helpers import REL_TOL, check_decode_dense, check_spmspv, f16_ulp_dist, gpu_matrix, log, oracle_matrix, to_dev, torch_mod
 
 pytestmark = pytest.mark.gpu
 
@@ -20,19 +20,7 @@ def torch():
     return t
 
 
-def check_decode(ctx, A, om, a16, path, label):
-    torch = torch_mod()
-    x = to_dev(a16)
-    y32 = torch.empty(om.m, dtype=torch.float32, device="cuda:0")
-    y, st = ctx.spmspv_dense(A, x, path=path, y32=y32, stats=True)
-    torch.cuda.synchronize()
-    y64, S, y16 = oracle.decode_linear(om, a16)
-    g16 = y.cpu().numpy()
-    d = f16_ulp_dist(g16, y16)
-    assert d.max(initial=0) <= 1, f"{label}: fp16 output off by {d.max()} ulp"
-    ok = oracle.within_tol(y32.cpu().numpy(), y64, S, REL_TOL)
-    assert ok.all(), f"{label}: {np.sum(~ok)} fp32 sums out of tolerance"
-    return st
+check_decode = check_decode_dense
 
 
 @pytest.mark.parametrize("shape", [(200, 320), (33, 1000), (1024, 256)])

@@ -73,3 +73,35 @@ def test_mutant_is_caught(name, tmp_path):
         caught = [["child", f"exit status {r.returncode}"]]
     assert caught, f"mutant {name} survived every pin"
     os.remove(lib)
+
+
+# Plausible slips in the acceptance rule every value comparison uses; each
+# must fail the rule's own pin (check_within_tol).
+TOL_MUTANTS = {
+    "tol_rel_plus_S": ("rel * s", "rel + s"),
+    "tol_no_abs": ("np.abs(g - r)", "(g - r)"),
+    "tol_strict": ("<= rel * s", "< rel * s"),
+    "tol_ref_scaled": ("rel * s", "rel * np.abs(r)"),
+    "tol_nan_either": ("np.isnan(g) & np.isnan(r)", "np.isnan(g) | np.isnan(r)"),
+    "tol_no_nan_rule": ("return close | same | both_nan", "return close | same"),
+    "tol_infinite_ref": ("np.isfinite(r) & ", ""),
+    "tol_reduced": ("return close | same | both_nan", "return bool(np.all(close | same | both_nan))"),
+    "tol_broadcast": ("if g.shape != r.shape or g.shape != s.shape:", "if False:"),
+    "tol_rel_ignored": ("rel * s", "1e-5 * s"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(TOL_MUTANTS))
+def test_tolerance_mutant_is_caught(name):
+    import inspect
+    import textwrap
+
+    import numpy as np
+
+    old, new = TOL_MUTANTS[name]
+    src = textwrap.dedent(inspect.getsource(oracle.within_tol))
+    assert src.count(old) >= 1, f"mutation anchor for {name} not found"
+    ns = {"np": np}
+    exec(compile(src.replace(old, new, 1), f"<within_tol:{name}>", "exec"), ns)
+    with pytest.raises((AssertionError, ValueError, TypeError)):
+        pins.check_within_tol(fn=ns["within_tol"])
