@@ -298,6 +298,36 @@ dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring sr, int32_
                       int complement_mask, dbs_path path, float th3, int32_t *d_y_idx,
                       void *d_y_val, int32_t *d_y_nnz, dbs_call_stats *stats);
 
+/* SpMSpV without device allocation, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops and harnesses
+ * that forbid hipMalloc.  Same operation, arguments, results and errors as
+ * dbs_spmspv, with no context and no statistics: the scratch buffers of the
+ * call (densified x, vector-block masks, push work items, fp64 y
+ * accumulators, look-back status words, counters) live in one static device
+ * array of DBS_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it
+ * runs on until the process ends.  The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); the caller passes x and y as for
+ * dbs_spmspv.
+ *   A        m and n at most DBS_NOALLOC_MAX_DIM, else DBS_ERR_UNSUPPORTED
+ *            before anything is launched
+ *   stream   a hipStream_t (NULL = the default stream); asynchronous
+ * The first call on a device looks up that device's copy of the array,
+ * fills it (all-ones bits in the densified x, zeros elsewhere) and waits for
+ * the fill on `stream`; make that first call outside a graph capture.  Every
+ * call leaves the array as it found it.  All calls on one GPU share that
+ * GPU's array: calls that overlap in time on one GPU (on two streams, or
+ * from two host threads) race and give undefined results; serialize them.
+ * Consecutive calls alternate between two copies of the look-back status
+ * words, chosen on the host, so a captured call cannot be replayed.  The
+ * pull path takes the segment loop at every activity: the compaction list
+ * of moderate activities would need memory proportional to the matrix.     */
+#define DBS_NOALLOC_MAX_DIM (1 << 20)
+#define DBS_NOALLOC_SCRATCH_BYTES (14u << 20)
+dbs_status dbs_spmspv_noalloc(const dbs_matrix *A, dbs_semiring sr, int32_t x_nnz, const int32_t *d_x_idx,
+                              const void *d_x_val, const uint32_t *d_mask, int complement_mask,
+                              dbs_path path, float th3, int32_t *d_y_idx, void *d_y_val, int32_t *d_y_nnz,
+                              void *stream);
+
 /* Sparse decode linear layer (Sec. 4.3): y = A a with a DENSE activation a
  * of length n in A's dtype whose entries are active iff nonzero (+0 and -0
  * are inactive); the vector blocks are built on the GPU by a wave ballot

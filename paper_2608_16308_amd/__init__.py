@@ -23,6 +23,7 @@ from ._lib import (BLOCK_TYPE_NAMES, DBS_F16, DBS_F32, DBS_OR_AND, DBS_PATH_AUTO
                    DBS_PATH_PUSH, DBS_PATTERN, DBS_PLUS_TIMES, DbsError, check)
 
 __all__ = ["HostMatrix", "Matrix", "Context", "BasicMatrix", "DbsError", "default_opts", "storage_model",
+           "spmspv_noalloc",
            "DBS_F32", "DBS_F16", "DBS_PATTERN", "PATHS"]
 
 PATHS = {"auto": DBS_PATH_AUTO, "push": DBS_PATH_PUSH, "pull": DBS_PATH_PULL}
@@ -447,6 +448,34 @@ class Context:
                  "frontier": [int(st.frontier[i]) for i in range(min(L, 64))]}
             return level[:n], parent[:n], s
         return level[:n], parent[:n]
+
+
+def spmspv_noalloc(A: Matrix, x_idx, x_val=None, semiring="plus_times", mask=None, complement=False,
+                   path="auto", th3=0.0, y_idx=None, y_val=None, y_nnz=None, stream=None):
+    """y = A x through dbs_spmspv_noalloc: no context, no device allocation
+    in the library (its scratch is a static device array; calls on one GPU
+    must not overlap).  Outputs may be preallocated (y_idx int32 and y_val of
+    at least m entries, y_nnz int32 [1]); returns (y_idx, y_val or None)
+    trimmed to nnz(y), which reads y_nnz back (a synchronization)."""
+    import torch
+    dev = torch.device("cuda", torch.cuda.current_device())
+    m = A.m
+    sr = DBS_OR_AND if semiring in ("or_and", DBS_OR_AND) else DBS_PLUS_TIMES
+    if y_idx is None:
+        y_idx = torch.empty(max(m, 1), dtype=torch.int32, device=dev)
+    if y_val is None and sr == DBS_PLUS_TIMES:
+        y_val = torch.empty(max(m, 1), dtype=torch.float16 if A.dtype == DBS_F16 else torch.float32, device=dev)
+    if y_nnz is None:
+        y_nnz = torch.zeros(1, dtype=torch.int32, device=dev)
+    if sr == DBS_OR_AND:
+        y_val = None
+    k = validate_spmspv(torch, A.m, A.n, A.dtype, sr, dev, x_idx, x_val, mask, y_idx, y_val, y_nnz)
+    st = (stream or torch.cuda.current_stream()).cuda_stream
+    check(lib().dbs_spmspv_noalloc(A._h, sr, k, _ptr(x_idx), _ptr(x_val), _ptr(mask), 1 if complement else 0,
+                                   PATHS[path], float(th3), _ptr(y_idx), _ptr(y_val), _ptr(y_nnz),
+                                   ctypes.c_void_p(st)))
+    cnt = int(y_nnz.item())
+    return y_idx[:cnt], None if y_val is None else y_val[:cnt]
 
 
 def _stats_dict(st: _lib.CallStats) -> dict:

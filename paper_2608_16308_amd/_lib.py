@@ -28,7 +28,9 @@ EXPORTED = [
     "dbs_ctx_destroy", "dbs_spmspv", "dbs_spmspv_dense", "dbs_spmm_dense", "dbs_bfs", "dbs_ctx_enable_timing",
     "dbs_ctx_read_timing", "dbs_last_error", "dbs_version", "dbs_basic_build", "dbs_basic_destroy",
     "dbs_basic_spmspv", "dbs_matrix_build_dense", "dbs_matrix_layout_get", "dbs_matrix_download",
+    "dbs_spmspv_noalloc",
 ]
+DBS_NOALLOC_MAX_DIM = 1 << 20
 
 
 class BuildOpts(ctypes.Structure):
@@ -128,6 +130,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dbs_ctx_destroy": (None, [vp]),
         "dbs_spmspv": (ctypes.c_int, [vp, vp, ctypes.c_int, i32, vp, vp, vp, ctypes.c_int, ctypes.c_int,
                                       f32, vp, vp, vp, P(CallStats)]),
+        "dbs_spmspv_noalloc": (ctypes.c_int, [vp, ctypes.c_int, i32, vp, vp, vp, ctypes.c_int, ctypes.c_int, f32,
+                                              vp, vp, vp, vp]),
         "dbs_spmspv_dense": (ctypes.c_int, [vp, vp, vp, ctypes.c_int, f32, vp, vp, P(CallStats)]),
         "dbs_spmm_dense": (ctypes.c_int, [vp, vp, i32, vp, vp, vp, P(CallStats)]),
         "dbs_bfs": (ctypes.c_int, [vp, vp, i32, vp, vp, ctypes.c_int, f32, P(BfsStats)]),

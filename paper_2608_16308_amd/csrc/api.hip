@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -449,30 +450,41 @@ static float norm_th3(float th3) { return th3 > 0.f ? th3 : DBS_TH3_DEFAULT; }
 // the spread rule's threshold: with the default th3 only
 static double spread_th3(float th3) { return th3 > 0.f ? 0.0 : (double)DBS_TH3_SPREAD; }
 
-extern "C" dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring sr, int32_t x_nnz,
-                                 const int32_t *d_x_idx, const void *d_x_val, const uint32_t *d_mask,
-                                 int complement_mask, dbs_path path, float th3, int32_t *d_y_idx,
-                                 void *d_y_val, int32_t *d_y_nnz, dbs_call_stats *stats)
+namespace {
+
+// Argument checks of one SpMSpV call shared by the context and no-allocation
+// entry points; sets the kernel mode.
+dbs_status spmspv_check_args(const dbs_matrix *A, dbs_semiring sr, int32_t x_nnz, const int32_t *d_x_idx,
+                             const void *d_x_val, dbs_path path, int32_t *d_y_idx, void *d_y_val,
+                             int32_t *d_y_nnz, int *mode)
 {
-    dbs_status st = check_ctx(ctx, A);
-    if (st != DBS_OK) return st;
     if (sr != DBS_PLUS_TIMES && sr != DBS_OR_AND) return dbs_fail(DBS_ERR_ARG, "unknown semiring");
     if (path < DBS_PATH_AUTO || path > DBS_PATH_PULL) return dbs_fail(DBS_ERR_ARG, "unknown path");
     if (x_nnz < 0 || x_nnz > A->d.n)
         return dbs_fail(DBS_ERR_ARG, "x_nnz %d outside [0, n=%d]", x_nnz, A->d.n);
     if (x_nnz > 0 && !d_x_idx) return dbs_fail(DBS_ERR_ARG, "d_x_idx is NULL");
     if (!d_y_idx || !d_y_nnz) return dbs_fail(DBS_ERR_ARG, "d_y_idx / d_y_nnz is NULL");
-    int mode;
     if (sr == DBS_OR_AND) {
-        mode = M_BOOL;
+        *mode = M_BOOL;
     } else {
         if (A->d.dtype == DBS_PATTERN)
             return dbs_fail(DBS_ERR_ARG, "a pattern matrix supports only the OR-AND semiring");
         if (x_nnz > 0 && !d_x_val) return dbs_fail(DBS_ERR_ARG, "d_x_val is NULL");
         if (!d_y_val) return dbs_fail(DBS_ERR_ARG, "d_y_val is NULL");
-        mode = A->d.dtype == DBS_F16 ? M_F16 : M_F32;
+        *mode = A->d.dtype == DBS_F16 ? M_F16 : M_F32;
     }
-    const hipStream_t s = ctx->stream;
+    return DBS_OK;
+}
+
+// The kernel launches of one SpMSpV call on the scratch buffers c (argument
+// checks done).  run(kernel class, launcher) issues one launch and maps its
+// error.
+template <class Run>
+dbs_status spmspv_launches(const dbs_matrix *A, DevCtx &c, hipStream_t s, int mode, dbs_semiring sr,
+                           int32_t x_nnz, const int32_t *d_x_idx, const void *d_x_val, const uint32_t *d_mask,
+                           int complement_mask, dbs_path path, float th3, int32_t *d_y_idx, void *d_y_val,
+                           int32_t *d_y_nnz, Run &&run)
+{
     // The automatic choice (push iff N_nzblk < th3 N_blk) is made on the
     // device, so both traversal kernels are launched and one returns at once.
     // Often k alone settles it: N_nzblk <= k, and N_nzblk >= ceil(k / 16)
@@ -487,19 +499,54 @@ extern "C" dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring
         if ((double)x_nnz < lim) launch_path = DBS_PATH_PUSH;
         else if ((double)((x_nnz + 15) / 16) >= lim_any) launch_path = DBS_PATH_PULL;
     }
+    dbs_status st;
     if (small_x_fits(A->d, (int32_t)x_nnz)) {
         // a short index list: blocker and scan in one workgroup
-        LAUNCH(ctx, DBS_K_SCAN, launch_small_x(A->d, ctx->c, mode, (int32_t)x_nnz, d_x_idx, d_x_val, launch_path,
-                                               (double)norm_th3(th3), spread_th3(th3), s));
+        st = run(DBS_K_SCAN, [&] {
+            return launch_small_x(A->d, c, mode, (int32_t)x_nnz, d_x_idx, d_x_val, launch_path,
+                                  (double)norm_th3(th3), spread_th3(th3), s);
+        });
+        if (st != DBS_OK) return st;
     } else {
-        LAUNCH(ctx, DBS_K_SCATTER, launch_scatter(A->d, ctx->c, mode, x_nnz, d_x_idx, d_x_val, s));
-        LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, launch_path, (double)norm_th3(th3), spread_th3(th3), s));
+        st = run(DBS_K_SCATTER, [&] { return launch_scatter(A->d, c, mode, x_nnz, d_x_idx, d_x_val, s); });
+        if (st != DBS_OK) return st;
+        st = run(DBS_K_SCAN,
+                 [&] { return launch_scan(A->d, c, launch_path, (double)norm_th3(th3), spread_th3(th3), s); });
+        if (st != DBS_OK) return st;
     }
-    LAUNCH(ctx, DBS_K_MAIN,
-           launch_main(A->d, ctx->c, mode, ctx->c.xd, d_mask, complement_mask ? 1 : 0, nullptr, launch_path, s));
-    LAUNCH(ctx, DBS_K_FINALIZE,
-           launch_finalize(A->d, ctx->c, mode, d_y_idx, sr == DBS_OR_AND ? nullptr : d_y_val, d_y_nnz,
-                           d_x_idx, x_nnz, s));
+    st = run(DBS_K_MAIN, [&] {
+        return launch_main(A->d, c, mode, c.xd, d_mask, complement_mask ? 1 : 0, nullptr, launch_path, s);
+    });
+    if (st != DBS_OK) return st;
+    return run(DBS_K_FINALIZE, [&] {
+        return launch_finalize(A->d, c, mode, d_y_idx, sr == DBS_OR_AND ? nullptr : d_y_val, d_y_nnz, d_x_idx,
+                               x_nnz, s);
+    });
+}
+
+}  // namespace
+
+extern "C" dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring sr, int32_t x_nnz,
+                                 const int32_t *d_x_idx, const void *d_x_val, const uint32_t *d_mask,
+                                 int complement_mask, dbs_path path, float th3, int32_t *d_y_idx,
+                                 void *d_y_val, int32_t *d_y_nnz, dbs_call_stats *stats)
+{
+    dbs_status st = check_ctx(ctx, A);
+    if (st != DBS_OK) return st;
+    int mode = 0;
+    st = spmspv_check_args(A, sr, x_nnz, d_x_idx, d_x_val, path, d_y_idx, d_y_val, d_y_nnz, &mode);
+    if (st != DBS_OK) return st;
+    st = spmspv_launches(A, ctx->c, ctx->stream, mode, sr, x_nnz, d_x_idx, d_x_val, d_mask, complement_mask, path,
+                         th3, d_y_idx, d_y_val, d_y_nnz, [ctx](int cls, auto &&launch) -> dbs_status {
+                             Timer t_(ctx, cls);
+                             const hipError_t e = launch();
+                             if (e != hipSuccess) {
+                                 ctx->broken = true;
+                                 return hip_fail(e, "kernel launch");
+                             }
+                             return DBS_OK;
+                         });
+    if (st != DBS_OK) return st;
     if (stats) {
         if ((st = sync_counters(ctx)) != DBS_OK) return st;
         const int32_t *h = ctx->h_counters;
@@ -644,4 +691,138 @@ extern "C" dbs_status dbs_bfs(dbs_ctx *ctx, const dbs_matrix *A, int32_t source,
         stats->reached = reached;
     }
     return DBS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// SpMSpV without device allocation
+// ---------------------------------------------------------------------------
+// The scratch of dbs_spmspv_noalloc: the buffers of one call for a matrix of
+// up to DBS_NOALLOC_MAX_DIM rows and columns, at fixed 256-byte aligned
+// offsets (the layout below).  Each GPU holds its own copy.  In host code
+// this name is a host-side stand-in, never a device address: the device
+// address of a GPU's copy comes from hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[DBS_NOALLOC_SCRATCH_BYTES];
+
+// Fills `words` 32-bit words at p with v (set-up of the scratch).
+static __global__ __launch_bounds__(256) void k_noalloc_fill(uint32_t *p, uint32_t v, int64_t words)
+{
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < words; i += (int64_t)gridDim.x * 256) p[i] = v;
+}
+
+namespace {
+
+constexpr int32_t NA_NB = (DBS_NOALLOC_MAX_DIM + 15) / 16;  // block rows / block columns at most
+constexpr size_t na_round(size_t b) { return (b + 255) / 256 * 256; }
+constexpr int32_t NA_NXWORDS = (NA_NB + 1) / 2 + 2;         // mask words (two 16-bit masks each)
+constexpr int32_t NA_ST_SCAN = 512, NA_ST_FIN = 1024;       // look-back status words per copy
+// byte offsets of the buffers (the roles of a context's scratch)
+constexpr size_t NA_XD = 0;                                                     // densified x, 16 NB values
+constexpr size_t NA_XMASK = NA_XD + na_round((size_t)16 * NA_NB * 4);           // blk_x_mask words
+constexpr size_t NA_XBITS = NA_XMASK + na_round((size_t)NA_NXWORDS * 4);        // activity bits
+constexpr size_t NA_ITEMS = NA_XBITS + na_round(((size_t)NA_NB + 31) / 32 * 4 + 256);  // push work items
+constexpr size_t NA_YACC = NA_ITEMS + na_round(((size_t)NA_NB + 2) * 16);       // fp64 y accumulators
+constexpr size_t NA_YBITS = NA_YACC + na_round((size_t)16 * NA_NB * 8);         // y structure words
+constexpr size_t NA_COUNTERS = NA_YBITS + na_round((size_t)NA_NXWORDS * 4);     // counters
+constexpr size_t NA_ST = NA_COUNTERS + na_round((size_t)C_COUNT * 4);           // statuses: scan x2, fin x2
+constexpr size_t NA_ST_SCAN_BYTES = na_round((size_t)NA_ST_SCAN * 8), NA_ST_FIN_BYTES = na_round((size_t)NA_ST_FIN * 8);
+constexpr size_t NA_END = NA_ST + 2 * NA_ST_SCAN_BYTES + 2 * NA_ST_FIN_BYTES;
+static_assert(NA_END <= DBS_NOALLOC_SCRATCH_BYTES, "the static scratch holds the buffers of a maximal call");
+
+constexpr int NA_MAX_DEVICES = 64;
+struct NoAllocDevice {
+    uint8_t *ptr = nullptr;  // device address of this GPU's copy of `scratch`
+    int scan_parity = 0, fin_parity = 0;
+};
+NoAllocDevice g_na[NA_MAX_DEVICES];
+std::mutex g_na_mu;  // guards g_na (held for the whole host side of a call)
+
+// The current device's scratch, set up on its first use: its address, then
+// its initial contents (all-ones bits in the densified x mark absent
+// entries, zeros elsewhere), waited for on the stream.
+dbs_status noalloc_device(hipStream_t s, NoAllocDevice **out)
+{
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+    if (dev < 0 || dev >= NA_MAX_DEVICES)
+        return dbs_fail(DBS_ERR_UNSUPPORTED, "device %d: the no-allocation path serves devices 0..%d", dev,
+                        NA_MAX_DEVICES - 1);
+    NoAllocDevice &d = g_na[dev];
+    if (!d.ptr) {
+        dbs_status st = check_device();
+        if (st != DBS_OK) return st;
+        if (scan_tiles(NA_NB) + 1 > NA_ST_SCAN || finalize_tiles(NA_NB) + 1 > NA_ST_FIN)
+            return dbs_fail(DBS_ERR_UNSUPPORTED, "static scratch: status regions too small");
+        void *p = nullptr;
+        HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress (static scratch)");
+        hipLaunchKernelGGL(k_noalloc_fill, dim3(1024), dim3(256), 0, s, (uint32_t *)p, 0xFFFFFFFFu,
+                           (int64_t)(NA_XMASK / 4));
+        HIP_TRY(hipGetLastError(), "kernel launch (scratch set-up)");
+        hipLaunchKernelGGL(k_noalloc_fill, dim3(1024), dim3(256), 0, s, (uint32_t *)((uint8_t *)p + NA_XMASK), 0u,
+                           (int64_t)((NA_END - NA_XMASK) / 4));
+        HIP_TRY(hipGetLastError(), "kernel launch (scratch set-up)");
+        HIP_TRY(hipStreamSynchronize(s), "hipStreamSynchronize (scratch set-up)");
+        d.ptr = (uint8_t *)p;
+    }
+    *out = &d;
+    return DBS_OK;
+}
+
+// Context buffers over a device's scratch.
+DevCtx noalloc_ctx(const NoAllocDevice &d)
+{
+    DevCtx c;
+    c.xd = d.ptr + NA_XD;
+    c.xmask = (uint32_t *)(d.ptr + NA_XMASK);
+    c.nxwords = NA_NXWORDS;
+    c.xbits = (uint32_t *)(d.ptr + NA_XBITS);
+    c.items = (int4 *)(d.ptr + NA_ITEMS);
+    c.yacc = (double *)(d.ptr + NA_YACC);
+    c.ybits = (uint32_t *)(d.ptr + NA_YBITS);
+    c.nywords = NA_NXWORDS;
+    c.visited = nullptr;  // (BFS only)
+    c.nextm = nullptr;
+    c.counters = (int32_t *)(d.ptr + NA_COUNTERS);
+    c.st_scan[0] = (uint64_t *)(d.ptr + NA_ST);
+    c.st_scan[1] = (uint64_t *)(d.ptr + NA_ST + NA_ST_SCAN_BYTES);
+    c.n_st_scan = scan_tiles(NA_NB) + 1;
+    c.st_fin[0] = (uint64_t *)(d.ptr + NA_ST + 2 * NA_ST_SCAN_BYTES);
+    c.st_fin[1] = (uint64_t *)(d.ptr + NA_ST + 2 * NA_ST_SCAN_BYTES + NA_ST_FIN_BYTES);
+    c.n_st_fin = finalize_tiles(NA_NB) + 1;
+    c.scan_parity = d.scan_parity;
+    c.fin_parity = d.fin_parity;
+    // no compaction list: pull takes the segment loop at every activity
+    c.clist = nullptr;
+    c.clist_cap = 0;
+    c.ccount = nullptr;
+    return c;
+}
+
+}  // namespace
+
+extern "C" dbs_status dbs_spmspv_noalloc(const dbs_matrix *A, dbs_semiring sr, int32_t x_nnz,
+                                         const int32_t *d_x_idx, const void *d_x_val, const uint32_t *d_mask,
+                                         int complement_mask, dbs_path path, float th3, int32_t *d_y_idx,
+                                         void *d_y_val, int32_t *d_y_nnz, void *stream)
+{
+    if (!A) return dbs_fail(DBS_ERR_ARG, "dbs_spmspv_noalloc: NULL matrix");
+    if (A->d.m > DBS_NOALLOC_MAX_DIM || A->d.n > DBS_NOALLOC_MAX_DIM)
+        return dbs_fail(DBS_ERR_UNSUPPORTED,
+                        "dbs_spmspv_noalloc: matrix %dx%d exceeds the static scratch's limit of %d rows and columns",
+                        A->d.m, A->d.n, DBS_NOALLOC_MAX_DIM);
+    int mode = 0;
+    dbs_status st = spmspv_check_args(A, sr, x_nnz, d_x_idx, d_x_val, path, d_y_idx, d_y_val, d_y_nnz, &mode);
+    if (st != DBS_OK) return st;
+    const hipStream_t s = (hipStream_t)stream;
+    std::lock_guard<std::mutex> lock(g_na_mu);
+    NoAllocDevice *d = nullptr;
+    if ((st = noalloc_device(s, &d)) != DBS_OK) return st;
+    DevCtx c = noalloc_ctx(*d);
+    st = spmspv_launches(A, c, s, mode, sr, x_nnz, d_x_idx, d_x_val, d_mask, complement_mask, path, th3, d_y_idx,
+                         d_y_val, d_y_nnz, [](int, auto &&launch) -> dbs_status {
+                             const hipError_t e = launch();
+                             return e == hipSuccess ? DBS_OK : hip_fail(e, "kernel launch");
+                         });
+    d->scan_parity = c.scan_parity;
+    d->fin_parity = c.fin_parity;
+    return st;
 }
