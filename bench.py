@@ -14,8 +14,11 @@ when timing starts.
 `value` is GB/s of algorithmic bytes (paper_2608_16308_amd.bytes_model) over
 the timed steps.  Also reported: per-density GB/s and GFLOP/s (useful flops
 2 * sum of nnz of the active columns, and the paper's SpMV convention
-2 * nnz(A)), the roofline of the traversal kernel from HIP events on the
-library's stream, the CPU oracle on the same inputs, and BFS GTEPS on an
+2 * nnz(A)); the roofline of the traversal kernels from HIP events on the
+library's stream, quoted from the cold protocol (every call alone after a
+1 GiB write that evicts the Infinity Cache and the L2s) with the warm figure
+beside it; the CPU oracle on the same inputs (SpMSpV per point and BFS, one
+thread, with the host's core count and CPU model); and BFS GTEPS on an
 R-MAT scale-22 graph from 16 sources (--bfs-scale 0 to skip).
 """
 from __future__ import annotations
@@ -63,6 +66,22 @@ def read_traffic(digest: str):
     return None
 
 
+PROFILE_BFS_TRAFFIC = os.path.join(ROOT, "profiles", "bfs_rmat22_traffic.md")
+
+
+def read_bfs_traffic(digest: str):
+    """HBM bytes of whole BFS calls per source from the committed counter
+    summary, if it was taken on the current kernel sources."""
+    if not os.path.exists(PROFILE_BFS_TRAFFIC):
+        return None
+    for line in open(PROFILE_BFS_TRAFFIC):
+        if line.startswith("bfs_traffic_json:"):
+            d = json.loads(line.split(":", 1)[1])
+            if d.get("kernel_sources") == digest:
+                return d.get("bytes_per_source")
+    return None
+
+
 def _time_call(torch, fn, reps):
     """Mean microseconds of fn() over reps back-to-back calls (HIP events on
     torch's current stream, which the library's context uses)."""
@@ -104,7 +123,7 @@ def _cold_us(torch, fn, reps, flush, ctx=None):
         if rnd:
             ctx.enable_timing(False)
     out = (float(np.median(whole)), float(np.mean(whole)))
-    return out + ((float(np.median(trav)),) if ctx is not None else ())
+    return out + ((float(np.median(trav)), float(np.mean(trav))) if ctx is not None else ())
 
 
 def copy_bandwidth(torch, dev, reps=10):
@@ -149,7 +168,7 @@ def other_configs(args, torch, dbs, wl, dev, flush):
         st = ctx.spmspv_raw(A, dxi, dxv, y_idx, y_val, y_nnz, stats=True)
         mod = model.call(xi, st["path"])
         us = _time_call(torch, call, reps)
-        cold, _, cold_trav = _cold_us(torch, call, reps, flush, ctx)
+        cold, _, cold_trav, _ = _cold_us(torch, call, reps, flush, ctx)
         rows.append({"density": d, "k": int(xi.size), "path": st["path"], "n_nzblk": st["n_nzblk"],
                      "y_nnz": st["y_nnz"], "bytes": mod["bytes_total"], "us": round(us, 2),
                      "GBs": round(mod["bytes_total"] / (us * 1e-6) / 1e9, 1),
@@ -179,7 +198,7 @@ def other_configs(args, torch, dbs, wl, dev, flush):
         mod = model.call_dense(nz, st["path"])
         call = lambda: ctx.spmspv_dense(A, x, y=y)
         us = _time_call(torch, call, reps)
-        cold, _, cold_trav = _cold_us(torch, call, reps, flush, ctx)
+        cold, _, cold_trav, _ = _cold_us(torch, call, reps, flush, ctx)
         wd = torch.from_numpy(w.dense().astype(np.float16)).to(dev)
         xr = x.view(1, in_f)
         lin = lambda: F.linear(xr, wd)
@@ -385,6 +404,63 @@ def run_ablation(args, torch, dbs, wl, dev):
             json.dump(out, f)
 
 
+def profile_cold(args, torch, dbs, wl, dev, ctx, A, points, run):
+    """Cold calls for counter passes: per sweep point --point-reps calls, each
+    alone after a write of a 1 GiB buffer (the bench's cold protocol); then 20
+    warm calls of the 11008x4096 decode layer; then BFS from --bfs-sources
+    sources of R-MAT --bfs-scale.  Prints the order of the work as JSON."""
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    order = []
+    for p in points:
+        for i in range(args.point_reps):
+            flush.fill_(float(i + 1))
+            run(p)
+        torch.cuda.synchronize()
+        order.append({"density": p["density"], "x": p["kind"], "path": p["path"], "calls": args.point_reps,
+                      "bytes_main": p["model"]["bytes_main"]})
+    del flush
+    w = wl.decode_layer(11008, 4096)
+    W = dbs.Matrix.from_csr(w.m, w.n, w.row_ptr, w.col_idx, w.vals)
+    wctx = dbs.Context(W)
+    x = torch.from_numpy(wl.decode_activation(4096, key=0).view(np.int16)).to(dev).view(torch.float16)
+    y = torch.empty(w.m, dtype=torch.float16, device=dev)
+    for _ in range(20):
+        wctx.spmspv_dense(W, x, y=y)
+    torch.cuda.synchronize()
+    del wctx, W
+    bfs = None
+    if args.bfs_scale > 0:
+        g = wl.rmat(args.bfs_scale, values=False)
+        srcs = wl.bfs_sources(g, args.bfs_sources, key=0)
+        G = dbs.Matrix.from_csr(g.m, g.n, g.row_ptr, g.col_idx, None)
+        gctx = dbs.Context(G)
+        level = torch.empty(g.n, dtype=torch.int32, device=dev)
+        parent = torch.empty(g.n, dtype=torch.int32, device=dev)
+        comp = wl.components(g)
+        deg = np.diff(g.row_ptr)
+        bfs = []
+        for s0 in srcs:
+            _, _, st = gctx.bfs(G, int(s0), level=level, parent=parent, stats=True)
+            bfs.append({"source": int(s0), "levels": st["levels"], "paths": st["path"],
+                        "edges": int(deg[comp == comp[s0]].sum()) // 2})
+        torch.cuda.synchronize()
+    print(json.dumps({"profile_run": "cold", "points": order, "decode_calls": 20, "bfs": bfs,
+                      "kernel_sources": kernel_sources_digest()}), flush=True)
+
+
+def cpu_description() -> dict:
+    """The host the CPU oracle runs on: logical cores and CPU model."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"host_logical_cores": os.cpu_count(), "cpu_model": model}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -394,6 +470,8 @@ def main():
     ap.add_argument("--bfs-scale", type=int, default=22)
     ap.add_argument("--bfs-sources", type=int, default=16)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--cpu-bfs-seconds", type=float, default=6.0,
+                    help="oracle BFS sample: sources are timed until this many seconds are spent")
     ap.add_argument("--point-reps", type=int, default=20)
     ap.add_argument("--json-out", default=None)
     ap.add_argument("--other-configs", type=int, default=1,
@@ -402,9 +480,11 @@ def main():
                     help="path / format / selector ablation on R-MAT (no bench line): push vs pull over a "
                          "finer density grid, the crossover in s_b = N_nzblk / N_blk, forced block formats, "
                          "and BFS under candidate th3 values")
-    ap.add_argument("--profile-run", action="store_true",
+    ap.add_argument("--profile-run", nargs="?", const="warm", default=None, choices=("warm", "cold"),
                     help="short run for rocprofv3 counter passes: a 1 GiB device copy (counter "
-                         "calibration) then warm-up + timed steps of the sweep only")
+                         "calibration), then either (warm) warm-up + timed steps of the sweep, or (cold) "
+                         "--point-reps calls per sweep point each after a 1 GiB cache flush, the 11008x4096 "
+                         "decode layer and BFS from --bfs-sources sources of R-MAT --bfs-scale")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py: this build runs on one GPU only (single-GPU kernel library; "
@@ -469,6 +549,9 @@ def main():
         assert p["model"]["n_nzblk"] == st["n_nzblk"] and p["model"]["y_nnz"] == st["y_nnz"]
     step_bytes = sum(p["model"]["bytes_total"] for p in points)
     step_main_bytes = sum(p["model"]["bytes_main"] for p in points)
+    if args.profile_run == "cold":
+        profile_cold(args, torch, dbs, wl, dev, ctx, A, points, run)
+        return
     step_useful = sum(p["model"]["useful_nnz"] for p in points)
     step_comp = sum(p["model"]["bytes_compulsory"] for p in points)
 
@@ -514,7 +597,7 @@ def main():
     flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
     copy_gbs = copy_bandwidth(torch, dev)
     log(f"[bench] 1 GiB device copy: {copy_gbs:.1f} GB/s")
-    cold_main_s = cold_whole_s = 0.0
+    cold_main_s = cold_median_main_s = cold_whole_s = 0.0
     sweep = []
     for p in points:
         row = {"density": p["density"], "x": p["kind"], "k": p["model"]["k"], "path": p["path"],
@@ -537,12 +620,14 @@ def main():
             if path == "auto":
                 row["useful_GFLOPs"] = round(2 * p["model"]["useful_nnz"] / (us * 1e-6) / 1e9, 2)
                 row["spmv_conv_GFLOPs"] = round(2 * a.nnz / (us * 1e-6) / 1e9, 1)
-        cold, cold_mean, cold_trav = _cold_us(torch, lambda: run(p), args.point_reps, flush, ctx)
+        cold, cold_mean, cold_trav, cold_trav_mean = _cold_us(torch, lambda: run(p), args.point_reps, flush, ctx)
         row["cold_us"] = round(cold, 2)
         row["cold_mean_us"] = round(cold_mean, 2)
         row["cold_GBs"] = round(p["model"]["bytes_total"] / (cold * 1e-6) / 1e9, 1)
         row["cold_traversal_us"] = round(cold_trav, 2)
-        cold_main_s += cold_trav * 1e-6
+        row["cold_traversal_mean_us"] = round(cold_trav_mean, 2)
+        cold_main_s += cold_trav_mean * 1e-6
+        cold_median_main_s += cold_trav * 1e-6
         cold_whole_s += cold * 1e-6
         sweep.append(row)
         log(f"[bench] {row}")
@@ -559,9 +644,21 @@ def main():
     reps = max(1, int(args.cpu_seconds / max(one, 1e-6)))
     cpu_s = om.time_spmspv(xs, reps)
     cpu_value = step_bytes * reps / cpu_s / 1e9
-    log(f"[bench] oracle: {reps} passes of the 8-point sweep in {cpu_s:.2f}s -> {cpu_value:.3f} GB/s")
+    # per point: microseconds per call and useful GFLOP/s (each point alone,
+    # about a tenth of the sample's time per point)
+    cpu_points = []
+    for p, x in zip(points, xs):
+        t1 = om.time_spmspv([x], 1)
+        r = max(1, int(0.1 * args.cpu_seconds / len(points) / max(t1, 1e-6)))
+        us = om.time_spmspv([x], r) / r * 1e6
+        cpu_points.append({"density": p["density"], "x": p["kind"], "us": round(us, 1),
+                           "useful_GFLOPs": round(2 * p["model"]["useful_nnz"] / (us * 1e-6) / 1e9, 3)})
+    log(f"[bench] oracle: {reps} passes of the 8-point sweep in {cpu_s:.2f}s -> {cpu_value:.3f} GB/s; {cpu_points}")
     del om
 
+    selector = {"rule": "push iff N_nzblk < th3 * N_blk (Sec. 3.3.1), th3 = 0.01; also push when x is "
+                        "spread (fewer than 2 indices per nonzero vector block) and N_nzblk < 0.12 N_blk",
+                "th3": 0.01, "spread_th3": 0.12, "spread_indices_per_block": 2}
     result = {
         "metric": "SpMSpV GB/s (fraction of HBM peak) + GFLOP/s vs x density; BFS GTEPS",
         "value": round(value, 2),
@@ -577,20 +674,26 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"rmat{args.scale}_spmspv_density_sweep", "scale": args.scale,
                    "edge_factor": 16, "n": a.n, "nnz": a.nnz, "densities": DENSITIES, "x_kinds": KINDS,
-                   "calls_per_step": len(points), "semiring": "plus_times", "path": "auto", "th3": 0.01,
-                   "nblk": info["nblk"], "db_build_s": round(build_s, 2),
+                   "calls_per_step": len(points), "semiring": "plus_times", "path": "auto",
+                   "selector": selector, "nblk": info["nblk"], "db_build_s": round(build_s, 2),
                    "useful_GFLOPs": round(2 * step_useful * args.steps / elapsed / 1e9, 2)},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": read_traffic(kernel_sources_digest()),
-                     "kernel": "k_main (push/pull traversal)", "avg_launch_us": round(main_avg_ms * 1e3, 2),
+        # the traversal kernels (push and/or pull launches of a call) under the
+        # cold protocol: every call alone after a 1 GiB write that evicts the
+        # Infinity Cache and the L2s; achieved = algorithmic bytes of the
+        # eight calls / sum over the points of the mean traversal time per
+        # call (HIP events on the library stream)
+        "roofline": {"bound": "hbm", "achieved": round(cold_achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(cold_achieved / HBM_PEAK_GBS, 4), "traffic": read_traffic(kernel_sources_digest()),
+                     "kernel": "k_traverse (push/pull traversal)", "protocol": "cold",
+                     "avg_launch_us": round(cold_main_s / len(points) * 1e6, 2),
                      "algorithmic_bytes_per_launch": round(step_main_bytes / len(points)),
-                     "copy_GBs": round(copy_gbs, 1), "frac_of_copy": round(achieved / copy_gbs, 4)},
-        # the same kernels with the Infinity Cache and L2 flushed before
-        # every call (one call at a time, median per point)
-        "roofline_cold": {"achieved": round(cold_achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                          "frac": round(cold_achieved / HBM_PEAK_GBS, 4),
-                          "frac_of_copy": round(cold_achieved / copy_gbs, 4),
-                          "whole_path_GBs": round(step_bytes / cold_whole_s / 1e9, 1)},
+                     "frac_median_times": round(step_main_bytes / cold_median_main_s / 1e9 / HBM_PEAK_GBS, 4),
+                     "copy_GBs": round(copy_gbs, 1), "frac_of_copy": round(cold_achieved / copy_gbs, 4),
+                     "whole_path_GBs": round(step_bytes / cold_whole_s / 1e9, 1)},
+        # the same kernels back to back in the timed steps (caches warm)
+        "roofline_warm": {"achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(achieved / HBM_PEAK_GBS, 4), "avg_launch_us": round(main_avg_ms * 1e3, 2),
+                          "frac_of_copy": round(achieved / copy_gbs, 4)},
         # path-independent view: the compulsory bytes (every stored entry of
         # the active columns, its x value and the y output) per second; the
         # model bytes depend on the path taken (push touches fewer)
@@ -599,7 +702,10 @@ def main():
                        "model_over_compulsory": round(step_bytes / step_comp, 3)},
         "cpu_baseline": {"value": round(cpu_value, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
                          "sample": f"{reps} passes over the same 8 x vectors on R-MAT {args.scale} "
-                                   f"({cpu_s:.1f} s, CSC built once outside the timing)"},
+                                   f"({cpu_s:.1f} s, CSC built once outside the timing); GB/s counts the "
+                                   f"GPU path's algorithmic bytes of the same calls",
+                         **cpu_description(),
+                         "points": cpu_points},
         "sweep": sweep,
     }
     if extra is not None:
@@ -640,6 +746,37 @@ def main():
                          "gteps_min": round(min(gteps), 3), "gteps_max": round(max(gteps), 3),
                          "ms_mean": round(1e3 * float(np.mean(times)), 3), "db_build_s": round(gbuild, 2),
                          "edges_counted": "undirected edges of the source's component", "per_source": per_src}
+        # HBM traffic of whole BFS calls (every kernel of the call) from the
+        # committed counter summary, when it was taken on these kernel sources
+        bt = read_bfs_traffic(kernel_sources_digest())
+        if bt:
+            ach = [bt[str(p["source"])] / (p["ms"] * 1e-3) / 1e9 for p in per_src if str(p["source"]) in bt]
+            if ach:
+                result["bfs"]["traffic_roofline"] = {
+                    "bound": "hbm", "achieved": round(float(np.mean(ach)), 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(float(np.mean(ach)) / HBM_PEAK_GBS, 4), "sources": len(ach),
+                    "basis": "rocprofv3 FETCH_SIZE + WRITE_SIZE of every kernel of a BFS call / its time"}
+        del gctx, G, level, parent
+        torch.cuda.empty_cache()
+        # the CPU oracle's queue BFS on the first sources (single thread)
+        import oracle
+        og = oracle.OracleMatrix(g.n, g.n, g.row_ptr, g.col_idx, None)
+        cg, ct = [], []
+        t_budget = 0.0
+        for s0 in srcs:
+            dt = og.time_bfs([int(s0)])
+            edges = int(deg[comp == comp[s0]].sum()) // 2
+            cg.append(edges / dt / 1e9)
+            ct.append(dt)
+            t_budget += dt
+            if t_budget > args.cpu_bfs_seconds:
+                break
+        del og
+        result["cpu_baseline"]["bfs"] = {"gteps_hmean": round(len(cg) / sum(1.0 / x for x in cg), 4),
+                                         "ms_mean": round(1e3 * float(np.mean(ct)), 1), "sources": len(cg),
+                                         "sample": f"the first {len(cg)} of the {len(srcs)} sources, "
+                                                   f"CSC built once outside the timing"}
+        log(f"[bench] oracle BFS: {result['cpu_baseline']['bfs']}")
 
     line = json.dumps(result)
     if args.json_out:
