@@ -188,7 +188,8 @@ dbs_status dbs_storage_model(int64_t rows, int64_t cols, int64_t nnz, int32_t va
 /* Device-resident matrix.                                                */
 /* ---------------------------------------------------------------------- */
 
-/* Copies a host-side DB matrix to the current device (one upload). */
+/* Copies a host-side DB matrix to the current device (one upload).
+ * DBS_ERR_UNSUPPORTED for more than 2^26 block columns (n > 2^30).          */
 dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **out);
 
 /* dbs_host_build_csr + dbs_matrix_upload + dbs_host_destroy. */
@@ -228,7 +229,10 @@ typedef struct {
 
 /* Host buffers for a copy of the device arrays (any member may be NULL to
  * skip that array), each at least as long as dbs_matrix_layout says:
- * slot block columns (-1 padding, sign bit: non-COO block) and descriptors,
+ * slot words (bits 25..0 block column; bit 30 set for a COO block with one
+ * entry held inline, bits 29..26 then that entry's local column; -1 for
+ * padding and the sign bit set for a block of the non-COO list) and
+ * descriptors,
  * segment words (block row | 1 << 31 for a plain-store row), the block-CSC
  * pointer, rows and descriptors, the non-COO list's block columns,
  * descriptors, chunk starts and chunk block rows, and the payload.         */

@@ -181,6 +181,8 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
     *out = nullptr;
     dbs_status st = check_device();
     if (st != DBS_OK) return st;
+    if ((int64_t)h->nbc > MAX_BLOCK_COLS)
+        return dbs_fail(DBS_ERR_UNSUPPORTED, "n = %d: the device format holds at most 2^26 block columns", h->n);
     dbs_matrix *A = new (std::nothrow) dbs_matrix();
     if (!A) return dbs_fail(DBS_ERR_ALLOC, "host allocation failed");
     DevMatrix &d = A->d;
@@ -207,13 +209,12 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
             for (uint32_t i = 0; i < nb; ++i) {
                 const size_t slot = (size_t)16 * s + i;
                 const uint64_t dd = h->desc[first + i];
-                sl_col[slot] = h->cb_col[first + i];
+                sl_col[slot] = slot_word(h->cb_col[first + i], dd);
                 sl_desc[slot] = dd;
                 if (desc_type(dd) != T_COO) {
                     // pulled from the non-COO list (flagged in the slot by the
-                    // sign bit of its block column); a new chunk starts at a
-                    // new block row or after HV_CHUNK blocks
-                    sl_col[slot] |= (int32_t)0x80000000u;
+                    // sign bit of its word); a new chunk starts at a new block
+                    // row or after HV_CHUNK blocks
                     const int32_t brow = (int32_t)seg_brow(sg);
                     if (hv_crow.empty() || hv_crow.back() != brow ||
                         (int64_t)hv_col.size() - hv_cstart.back() == HV_CHUNK) {

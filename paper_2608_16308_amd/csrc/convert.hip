@@ -301,7 +301,7 @@ __global__ __launch_bounds__(CTPB) void k_conv_write(const void *w, int64_t ld, 
         const uint32_t bl = tb[tile] & 0x0FFFFFFFu, pi = tb[tile] >> 28;
         const int64_t b = P[0] + bl;
         const int64_t slot = (P[2] + (int64_t)tseg[tile]) * 16 + pi;
-        out.sl_col[slot] = J | (type != T_COO ? (int32_t)0x80000000u : 0);
+        out.sl_col[slot] = slot_word(J, d);
         out.sl_desc[slot] = d;
         out.blk_desc[b] = d;
         if (type != T_COO) {

@@ -51,6 +51,30 @@ DBS_HD bool desc_inline(uint64_t d) { return (d & DESC_INLINE) != 0; }
 DBS_HD uint32_t inline_capacity(uint32_t vbytes) { return 48u / (8u + 8u * vbytes); }
 DBS_HD uint32_t inline_shift(uint32_t e, uint32_t vbytes) { return 16u + e * (8u + 8u * vbytes); }
 
+// Device word of a pull-segment slot: the block column, and for a COO block
+// with one entry held inline in its descriptor also that entry's local
+// column, so that the compaction of the slots can test the exact x entry
+// without reading the descriptor:
+//   bits 25..0   block column (a matrix has at most 2^26 block columns)
+//   bits 29..26  local column of the single inline entry (bit 30 set)
+//   bit  30      the block is COO with exactly one entry, held inline
+//   bit  31      padding (the whole word is -1) or a block of the non-COO list
+constexpr int32_t SLOT_PAD = -1;
+constexpr uint32_t SLOT_J_MASK = (1u << 26) - 1u;
+constexpr uint32_t SLOT_ONE = 1u << 30;
+constexpr uint32_t SLOT_LISTED = 1u << 31;
+constexpr int64_t MAX_BLOCK_COLS = (int64_t)1 << 26;
+DBS_HD int32_t slot_word(int32_t J, uint64_t d)
+{
+    if (desc_type(d) != T_COO) return (int32_t)((uint32_t)J | SLOT_LISTED);
+    uint32_t w = (uint32_t)J;
+    if (desc_inline(d) && desc_nnz(d) == 1) w |= SLOT_ONE | ((uint32_t)((d >> 16) & 15u) << 26);
+    return (int32_t)w;
+}
+DBS_HD int32_t slot_col(int32_t w) { return (int32_t)((uint32_t)w & SLOT_J_MASK); }
+DBS_HD uint32_t slot_c(int32_t w) { return ((uint32_t)w >> 26) & 15u; }
+DBS_HD bool slot_one(int32_t w) { return w >= 0 && ((uint32_t)w & SLOT_ONE) != 0; }
+
 DBS_HD uint64_t seg_make(uint32_t first, uint32_t brow, uint32_t nb, bool single)
 {
     return (uint64_t)first | ((uint64_t)brow << 32) | ((uint64_t)(nb - 1) << 59) |

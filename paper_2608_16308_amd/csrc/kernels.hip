@@ -1481,7 +1481,8 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             vs[k] = k < spq && sid < a.nseg;
             s[k] = vs[k] ? __builtin_nontemporal_load(&a.seg_rs[sid]) : 0u;
             b[k] = (int32_t)(sid * 16 + i);
-            J[k] = vs[k] ? __builtin_nontemporal_load(&a.sl_col[b[k]]) : -1;
+            const int32_t w = vs[k] ? __builtin_nontemporal_load(&a.sl_col[b[k]]) : SLOT_PAD;
+            J[k] = w >= 0 ? slot_col(w) : -1;
             d[k] = (vs[k] && spec) ? __builtin_nontemporal_load(&a.sl_desc[b[k]]) : 0ull;
         }
         // block activity: the LDS bitmap when it fits, else the vector-block
@@ -1608,28 +1609,35 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
 // (more vector blocks than this many bits) the segment loop is used.
 constexpr int32_t COMPACT_BITMAP_WORDS = 8192;
 // Region r (wave r of the compaction fills it, wave r of the walk takes it)
-// covers spw consecutive segments and holds up to 16 spw entries.  False when
-// the list is absent or too small.
-__device__ __forceinline__ bool compact_pull(const MainArgs &a, int32_t N, int64_t &spw)
+// covers rcap / 16 consecutive segments and holds up to rcap entries.  False
+// when the list is absent or too small.
+__device__ __forceinline__ bool compact_pull(const MainArgs &a, int32_t N, int64_t &rcap)
 {
     const int nw = a.nreg;
-    spw = (a.nseg + nw - 1) / nw;
+    rcap = (a.nseg + nw - 1) / nw * 16;
     return a.clist != nullptr && a.nseg > 0 && (int64_t)N * 1000 < (int64_t)a.nbc * a.cpm &&
-           ((a.nbc + 31) >> 5) <= COMPACT_BITMAP_WORDS && (int64_t)nw * spw * 16 <= a.clist_cap;
+           ((a.nbc + 31) >> 5) <= COMPACT_BITMAP_WORDS && (int64_t)nw * rcap <= a.clist_cap;
 }
 
-// First half: wave gw takes segments [gw spw, (gw + 1) spw), one segment per
-// lane and round (its 16 block columns by four 16-byte loads), and appends
-// the slots that hold work -- a COO block (the listed non-COO blocks carry
-// the sign bit) whose vector block is active, in an admitted block row -- to
-// its own region, in slot order.  The region's entry count goes to
-// ccount[gw].  The activity bitmap is copied into LDS when it fits.
+// First half: wave gw takes the segments of its region, one segment per lane
+// and round (its 16 slot words by four 16-byte loads), and appends the slots
+// that hold work -- a COO block (the listed
+// non-COO blocks carry the sign bit) whose vector block is active, in an
+// admitted block row -- to its region of the list, in slot order.  When x is
+// spread (fewer than 4 indices per nonzero vector block on average, so that
+// most single entries miss), a block whose single entry is held inline is
+// listed only if x stores that entry's column (tested from the local column
+// in the slot word against the vector block's mask).  The region's entry
+// count goes to ccount[gw].  The activity bitmap is copied into LDS when it
+// fits.
 template <bool LDSBITS>
-__device__ void pull_compact(const MainArgs &a, int gw, int64_t spw)
+__device__ void pull_compact(const MainArgs &a, int gw, int64_t rcap)
 {
     const int lane = lane_id();
-    const int64_t s0 = (int64_t)gw * spw;
-    const int64_t s1 = min(a.nseg, s0 + spw);
+    const int32_t N = a.counters[C_NZBLK];
+    const bool exact = (int64_t)a.counters[C_XPOP] < 4 * (int64_t)N;
+    const int64_t s0 = (int64_t)gw * (rcap / 16);
+    const int64_t s1 = min(a.nseg, s0 + rcap / 16);
     int32_t *out = a.clist + s0 * 16;
     uint32_t n = 0;
     for (int64_t base = s0; base < s1; base += WAVE) {
@@ -1642,12 +1650,33 @@ __device__ void pull_compact(const MainArgs &a, int gw, int64_t spw)
             const int32_t col[16] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w,
                                      c2.x, c2.y, c2.z, c2.w, c3.x, c3.y, c3.z, c3.w};
             if (am) {
+                uint32_t one = 0;
+                uint32_t m16[LDSBITS ? 1 : 16];
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
+                    const int32_t J = slot_col(col[i]);
                     bool on = col[i] >= 0;
-                    if constexpr (LDSBITS) on = on && block_active(col[i]);
-                    else on = on && mask16(a.xmask, col[i]) != 0u;
+                    if constexpr (LDSBITS) {
+                        on = on && block_active(J);
+                    } else {
+                        m16[i] = on ? mask16(a.xmask, J) : 0u;
+                        on = m16[i] != 0u;
+                    }
                     f |= (on ? 1u : 0u) << i;
+                    one |= (exact && on && slot_one(col[i]) ? 1u : 0u) << i;
+                }
+                if (one) {
+                    // (with the bitmap in LDS, the masks of all such slots of
+                    // the segment are gathered together)
+                    uint32_t mw[16];
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        if constexpr (LDSBITS) mw[i] = ((one >> i) & 1u) ? mask16(a.xmask, slot_col(col[i])) : 0u;
+                        else mw[i] = m16[i];
+                    }
+#pragma unroll
+                    for (int i = 0; i < 16; ++i)
+                        if (((one >> i) & 1u) && !((mw[i] >> slot_c(col[i])) & 1u)) f &= ~(1u << i);
                 }
             }
         }
@@ -1672,18 +1701,18 @@ __global__ __launch_bounds__(TPB) void k_pull_compact(MainArgs a)
 {
     __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE, 1>::WORDS];
     const int32_t N = a.counters[C_NZBLK];
-    int64_t spw;
-    if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, spw)) return;
+    int64_t rcap;
+    if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, rcap)) return;
     const int gw = blockIdx.x * (TPB / WAVE) + (threadIdx.x >> 6);
     const int32_t nwords = (a.nbc + 31) >> 5;
     if (nwords <= COMPACT_BITMAP_WORDS) {  // (always, by compact_pull)
         for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
         __syncthreads();
         pull_rows<MODE, true>(a, rows_lds);
-        if (gw < a.nreg) pull_compact<true>(a, gw, spw);
+        if (gw < a.nreg) pull_compact<true>(a, gw, rcap);
     } else {
         pull_rows<MODE, false>(a, rows_lds);
-        if (gw < a.nreg) pull_compact<false>(a, gw, spw);
+        if (gw < a.nreg) pull_compact<false>(a, gw, rcap);
     }
 }
 
@@ -1849,7 +1878,7 @@ struct ActiveLds {
 };
 
 template <int MODE>
-__device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t spw)
+__device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rcap)
 {
     const int lane = lane_id();
     float *sy = (float *)L.acc;
@@ -1859,7 +1888,7 @@ __device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t spw
     if (lane < RUN_CAP) L.hm[lane] = 0u;
     wave_lds_sync();
     const uint32_t cnt = a.ccount[gw];
-    const int32_t *list = a.clist + (int64_t)gw * spw * 16;
+    const int32_t *list = a.clist + (int64_t)gw * rcap;
     constexpr int IM = inline_max<MODE>();
     for (uint32_t base = 0; base < cnt;) {
         bool v[SLOTS];
@@ -1874,7 +1903,7 @@ __device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t spw
         uint64_t d[SLOTS];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
-            J[k] = v[k] ? a.sl_col[slot[k]] : -1;
+            J[k] = v[k] ? slot_col(a.sl_col[slot[k]]) : -1;  // (listed slots are COO blocks)
             d[k] = v[k] ? a.sl_desc[slot[k]] : 0ull;
             R[k] = v[k] ? (int32_t)(a.seg_rs[slot[k] >> 4] & 0x7FFFFFFFu) : -1;
         }
@@ -2016,10 +2045,10 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(Mai
     const int w = threadIdx.x >> 6, lane = lane_id();
     if constexpr (PATH == PATH_PUSH) {
         if (path == PATH_PULL) {
-            int64_t spw;
+            int64_t rcap;
             const int gw = blockIdx.x * (TPB / WAVE) + w;
-            if (a.nreg > 0 && compact_pull(a, N, spw) && gw < a.nreg)
-                pull_active<MODE>(a, ((ActiveLds *)lds_raw)[w], gw, spw);
+            if (a.nreg > 0 && compact_pull(a, N, rcap) && gw < a.nreg)
+                pull_active<MODE>(a, ((ActiveLds *)lds_raw)[w], gw, rcap);
             return;
         }
     }
@@ -2044,8 +2073,8 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(Mai
         const int32_t nwords = (a.nbc + 31) >> 5;
         // below the compaction threshold: the non-COO blocks and the
         // compaction of the segments (the push kernel walks the regions)
-        int64_t spw;
-        const bool compact = a.nreg > 0 && compact_pull(a, N, spw);
+        int64_t rcap;
+        const bool compact = a.nreg > 0 && compact_pull(a, N, rcap);
         if (!pull_takes_compaction<MODE>() && compact) return;  // k_pull_compact
         if (nwords <= LDS_BITMAP_WORDS) {
             for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
@@ -2054,7 +2083,7 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(Mai
             pull_rows<MODE, true>(a, (uint32_t *)lds_raw);
             if constexpr (pull_takes_compaction<MODE>()) {
                 if (compact) {
-                    if (gw < a.nreg) pull_compact<true>(a, gw, spw);
+                    if (gw < a.nreg) pull_compact<true>(a, gw, rcap);
                     return;
                 }
             }
