@@ -326,6 +326,40 @@ def run_ablation(args, torch, dbs, wl, dev):
     out["basic_alg1"] = {"matrix": f"R-MAT {args.scale}", "rows": basic}
     del ctx, A, B
 
+    # (1c) single launch (blocker, selector, traversal and compaction of y in
+    # one kernel, Sec. 4.1) against separate launches, for the index lists
+    # short enough for it: whole-call microseconds warm (back to back) and
+    # cold (each call alone after a 1 GiB write), and the host time to
+    # enqueue one call
+    A = dbs.Matrix.from_csr(a.m, a.n, a.row_ptr, a.col_idx, a.vals)
+    ctx = dbs.Context(A)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    single = []
+    for di, d in enumerate([1e-4, 2e-4, 5e-4, 1e-3, 2e-3]):
+        for kind in KINDS:
+            xi, xv = wl.sparse_x(a.n, d, kind, key=(23, di, KINDS.index(kind)))
+            if xi.size > 2048:
+                continue
+            dxi, dxv = torch.from_numpy(xi).to(dev), torch.from_numpy(xv).to(dev)
+            row = {"density": d, "x": kind, "k": int(xi.size)}
+            for on in (False, True):
+                ctx.set_single_launch(on)
+                fn = lambda: ctx.spmspv_raw(A, dxi, dxv, y_idx, y_val, y_nnz)
+                tag = "single" if on else "separate"
+                row[f"{tag}_warm_us"] = round(_time_call(torch, fn, 100), 2)
+                row[f"{tag}_cold_us"] = round(_cold_us(torch, fn, 20, flush)[0], 2)
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for _ in range(100):
+                    fn()
+                row[f"{tag}_host_enqueue_us"] = round((time.perf_counter() - t0) * 1e4, 2)
+                torch.cuda.synchronize()
+            ctx.set_single_launch(False)
+            single.append(row)
+            log(f"[ablation] single launch {row}")
+    out["single_launch"] = {"matrix": f"R-MAT {args.scale}", "rows": single}
+    del ctx, A, flush
+
     # (2) forced formats (all blocks COO / all patched CSR / classifier)
     fmt = {}
     for name, force in (("classifier", -1), ("coo_only", 0), ("csr_only", 4)):

@@ -265,13 +265,29 @@ dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs_ctx **out)
 dbs_status dbs_ctx_set_stream(dbs_ctx *ctx, void *stream);
 void dbs_ctx_destroy(dbs_ctx *ctx);
 
+/* Single-launch execution (Sec. 4.1 generates the vector mask and counts
+ * the nonzero blocks inside the SpMSpV launch).  enable != 0: a dbs_spmspv
+ * call with at most 2048 x indices, on a matrix of at most 131072 block
+ * columns, runs as ONE kernel launch -- blocker and selector in one
+ * workgroup while the others wait on a ready word, the chosen traversal
+ * (pull by the segment loop), then the compaction of y by the first
+ * workgroups once every workgroup has set its own done word.  Same results
+ * and statistics as the separate launches.  enable = 0 (the default of a
+ * new context, and the only mode of dbs_spmspv_noalloc): blocker/scan,
+ * traversal and compaction as kernels of their own, which measured faster
+ * on the device (the single launch costs the host a third of the enqueue
+ * time).  Single-launch calls on different streams may overlap in time.     */
+dbs_status dbs_ctx_set_single_launch(dbs_ctx *ctx, int enable);
+
 typedef struct {
     int32_t path;         /* dbs_path actually taken (PUSH or PULL) */
     int32_t n_nzblk;      /* nonzero vector blocks, N_nzblk (Sec. 3.3.1) */
     int32_t n_blk;        /* vector blocks, N_blk = ceil(n/16) */
     int32_t y_nnz;        /* entries written to y */
     int64_t tasks;        /* push: block tasks; pull: segments scanned */
-    int32_t error_flags;  /* bit 0: x index out of range (skipped); bit 1: duplicate x index */
+    int32_t error_flags;  /* bit 0: x index out of range (skipped); bit 1: duplicate x index;
+                             bit 2: single launch: a bounded wait for other workgroups ran
+                             out (y is not valid) */
     int32_t reserved;
 } dbs_call_stats;
 
@@ -430,7 +446,9 @@ typedef enum {
     DBS_K_FINALIZE = 3,  /* compaction / conversion of y, scratch reset       */
     DBS_K_BFS_UPDATE = 4,/* BFS level, visited and frontier update            */
     DBS_K_OTHER = 5,     /* BFS init / finish                                 */
-    DBS_K_COUNT = 6
+    DBS_K_FUSED = 6,     /* single launch: blocker, selector, traversal and
+                            compaction of y (up to 2048 x indices)            */
+    DBS_K_COUNT = 7
 } dbs_kernel_class;
 
 typedef struct {

@@ -358,6 +358,10 @@ class Context:
             lib().dbs_ctx_destroy(h)
             self._h = None
 
+    def set_single_launch(self, on: bool = True):
+        """Short index lists (<= 2048) as one kernel launch (default off)."""
+        check(lib().dbs_ctx_set_single_launch(self._h, 1 if on else 0))
+
     # -- measurement hooks
     def enable_timing(self, on: bool = True):
         check(lib().dbs_ctx_enable_timing(self._h, 1 if on else 0))

@@ -17,7 +17,7 @@ DBS_PLUS_TIMES, DBS_OR_AND = 0, 1
 DBS_PATH_AUTO, DBS_PATH_PUSH, DBS_PATH_PULL = 0, 1, 2
 DBS_BLK_COO, DBS_BLK_DENSE, DBS_BLK_FCSR, DBS_BLK_FCSC, DBS_BLK_CSR = range(5)
 BLOCK_TYPE_NAMES = ["coo", "dense", "fcsr", "fcsc", "csr"]
-DBS_K_NAMES = ["scatter", "scan", "main", "finalize", "bfs_update", "other"]
+DBS_K_NAMES = ["scatter", "scan", "main", "finalize", "bfs_update", "other", "fused"]
 DBS_BFS_MAX_LEVEL_STATS = 64
 DBS_MAX_BATCH = 8
 
@@ -28,7 +28,7 @@ EXPORTED = [
     "dbs_ctx_destroy", "dbs_spmspv", "dbs_spmspv_dense", "dbs_spmm_dense", "dbs_bfs", "dbs_ctx_enable_timing",
     "dbs_ctx_read_timing", "dbs_last_error", "dbs_version", "dbs_basic_build", "dbs_basic_destroy",
     "dbs_basic_spmspv", "dbs_matrix_build_dense", "dbs_matrix_layout_get", "dbs_matrix_download",
-    "dbs_spmspv_noalloc",
+    "dbs_spmspv_noalloc", "dbs_ctx_set_single_launch",
 ]
 DBS_NOALLOC_MAX_DIM = 1 << 20
 
@@ -82,7 +82,7 @@ class BfsStats(ctypes.Structure):
 
 
 class Timing(ctypes.Structure):
-    _fields_ = [("ms", ctypes.c_double * 6), ("launches", ctypes.c_int64 * 6)]
+    _fields_ = [("ms", ctypes.c_double * 7), ("launches", ctypes.c_int64 * 7)]
 
 
 class DbsError(RuntimeError):
@@ -136,6 +136,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dbs_spmm_dense": (ctypes.c_int, [vp, vp, i32, vp, vp, vp, P(CallStats)]),
         "dbs_bfs": (ctypes.c_int, [vp, vp, i32, vp, vp, ctypes.c_int, f32, P(BfsStats)]),
         "dbs_ctx_enable_timing": (ctypes.c_int, [vp, ctypes.c_int]),
+        "dbs_ctx_set_single_launch": (ctypes.c_int, [vp, ctypes.c_int]),
         "dbs_ctx_read_timing": (ctypes.c_int, [vp, P(Timing)]),
         "dbs_basic_build": (ctypes.c_int, [i32, i32, i64, vp, vp, vp, P(vp)]),
         "dbs_basic_destroy": (None, [vp]),

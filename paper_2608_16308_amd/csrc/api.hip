@@ -92,6 +92,7 @@ struct dbs_ctx {
     double ms[DBS_K_COUNT] = {0};
     int64_t launches[DBS_K_COUNT] = {0};
     bool broken = false;
+    bool single = false;  // one launch per call for short index lists (fused_fits)
     // batched dense activations: DBS_MAX_BATCH padded x copies and
     // accumulator sets, allocated by the first batched call
     void *xdb = nullptr;
@@ -370,7 +371,8 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
         (st = dev_zeros(ctx->allocs, (size_t)c.n_st_fin, &c.st_fin[0])) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.n_st_fin, &c.st_fin[1])) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)compact_list_entries(sizing->d.nseg), &c.clist)) != DBS_OK ||
-        (st = dev_zeros(ctx->allocs, (size_t)compact_list_regions(), &c.ccount)) != DBS_OK) {
+        (st = dev_zeros(ctx->allocs, (size_t)compact_list_regions(), &c.ccount)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)SYNC_WORDS, &c.sync)) != DBS_OK) {
         free_all(ctx->allocs);
         delete ctx;
         return st;
@@ -412,6 +414,13 @@ extern "C" void dbs_ctx_destroy(dbs_ctx *ctx)
     if (ctx->yaccb) (void)hipFree(ctx->yaccb);
     if (ctx->h_counters) (void)hipHostFree(ctx->h_counters);
     delete ctx;
+}
+
+extern "C" dbs_status dbs_ctx_set_single_launch(dbs_ctx *ctx, int enable)
+{
+    if (!ctx) return dbs_fail(DBS_ERR_ARG, "NULL context");
+    ctx->single = enable != 0;
+    return DBS_OK;
 }
 
 extern "C" dbs_status dbs_ctx_enable_timing(dbs_ctx *ctx, int enable)
@@ -484,8 +493,17 @@ template <class Run>
 dbs_status spmspv_launches(const dbs_matrix *A, DevCtx &c, hipStream_t s, int mode, dbs_semiring sr,
                            int32_t x_nnz, const int32_t *d_x_idx, const void *d_x_val, const uint32_t *d_mask,
                            int complement_mask, dbs_path path, float th3, int32_t *d_y_idx, void *d_y_val,
-                           int32_t *d_y_nnz, Run &&run)
+                           int32_t *d_y_nnz, bool single, Run &&run)
 {
+    if (single && fused_fits(A->d, x_nnz)) {
+        // a short index list: the whole call in one launch (the device
+        // chooses the path; pull takes the segment loop)
+        return run(DBS_K_FUSED, [&] {
+            return launch_fused(A->d, c, mode, x_nnz, d_x_idx, d_x_val, d_mask, complement_mask ? 1 : 0, (int)path,
+                                (double)norm_th3(th3), spread_th3(th3), d_y_idx,
+                                sr == DBS_OR_AND ? nullptr : d_y_val, d_y_nnz, s);
+        });
+    }
     // The automatic choice (push iff N_nzblk < th3 N_blk) is made on the
     // device, so both traversal kernels are launched and one returns at once.
     // Often k alone settles it: N_nzblk <= k, and N_nzblk >= ceil(k / 16)
@@ -538,7 +556,7 @@ extern "C" dbs_status dbs_spmspv(dbs_ctx *ctx, const dbs_matrix *A, dbs_semiring
     st = spmspv_check_args(A, sr, x_nnz, d_x_idx, d_x_val, path, d_y_idx, d_y_val, d_y_nnz, &mode);
     if (st != DBS_OK) return st;
     st = spmspv_launches(A, ctx->c, ctx->stream, mode, sr, x_nnz, d_x_idx, d_x_val, d_mask, complement_mask, path,
-                         th3, d_y_idx, d_y_val, d_y_nnz, [ctx](int cls, auto &&launch) -> dbs_status {
+                         th3, d_y_idx, d_y_val, d_y_nnz, ctx->single, [ctx](int cls, auto &&launch) -> dbs_status {
                              Timer t_(ctx, cls);
                              const hipError_t e = launch();
                              if (e != hipSuccess) {
@@ -726,13 +744,15 @@ constexpr size_t NA_YBITS = NA_YACC + na_round((size_t)16 * NA_NB * 8);         
 constexpr size_t NA_COUNTERS = NA_YBITS + na_round((size_t)NA_NXWORDS * 4);     // counters
 constexpr size_t NA_ST = NA_COUNTERS + na_round((size_t)C_COUNT * 4);           // statuses: scan x2, fin x2
 constexpr size_t NA_ST_SCAN_BYTES = na_round((size_t)NA_ST_SCAN * 8), NA_ST_FIN_BYTES = na_round((size_t)NA_ST_FIN * 8);
-constexpr size_t NA_END = NA_ST + 2 * NA_ST_SCAN_BYTES + 2 * NA_ST_FIN_BYTES;
+constexpr size_t NA_SYNC = NA_ST + 2 * NA_ST_SCAN_BYTES + 2 * NA_ST_FIN_BYTES;  // single-launch flags
+constexpr size_t NA_END = NA_SYNC + na_round((size_t)SYNC_WORDS * 4);
 static_assert(NA_END <= DBS_NOALLOC_SCRATCH_BYTES, "the static scratch holds the buffers of a maximal call");
 
 constexpr int NA_MAX_DEVICES = 64;
 struct NoAllocDevice {
     uint8_t *ptr = nullptr;  // device address of this GPU's copy of `scratch`
     int scan_parity = 0, fin_parity = 0;
+    uint32_t gen = 0;        // number of the last single-launch call
 };
 NoAllocDevice g_na[NA_MAX_DEVICES];
 std::mutex g_na_mu;  // guards g_na (held for the whole host side of a call)
@@ -791,6 +811,8 @@ DevCtx noalloc_ctx(const NoAllocDevice &d)
     c.n_st_fin = finalize_tiles(NA_NB) + 1;
     c.scan_parity = d.scan_parity;
     c.fin_parity = d.fin_parity;
+    c.sync = (uint32_t *)(d.ptr + NA_SYNC);
+    c.gen = d.gen;
     // no compaction list: pull takes the segment loop at every activity
     c.clist = nullptr;
     c.clist_cap = 0;
@@ -819,11 +841,12 @@ extern "C" dbs_status dbs_spmspv_noalloc(const dbs_matrix *A, dbs_semiring sr, i
     if ((st = noalloc_device(s, &d)) != DBS_OK) return st;
     DevCtx c = noalloc_ctx(*d);
     st = spmspv_launches(A, c, s, mode, sr, x_nnz, d_x_idx, d_x_val, d_mask, complement_mask, path, th3, d_y_idx,
-                         d_y_val, d_y_nnz, [](int, auto &&launch) -> dbs_status {
+                         d_y_val, d_y_nnz, false, [](int, auto &&launch) -> dbs_status {
                              const hipError_t e = launch();
                              return e == hipSuccess ? DBS_OK : hip_fail(e, "kernel launch");
                          });
     d->scan_parity = c.scan_parity;
     d->fin_parity = c.fin_parity;
+    d->gen = c.gen;
     return st;
 }

@@ -57,6 +57,7 @@ __device__ __forceinline__ uint32_t wave_or(uint32_t v)
 namespace dppc {
 constexpr int ROW_SHR = 0x110;    // + n: lane i of a 16-lane row reads lane i - n of the row
 constexpr int ROW_ROR = 0x120;    // + n: rotate right within the row
+constexpr int WF_SL1 = 0x130;     // lane i reads lane i + 1 of the wave
 constexpr int WF_SR1 = 0x138;     // lane i reads lane i - 1 of the wave
 constexpr int ROW_BCAST15 = 0x142;  // lane 15 of each row feeds the next row
 constexpr int ROW_BCAST31 = 0x143;  // lane 31 feeds rows 2 and 3
@@ -92,6 +93,27 @@ __device__ __forceinline__ uint32_t wave_incl_max(uint32_t v)
 }
 // The value of lane i - 1 (0 for lane 0).
 __device__ __forceinline__ uint32_t wave_shr1(uint32_t v) { return dpp_mov<dppc::WF_SR1>(0u, v); }
+
+// OR of v over the lanes up to this one whose key equals this lane's, for
+// keys in contiguous runs (a Hillis-Steele scan that stops at a key change;
+// with a key repeated after a gap it may also merge across the gap).
+__device__ __forceinline__ uint32_t wave_run_or(uint32_t v, uint32_t key)
+{
+#define DBS_RUN_STEP(CTRL, RM)                                       \
+    {                                                                \
+        const uint32_t pv = dpp_mov<CTRL, RM>(0u, v);                \
+        const uint32_t pk = dpp_mov<CTRL, RM>(~key, key);            \
+        if (pk == key) v |= pv;                                      \
+    }
+    DBS_RUN_STEP(dppc::ROW_SHR + 1, 0xF)
+    DBS_RUN_STEP(dppc::ROW_SHR + 2, 0xF)
+    DBS_RUN_STEP(dppc::ROW_SHR + 4, 0xF)
+    DBS_RUN_STEP(dppc::ROW_SHR + 8, 0xF)
+    DBS_RUN_STEP(dppc::ROW_BCAST15, 0xA)
+    DBS_RUN_STEP(dppc::ROW_BCAST31, 0xC)
+#undef DBS_RUN_STEP
+    return v;
+}
 
 __device__ __forceinline__ uint32_t or16_in_quarter(uint32_t v)
 {

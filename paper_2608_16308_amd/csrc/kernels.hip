@@ -36,6 +36,7 @@
 //    are committed to an fp64 accumulator per row: a plain store when the
 //    block row has one segment, a global fp64 atomic otherwise.
 //  * wave scans and row reductions use DPP row shifts and broadcasts.
+#include <algorithm>
 #include <climits>
 
 #include "device_common.hpp"
@@ -419,10 +420,9 @@ __global__ __launch_bounds__(STPB) void k_scan(uint32_t *__restrict__ xmask, con
 // J: push needs only increasing first tasks).  The counters, the path choice
 // and the whole bitmap are then written as k_scan writes them.
 constexpr int SX_TPB = 1024;
-constexpr int SX_PER = SMALL_X_MAX / SX_TPB;   // indices per thread
 constexpr int SX_HASH_LOG = 12;
 constexpr int SX_HASH = 1 << SX_HASH_LOG;      // hash slots: twice the indices
-static_assert(SX_PER * SX_TPB == SMALL_X_MAX && SX_HASH == 2 * SMALL_X_MAX, "small-x tile");
+static_assert(SX_HASH == 2 * SMALL_X_MAX, "small-x hash table");
 
 __device__ __forceinline__ bool sx_insert(uint32_t *tab, uint32_t key)
 {
@@ -437,42 +437,50 @@ __device__ __forceinline__ bool sx_insert(uint32_t *tab, uint32_t key)
     }
 }
 
-template <int MODE>
-__global__ __launch_bounds__(SX_TPB) void k_small_x(const int32_t *__restrict__ xi, const void *__restrict__ xv,
-                                                   int32_t k, int32_t n, void *__restrict__ xd,
-                                                   uint32_t *__restrict__ xmask,
-                                                   const int32_t *__restrict__ cb_ptr, int32_t nbc,
-                                                   int4 *__restrict__ items, uint32_t *__restrict__ xbits,
-                                                   int32_t *__restrict__ counters, int32_t forced_path,
-                                                   double th3, double th3s)
+// The work of one workgroup of NTH threads (SMALL_X_MAX / NTH indices per
+// thread) over LDS scratch s_hash[SX_HASH], s_bits[(nbc + 31) / 32] and
+// lds4[NTH / 64]; ends with every global write issued (not fenced).
+template <int MODE, int NTH>
+__device__ __forceinline__ void small_x_body(const int32_t *__restrict__ xi, const void *__restrict__ xv,
+                                             int32_t k, int32_t n, void *__restrict__ xd,
+                                             uint32_t *__restrict__ xmask, const int32_t *__restrict__ cb_ptr,
+                                             int32_t nbc, int4 *__restrict__ items, uint32_t *__restrict__ xbits,
+                                             int32_t *__restrict__ counters, int32_t forced_path, double th3,
+                                             double th3s, uint32_t *s_hash, uint32_t *s_bits, uint64_t *lds4)
 {
-    __shared__ uint32_t s_hash[SX_HASH];
-    __shared__ uint32_t s_bits[SMALL_X_WORDS];
-    __shared__ uint64_t lds4[SX_TPB / WAVE];
+    constexpr int PER = SMALL_X_MAX / NTH;
+    static_assert(PER * NTH == SMALL_X_MAX, "small-x tile");
     const int t = threadIdx.x;
     const int32_t nwords = (nbc + 31) >> 5;
-    int32_t j[SX_PER];
-    uint32_t v[SX_PER];
+    int32_t j[PER];
+    uint32_t v[PER];
 #pragma unroll
-    for (int e = 0; e < SX_PER; ++e) {
-        const int32_t i = e * SX_TPB + t;
+    for (int e = 0; e < PER; ++e) {
+        const int32_t i = e * NTH + t;
         j[e] = i < k ? xi[i] : -1;
         v[e] = 0;
         if constexpr (MODE == M_F32) v[e] = i < k ? ((const uint32_t *)xv)[i] : 0u;
         if constexpr (MODE == M_F16) v[e] = i < k ? ((const uint16_t *)xv)[i] : 0u;
     }
-    for (int32_t i = t; i < SX_HASH; i += SX_TPB) s_hash[i] = 0xFFFFFFFFu;
-    for (int32_t i = t; i < nwords; i += SX_TPB) s_bits[i] = 0u;
-    __syncthreads();
-    const int lane = lane_id();
+    for (int32_t i = t; i < SX_HASH; i += NTH) s_hash[i] = 0xFFFFFFFFu;
+    for (int32_t i = t; i < nwords; i += NTH) s_bits[i] = 0u;
     uint32_t bad = 0, pop = 0, own = 0;
-    int32_t cs[SX_PER], ce[SX_PER];
+    int32_t cs[PER], ce[PER];
+    uint32_t bits[PER], old[PER];
+    // every memory operation that depends only on the index goes out at
+    // once: the value's scatter, the mask atomic (its old word is used only
+    // for the final counts) and the block-column extent of the index's
+    // vector block (kept by the lane that owns the block below)
 #pragma unroll
-    for (int e = 0; e < SX_PER; ++e) {
-        const int32_t i = e * SX_TPB + t;
+    for (int e = 0; e < PER; ++e) {
+        const int32_t i = e * NTH + t;
         const bool valid = i < k && j[e] >= 0 && j[e] < n;
         if (i < k && !valid) ++bad;
+        if (!valid) j[e] = -1;
         cs[e] = ce[e] = 0;
+        bits[e] = 0u;
+        old[e] = 0xFFFFFFFFu;
+        if (!ballot(i < k)) continue;  // (wave-uniform) no index left for this wave
         // an input equal to the absent-entry marker becomes the canonical NaN
         if (valid) {
             if constexpr (MODE == M_F32) ((uint32_t *)xd)[j[e]] = v[e] == 0xFFFFFFFFu ? 0x7FC00000u : v[e];
@@ -483,40 +491,44 @@ __global__ __launch_bounds__(SX_TPB) void k_small_x(const int32_t *__restrict__ 
         // merged first: one returning atomic per run, whose old word tells
         // which of the run's bits were already stored
         const int32_t w = valid ? j[e] >> 5 : -1;
-        uint32_t bits = valid ? 1u << (j[e] & 31) : 0u;
-#pragma unroll
-        for (int o = 1; o < WAVE; o <<= 1) {
-            const uint32_t vb = (uint32_t)__shfl_up((int)bits, o, WAVE);
-            const int32_t vw = __shfl_up(w, o, WAVE);
-            if (lane >= o && vw == w) bits |= vb;
-        }
-        const int32_t nextw = __shfl_down(w, 1, WAVE);
-        if (w >= 0 && (lane == WAVE - 1 || nextw != w)) pop += __popc(bits & ~atomicOr(&xmask[w], bits));
-        // likewise the vector blocks: the first lane of a run inserts
-        const int32_t J = valid ? j[e] >> 4 : -1;
-        const int32_t prevJ = __shfl_up(J, 1, WAVE);
-        if (valid && (lane == 0 || prevJ != J) && sx_insert(s_hash, (uint32_t)J)) {
-            own |= 1u << e;
+        bits[e] = wave_run_or(valid ? 1u << (j[e] & 31) : 0u, (uint32_t)w);
+        const int32_t nextw = (int32_t)dpp_mov<dppc::WF_SL1>(~(uint32_t)w, (uint32_t)w);
+        const bool last = w >= 0 && nextw != w;
+        if (last) old[e] = atomicOr(&xmask[w], bits[e]);
+        if (valid) {
+            const int32_t J = j[e] >> 4;
             cs[e] = cb_ptr[J];
             ce[e] = cb_ptr[J + 1];
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+        // likewise the vector blocks: the first lane of a run inserts
+        const int32_t J = j[e] >= 0 ? j[e] >> 4 : -1;
+        const int32_t prevJ = (int32_t)dpp_mov<dppc::WF_SR1>(~(uint32_t)J, (uint32_t)J);
+        if (J >= 0 && prevJ != J && sx_insert(s_hash, (uint32_t)J)) {
+            own |= 1u << e;
             atomicOr(&s_bits[J >> 5], 1u << (J & 31));
         }
     }
+#pragma unroll
+    for (int e = 0; e < PER; ++e) pop += __popc(bits[e] & ~old[e]);
     uint64_t mine = 0;
 #pragma unroll
-    for (int e = 0; e < SX_PER; ++e) {
+    for (int e = 0; e < PER; ++e) {
         const uint32_t len = (uint32_t)(ce[e] - cs[e]);
         if (((own >> e) & 1u) && len) mine += (1ull << 34) + len;
     }
     uint64_t total, ctot;
-    const uint64_t excl = block_exclusive_scan<SX_TPB>(mine, &total, lds4);
+    const uint64_t excl = block_exclusive_scan<NTH>(mine, &total, lds4);
     // block totals of (distinct indices, bad indices, distinct vector blocks)
-    block_exclusive_scan<SX_TPB>(((uint64_t)pop << 32) | ((uint64_t)bad << 16) | (uint64_t)__popc(own), &ctot,
+    block_exclusive_scan<NTH>(((uint64_t)pop << 32) | ((uint64_t)bad << 16) | (uint64_t)__popc(own), &ctot,
                                  lds4);
     int64_t idx = (int64_t)(excl >> 34);
     int64_t off = (int64_t)(excl & ((1ull << 34) - 1));
 #pragma unroll
-    for (int e = 0; e < SX_PER; ++e) {
+    for (int e = 0; e < PER; ++e) {
         const int32_t len = ce[e] - cs[e];
         if (((own >> e) & 1u) && len) {
             items[idx] = make_int4((int32_t)off, j[e] >> 4, cs[e] - (int32_t)off, 0);
@@ -525,7 +537,7 @@ __global__ __launch_bounds__(SX_TPB) void k_small_x(const int32_t *__restrict__ 
         }
     }
     // (the scans' barriers have completed the LDS bitmap)
-    for (int32_t i = t; i < nwords; i += SX_TPB) xbits[i] = s_bits[i];
+    for (int32_t i = t; i < nwords; i += NTH) xbits[i] = s_bits[i];
     if (t == 0) {
         const int32_t NT = (int32_t)(total >> 34);
         const int32_t T = (int32_t)(total & ((1ull << 34) - 1));
@@ -545,6 +557,22 @@ __global__ __launch_bounds__(SX_TPB) void k_small_x(const int32_t *__restrict__ 
         }
         counters[C_PATH] = path;
     }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(SX_TPB) void k_small_x(const int32_t *__restrict__ xi, const void *__restrict__ xv,
+                                                   int32_t k, int32_t n, void *__restrict__ xd,
+                                                   uint32_t *__restrict__ xmask,
+                                                   const int32_t *__restrict__ cb_ptr, int32_t nbc,
+                                                   int4 *__restrict__ items, uint32_t *__restrict__ xbits,
+                                                   int32_t *__restrict__ counters, int32_t forced_path,
+                                                   double th3, double th3s)
+{
+    __shared__ uint32_t s_hash[SX_HASH];
+    __shared__ uint32_t s_bits[SMALL_X_WORDS];
+    __shared__ uint64_t lds4[SX_TPB / WAVE];
+    small_x_body<MODE, SX_TPB>(xi, xv, k, n, xd, xmask, cb_ptr, nbc, items, xbits, counters, forced_path, th3, th3s,
+                               s_hash, s_bits, lds4);
 }
 
 // ---------------------------------------------------------------------------
@@ -789,6 +817,7 @@ struct MainArgs {
     int32_t nreg;           // compacted pull: regions (waves of the second kernel's grid)
     int32_t cpw;            // non-COO pass: chunks per workgroup round (1..16)
     int32_t cpm;            // compacted pull below N_nzblk / N_blk = cpm / 1000
+    int32_t atomic_commit;  // 1: every accumulator commit is an atomic (single launch)
 };
 
 // Independent work units per lane and loop iteration: four segments per
@@ -1180,7 +1209,7 @@ __device__ __forceinline__ void row_values(const uint8_t *vals, bool colview, co
 // multiplied with the NB dense x (zeros where a vector has no entry), and
 // the NB sums go to NB accumulator sets (x and accumulators NB-strided).
 template <int MODE, bool LDSBITS, int NB = 1>
-__device__ void pull_rows(const MainArgs &a, uint32_t *L)
+__device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L)
 {
     using Y = RowsLds<MODE, NB>;
     static_assert(NB == 1 || valued<MODE>(), "batched pull is for valued modes");
@@ -1457,7 +1486,7 @@ __device__ void pull_rows(const MainArgs &a, uint32_t *L)
 }
 
 template <int MODE, bool LDSBITS>
-__device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<false> *hs,
+__device__ __forceinline__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<false> *hs,
                           bool spec)
 {
     const int lane = lane_id(), q = lane >> 4, i = lane & 15;
@@ -1566,7 +1595,7 @@ __device__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t 
             } else if (vs[k]) {
                 if ((hq[k] >> i) & 1u) {
                     const int64_t row = (int64_t)R * BS + i;
-                    const bool single = (s[k] >> 31) != 0;
+                    const bool single = (s[k] >> 31) != 0 && !a.atomic_commit;
                     if constexpr (valued<MODE>()) {
                         const float v = my[lane];
                         if (single) a.yacc[row] = (double)v;
@@ -1764,7 +1793,7 @@ __device__ __forceinline__ void wave_search(const int32_t *__restrict__ arr, int
 // its own item by a 6-step binary search over the next 64 item starts, held
 // one per lane and read by shuffles.
 template <int MODE>
-__device__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<true> *hs)
+__device__ __forceinline__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<true> *hs)
 {
     const int lane = lane_id();
     const int32_t T = a.counters[C_TASKS];
@@ -2392,6 +2421,283 @@ __global__ __launch_bounds__(TPB) void k_bfs_finish(int32_t n, int32_t *__restri
 }
 
 // ---------------------------------------------------------------------------
+// single launch for short index lists (Sec. 4.1: blocker, nonzero-block count
+// and path choice inside the SpMSpV launch)
+// ---------------------------------------------------------------------------
+// One kernel runs the whole call for up to SMALL_X_MAX x indices:
+//   1. workgroup 0 runs the blocker and the selector (small_x_body) and then
+//      publishes the call's number in the `ready` words; the other
+//      workgroups wait for it (one writer, many readers);
+//   2. every workgroup takes its share of the chosen traversal (push, or
+//      the non-COO pass plus the segment loop of pull) and then publishes
+//      the call's number in its own `done` word;
+//   3. one wave of workgroup 0 waits until every done word holds it and
+//      publishes it in the `all` words; the first nfin workgroups wait for
+//      those, then compact y (look-back over tiles of FF_WORDS structure
+//      words) and restore the scratch.
+// Device-wide barriers built from contended atomic counters cost 4-30
+// microseconds on this GPU (the atomics on one address are serialized),
+// more than the kernel boundaries they would replace, and so does a done
+// word polled by many workgroups; here every word has one writer, a single
+// wave polls the done words, and the many readers of `ready` and `all`
+// spread over eight copies 4 KB apart.  Only workgroups below nfin ever
+// wait on workgroups that may not have started, so the others always
+// finish and free their slots.  Every wait is bounded: a wait that runs out
+// sets bit 2 of the call's error flags instead of hanging.
+#ifndef FUSED_MAX_GRID
+#define FUSED_MAX_GRID 512
+#endif
+static_assert(FUSED_MAX_GRID <= MAX_MAIN_GRID, "one done word per workgroup");
+constexpr int FF_WORDS = 2 * TPB;       // y-structure words per compaction tile (2 per thread)
+constexpr int FUSED_MAX_FIN = 128;      // compacting workgroups at most
+constexpr uint32_t FUSED_SPIN_MAX = 1u << 22;
+// sync words: copy c (< 8) of `ready` at 1024 c and of `all` at 1024 c + 512;
+// the done word of workgroup g at SYNC_DONE + g
+constexpr int SYNC_COPIES = 8, SYNC_STRIDE = 1024, SYNC_ALL = 512, SYNC_DONE = SYNC_COPIES * SYNC_STRIDE;
+static_assert(SYNC_WORDS == SYNC_DONE + MAX_MAIN_GRID, "single-launch sync words");
+
+struct FusedArgs {
+    const int32_t *x_idx;
+    const void *x_val;
+    int32_t k, n;
+    void *xd;
+    uint32_t *xmask;
+    uint32_t *xbits;
+    int4 *items;
+    const int32_t *cb_ptr;
+    int32_t forced_path;
+    double th3, th3s;
+    int32_t *y_idx;
+    void *y_val;
+    int32_t *y_nnz;
+    uint32_t *sync;
+    uint32_t gen;            // this call's number (never 0)
+    uint64_t *status;        // compaction look-back statuses of this call (zero)
+    uint64_t *next_status;   // the other copy, cleared for the next call
+    int32_t n_status;
+    int32_t nfin;            // compacting workgroups
+    int32_t ntiles;          // compaction tiles
+    int32_t nywords;
+};
+
+// Waits (one lane) until *p == v; false if the bound ran out.
+__device__ __forceinline__ bool fused_wait_one(const uint32_t *p, uint32_t v)
+{
+    for (uint32_t i = 0; i < FUSED_SPIN_MAX; ++i) {
+        if (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == v) return true;
+        __builtin_amdgcn_s_sleep(8);
+    }
+    return false;
+}
+
+// Publishes v in the SYNC_COPIES copies of a word (one lane).
+__device__ __forceinline__ void fused_publish(uint32_t *base, uint32_t v)
+{
+    for (int c = 0; c < SYNC_COPIES; ++c)
+        __hip_atomic_store(&base[c * SYNC_STRIDE], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Waits until every memory operation this wave issued has completed (the
+// fence keeps the compiler from moving them past the wait).
+__device__ __forceinline__ void wave_drain()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_s_waitcnt(0);
+}
+
+// Waits (one wave) until the g words at p all hold v.
+__device__ __forceinline__ bool fused_wait_all(const uint32_t *p, int32_t g, uint32_t v)
+{
+    const int lane = lane_id();
+    for (uint32_t i = 0; i < FUSED_SPIN_MAX; ++i) {
+        bool ok = true;
+        for (int32_t q = lane; q < g; q += WAVE)
+            ok &= __hip_atomic_load(&p[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == v;
+        if (!ballot(!ok)) return true;
+        __builtin_amdgcn_s_sleep(8);
+    }
+    return false;
+}
+
+// One compaction tile of the single launch: thread t owns structure words
+// 2 t and 2 t + 1 of the tile and writes the rows of their set bits in
+// ascending order (the outputs of a short x are sparse, so only set bits
+// are visited).
+template <int MODE>
+__device__ __forceinline__ void fused_finalize_tile(const FusedArgs &f, double *yacc, uint32_t *ybits, int tile, uint64_t *lds4,
+                                    uint64_t *s_prefix)
+{
+    const int t = threadIdx.x;
+    const int32_t w0 = tile * FF_WORDS + 2 * t;
+    uint32_t wd[2];
+    wd[0] = w0 < f.nywords ? __hip_atomic_load(&ybits[w0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+    wd[1] = w0 + 1 < f.nywords ? __hip_atomic_load(&ybits[w0 + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+    uint64_t total;
+    const uint64_t excl = block_exclusive_scan<TPB>((uint64_t)(__popc(wd[0]) + __popc(wd[1])), &total, lds4);
+    if (t < WAVE) {
+        uint64_t prefix = 0;
+        if (tile == 0) {
+            if (t == 0) st_store(&f.status[0], ST_INC | total);
+        } else {
+            if (t == 0) st_store(&f.status[tile], ST_AGG | total);
+            prefix = lookback(f.status, tile);
+            if (t == 0) st_store(&f.status[tile], ST_INC | (prefix + total));
+        }
+        if (t == 0) *s_prefix = prefix;
+    }
+    __syncthreads();
+    const int64_t prefix = (int64_t)*s_prefix;
+    int64_t pos = prefix + (int64_t)excl;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        uint32_t w = wd[h];
+        if (!w) continue;
+        ybits[w0 + h] = 0u;
+        const int64_t row0 = (int64_t)(w0 + h) * 32;
+        while (w) {
+            // up to four rows at a time: their accumulator loads go out together
+            int64_t r[4];
+            double v[4];
+            int cnt = 0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                r[u] = row0 + ctz32(w);
+                v[u] = 0.0;
+                if (w) {
+                    if constexpr (valued<MODE>())
+                        v[u] = __hip_atomic_load(&yacc[r[u]], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    w &= w - 1u;
+                    cnt = u + 1;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (u >= cnt) break;
+                f.y_idx[pos] = (int32_t)r[u];
+                if constexpr (MODE == M_F32) ((float *)f.y_val)[pos] = (float)v[u];
+                if constexpr (MODE == M_F16) ((uint16_t *)f.y_val)[pos] = f64_to_f16_rne(v[u]);
+                if constexpr (valued<MODE>()) yacc[r[u]] = 0.0;
+                ++pos;
+            }
+        }
+    }
+    if (tile == f.ntiles - 1 && t == 0) {
+        const int32_t tot = (int32_t)(prefix + (int64_t)total);
+        *f.y_nnz = tot;
+    }
+    __syncthreads();  // *s_prefix is read again by the next tile
+}
+
+// LDS of the single-launch kernel: the traversal's (either path) or the
+// blocker's hash table, whichever is larger.
+template <int MODE>
+constexpr size_t fused_lds_bytes()
+{
+    const size_t a = traverse_lds_bytes<MODE, PATH_PUSH>(), b = traverse_lds_bytes<MODE, PATH_PULL>();
+    const size_t c = (size_t)SX_HASH * sizeof(uint32_t);
+    const size_t ab = a > b ? a : b;
+    return ab > c ? ab : c;
+}
+
+template <int MODE>
+__global__ __launch_bounds__(TPB, 3) void k_fused(MainArgs a, FusedArgs f)
+{
+    __shared__ __align__(16) uint8_t lds_raw[fused_lds_bytes<MODE>()];
+    __shared__ uint64_t lds4[TPB / WAVE];
+    __shared__ uint64_t s_prefix;
+    const int t = threadIdx.x;
+    const int copy = (blockIdx.x % SYNC_COPIES) * SYNC_STRIDE;
+    uint32_t *ready = f.sync, *all = f.sync + SYNC_ALL, *done = f.sync + SYNC_DONE;
+    // 1. blocker and selector (workgroup 0); the others wait for them.
+    // Workgroup 0's plain stores reach memory by one release (an L2
+    // write-back); the waiting workgroups read nothing of them before the
+    // ready word, and the caches held none of these lines at the launch.
+    if (blockIdx.x == 0) {
+        small_x_body<MODE, TPB>(f.x_idx, f.x_val, f.k, f.n, f.xd, f.xmask, f.cb_ptr, a.nbc, f.items, f.xbits,
+                                a.counters, f.forced_path, f.th3, f.th3s, (uint32_t *)lds_raw, lds_bits, lds4);
+        wave_drain();
+        __syncthreads();
+        if (t == 0) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            fused_publish(ready, f.gen);
+        }
+    } else {
+        if (t == 0 && !fused_wait_one(ready + copy, f.gen)) atomicOr(&a.counters[C_SYNCERR], 1);
+        __syncthreads();
+    }
+    // 2. traversal
+    const int32_t N = __hip_atomic_load(&a.counters[C_NZBLK], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int32_t path = __hip_atomic_load(&a.counters[C_PATH], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int w = t >> 6, lane = lane_id();
+    const int gw = blockIdx.x * (TPB / WAVE) + w, nw = gridDim.x * (TPB / WAVE);
+    if (N > 0) {
+        if (path == PATH_PUSH) {
+            WaveLds<true> &L = ((WaveLds<true> *)lds_raw)[w];
+#pragma unroll
+            for (int q = 0; q < SLOTS; ++q) L.acc[q * WAVE + lane] = 0u;
+            wave_lds_sync();
+            push_loop<MODE>(a, gw, nw, (float *)L.acc, (int32_t *)L.acc, &L.hs);
+        } else {
+            const bool spec = (int64_t)N * 8 >= (int64_t)a.nbc;
+            const int32_t nwords = (a.nbc + 31) >> 5;
+            for (int32_t i = t; i < nwords; i += TPB) lds_bits[i] = a.xbits[i];
+            __syncthreads();
+            pull_rows<MODE, true>(a, (uint32_t *)lds_raw);
+            WaveLds<false> &L = ((WaveLds<false> *)lds_raw)[w];
+#pragma unroll
+            for (int q = 0; q < SLOTS; ++q) L.acc[q * WAVE + lane] = 0u;
+            wave_lds_sync();
+            pull_loop<MODE, true>(a, gw, nw, (float *)L.acc, (int32_t *)L.acc, &L.hs, spec);
+        }
+    }
+    // 3. completion.  The traversal's results are device-scope atomics
+    // (a.atomic_commit), complete once the wave's memory counter drains, so
+    // a done word needs no cache write-back; the compaction reads them with
+    // device-coherent loads.
+    wave_drain();
+    __syncthreads();
+    if (t == 0) __hip_atomic_store(&done[blockIdx.x], f.gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((int)blockIdx.x >= f.nfin) return;
+    if (blockIdx.x == 0) {
+        if (t < WAVE) {
+            const bool ok = fused_wait_all(done, (int32_t)gridDim.x, f.gen);
+            if (t == 0) {
+                if (!ok) atomicOr(&a.counters[C_SYNCERR], 1);
+                fused_publish(all, f.gen);
+            }
+        }
+    } else if (t == 0 && !fused_wait_one(all + copy, f.gen)) {
+        atomicOr(&a.counters[C_SYNCERR], 1);
+    }
+    __syncthreads();
+    const int32_t gstride = f.nfin * TPB;
+    for (int32_t i = blockIdx.x * TPB + t; i < f.n_status; i += gstride) f.next_status[i] = 0;
+    // clear the blk_x_mask words of this call's x indices and put the
+    // absent-entry marker back into the densified x
+    for (int32_t q = blockIdx.x * TPB + t; q < f.k; q += gstride) {
+        const int32_t j = f.x_idx[q];
+        if (j >= 0 && j < f.n) {
+            f.xmask[j >> 5] = 0u;
+            if constexpr (MODE == M_F32) ((uint32_t *)f.xd)[j] = 0xFFFFFFFFu;
+            if constexpr (MODE == M_F16) ((uint16_t *)f.xd)[j] = (uint16_t)0xFFFFu;
+        }
+    }
+    for (int tile = blockIdx.x; tile < f.ntiles; tile += f.nfin)
+        fused_finalize_tile<MODE>(f, a.yacc, a.ybits, tile, lds4, &s_prefix);
+    if ((int)blockIdx.x == (f.ntiles - 1) % f.nfin && t == 0) {
+        // the workgroup of the last tile: the call's counters and error flags
+        const int32_t tot = *f.y_nnz;
+        a.counters[C_YNNZ] = tot;
+        const int32_t bad = a.counters[C_XBAD], pop = a.counters[C_XPOP];
+        const int32_t serr = __hip_atomic_load(&a.counters[C_SYNCERR], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        a.counters[C_ERR_LAST] = (bad ? 1 : 0) | (pop < f.k - bad ? 2 : 0) | (serr ? 4 : 0);
+        a.counters[C_XBAD] = 0;
+        a.counters[C_XPOP] = 0;
+        a.counters[C_SYNCERR] = 0;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // host launch wrappers
 // ---------------------------------------------------------------------------
 static inline int grid_for(int64_t items, int per_block, int cap)
@@ -2607,6 +2913,7 @@ static void fill_main_args(const DevMatrix &A, const DevCtx &C, int mode, const 
     a.nreg = 0;
     a.cpw = TPB / 16;
     a.cpm = 0;
+    a.atomic_commit = 0;
 }
 
 int64_t compact_list_entries(int64_t nseg) { return (nseg + 4 * MAX_MAIN_GRID) * 16; }
@@ -2624,6 +2931,90 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
     case M_BOOL: return launch_paths<M_BOOL>(A, a, forced_path, s);
     default: return launch_paths<M_BFS>(A, a, forced_path, s);
     }
+}
+
+bool fused_fits(const DevMatrix &A, int32_t k)
+{
+    return small_x_fits(A, k) && ((int64_t)A.nbc + 31) / 32 <= LDS_BITMAP_WORDS;
+}
+
+// Resident workgroups of the single-launch kernel (one round of residency).
+template <int MODE>
+static int fused_grid(size_t dyn_lds)
+{
+    static size_t cached_lds[8];
+    static int cached_grid[8];
+    static int ncached = 0;
+    for (int i = 0; i < ncached; ++i)
+        if (cached_lds[i] == dyn_lds) return cached_grid[i];
+    int dev = 0, cus = 0, per_cu = 0, grid = 256;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_fused<MODE>, TPB, dyn_lds) == hipSuccess &&
+        cus > 0 && per_cu > 0)
+        grid = cus * per_cu;
+    if (grid > FUSED_MAX_GRID) grid = FUSED_MAX_GRID;
+    if (ncached < 8) {
+        cached_lds[ncached] = dyn_lds;
+        cached_grid[ncached] = grid;
+        ++ncached;
+    }
+    return grid;
+}
+
+hipError_t launch_fused(const DevMatrix &A, DevCtx &C, int mode, int32_t k, const int32_t *x_idx,
+                        const void *x_val, const uint32_t *omask, int complement, int forced_path, double th3,
+                        double th3s, int32_t *y_idx, void *y_val, int32_t *y_nnz, hipStream_t s)
+{
+    if (!fused_fits(A, k) || !C.sync || mode == M_BFS) return hipErrorInvalidValue;
+    MainArgs a;
+    fill_main_args(A, C, mode, C.xd, omask, complement, nullptr, a);
+    a.clist = nullptr;  // the segment loop at every activity
+    a.atomic_commit = 1;
+    FusedArgs f;
+    f.x_idx = x_idx;
+    f.x_val = x_val;
+    f.k = k;
+    f.n = A.n;
+    f.xd = C.xd;
+    f.xmask = C.xmask;
+    f.xbits = C.xbits;
+    f.items = C.items;
+    f.cb_ptr = A.cb_ptr;
+    f.forced_path = forced_path;
+    f.th3 = th3;
+    f.th3s = th3s;
+    f.y_idx = y_idx;
+    f.y_val = y_val;
+    f.y_nnz = y_nnz;
+    f.sync = C.sync;
+    if (++C.gen == 0) C.gen = 1;
+    f.gen = C.gen;
+    const int p = C.fin_parity;
+    f.status = C.st_fin[p];
+    f.next_status = C.st_fin[1 - p];
+    f.n_status = C.n_st_fin;
+    f.nywords = (A.nbr + 1) / 2;
+    f.ntiles = (f.nywords + FF_WORDS - 1) / FF_WORDS;
+    if (f.ntiles < 1) f.ntiles = 1;
+    const int32_t nwords = (A.nbc + 31) >> 5;
+    const size_t dyn = (size_t)(nwords > 0 ? nwords : 1) * 4;
+    int grid = 256;
+    switch (mode) {
+    case M_F32: grid = fused_grid<M_F32>(dyn); break;
+    case M_F16: grid = fused_grid<M_F16>(dyn); break;
+    default: grid = fused_grid<M_BOOL>(dyn); break;
+    }
+    f.nfin = std::min(std::min(grid, f.ntiles), FUSED_MAX_FIN);
+    if (f.ntiles + 1 > f.n_status) return hipErrorInvalidValue;
+    switch (mode) {
+    case M_F32: hipLaunchKernelGGL(k_fused<M_F32>, dim3(grid), dim3(TPB), dyn, s, a, f); break;
+    case M_F16: hipLaunchKernelGGL(k_fused<M_F16>, dim3(grid), dim3(TPB), dyn, s, a, f); break;
+    default: hipLaunchKernelGGL(k_fused<M_BOOL>, dim3(grid), dim3(TPB), dyn, s, a, f); break;
+    }
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) C.fin_parity = 1 - p;
+    return e;
 }
 
 int32_t scan_tiles(int32_t nbc) { return (nbc + SCAN_TILE - 1) / SCAN_TILE; }

@@ -49,6 +49,7 @@ enum Counter : int {
     C_NZACC = 7,     // nonzero vector blocks, summed by the scan tiles (consumed by its last tile)
     C_NTB = 8,       // push work items (nonzero vector blocks with a nonempty block column)
     C_XPOP = 9,      // distinct x indices (mask popcounts), summed by the scan tiles
+    C_SYNCERR = 10,  // single launch: a bounded wait for other workgroups ran out
     C_COUNT = 12
 };
 constexpr int PATH_PUSH = 1, PATH_PULL = 2;
@@ -102,7 +103,14 @@ struct DevCtx {
     int32_t *clist = nullptr;
     int64_t clist_cap = 0;
     uint32_t *ccount = nullptr;
+    // Single launch (short index lists): ready / all-done words (eight
+    // copies) and one done word per workgroup (SYNC_WORDS in all), and the
+    // number of the last such call (the words hold it once written; 0 is
+    // never used).
+    uint32_t *sync = nullptr;
+    uint32_t gen = 0;
 };
+constexpr int32_t SYNC_WORDS = 8 * 1024 + 4096;
 // Entries and regions of the compacted pull's list for a matrix of nseg
 // pull segments.
 int64_t compact_list_entries(int64_t nseg);
@@ -125,6 +133,13 @@ constexpr int32_t SMALL_X_WORDS = 8192;
 bool small_x_fits(const DevMatrix &A, int32_t k);
 hipError_t launch_small_x(const DevMatrix &A, const DevCtx &C, int mode, int32_t k, const int32_t *x_idx,
                           const void *x_val, int forced_path, double th3, double th3s, hipStream_t s);
+// Blocker, selector, traversal and compaction of y in one launch, for an
+// index list small_x_fits accepts whose activity bitmap also fits the pull
+// kernel's LDS copy (fused_fits); valued and OR-AND modes.
+bool fused_fits(const DevMatrix &A, int32_t k);
+hipError_t launch_fused(const DevMatrix &A, DevCtx &C, int mode, int32_t k, const int32_t *x_idx,
+                        const void *x_val, const uint32_t *omask, int complement, int forced_path, double th3,
+                        double th3s, int32_t *y_idx, void *y_val, int32_t *y_nnz, hipStream_t s);
 // Dense activation with n a multiple of 16 and a 16-byte aligned x: the
 // blocker runs inside the scan (one launch fewer).
 bool scan_takes_dense(const DevMatrix &A, const void *x_dense);
