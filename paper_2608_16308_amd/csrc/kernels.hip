@@ -1919,6 +1919,13 @@ __device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rca
     const uint32_t cnt = a.ccount[gw];
     const int32_t *list = a.clist + (int64_t)gw * rcap;
     constexpr int IM = inline_max<MODE>();
+    // spread x (fewer than 4 indices per nonzero vector block on average):
+    // a stored COO block's entries are tested against its vector block's
+    // mask before x is gathered (the mask words are L2-resident, and most
+    // entries then miss); the mask gathers go out with the inline blocks' x
+    // gathers and are waited for only once the records' loads are in flight
+    constexpr bool MXV = valued<MODE>();
+    const bool mxf = MXV && (int64_t)a.counters[C_XPOP] < 4 * (int64_t)a.counters[C_NZBLK];
     for (uint32_t base = 0; base < cnt;) {
         bool v[SLOTS];
         int32_t slot[SLOTS];
@@ -1968,7 +1975,7 @@ __device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rca
         }
         const uint32_t nruns = nr < (uint32_t)RUN_CAP ? nr : (uint32_t)RUN_CAP;
         uint32_t xr[SLOTS][IM];
-        uint32_t cnf[SLOTS];
+        uint32_t cnf[SLOTS], mxg[SLOTS];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
             const bool inl = act[k] && desc_inline(d[k]);
@@ -1980,9 +1987,18 @@ __device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rca
                                : 0u;
             const bool flat = act[k] && flat_coo(d[k]);
             cnf[k] = flat ? nnz : 0u;
-            if (flat) L.hs.stage(k * WAVE + lane, d[k], J[k], 0u, am[k], (int32_t)run[k]);
+            mxg[k] = (MXV && flat && mxf) ? a.xmask[J[k] >> 1] : 0u;
+            if (flat) L.hs.stage(k * WAVE + lane, d[k], J[k], MXV ? 0xFFFFu : 0u, am[k], (int32_t)run[k]);
         }
         auto inline_products = [&]() {
+            if constexpr (MXV) {
+                if (mxf) {
+#pragma unroll
+                    for (int k = 0; k < SLOTS; ++k)
+                        if (cnf[k]) L.hs.mxam[k * WAVE + lane] = ((mxg[k] >> ((J[k] & 1) * 16)) & 0xFFFFu) | (am[k] << 16);
+                    wave_lds_sync();
+                }
+            }
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k) {
                 if (act[k] && desc_inline(d[k])) {
@@ -1994,7 +2010,7 @@ __device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rca
         };
         if (ballot(cnf[0] | cnf[1] | cnf[2] | cnf[3])) {
             wave_lds_sync();
-            flat_pass<MODE, true, false, false, true>(a, &L.hs, cnf, d, sy, sp, inline_products);
+            flat_pass<MODE, true, MXV, false, true>(a, &L.hs, cnf, d, sy, sp, inline_products);
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k) {
                 const uint32_t h = cnf[k] ? L.hs.hitw[k * WAVE + lane] : 0u;
