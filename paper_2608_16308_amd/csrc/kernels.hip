@@ -2070,15 +2070,15 @@ constexpr size_t traverse_lds_bytes()
 //   push kernel: push, or the compacted pull's walk of the regions -- one
 //                launch for the two, so that an automatic path choice costs
 //                two traversal launches, not four.
-// Pull is held to 96 registers (five waves per SIMD; a few spill), which
-// measured faster than four waves without spills; push keeps its registers.
-// In the Boolean modes the compaction inside the pull kernel pushes its
-// arrays out to scratch memory under that limit, so there k_pull_compact
-// always takes it.
+// Pull is held to 128 registers (four waves per SIMD, no spills: measured
+// faster than five waves with 96 registers and a few spills); push keeps its
+// registers.  In the Boolean modes k_pull_compact always takes the
+// compaction (inside the pull kernel it pushed the BFS kernel's arrays out
+// to scratch memory under the earlier 96-register limit).
 template <int MODE> constexpr bool pull_takes_compaction() { return valued<MODE>(); }
 
 template <int MODE, int PATH>
-__global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 5 : 1) void k_traverse(MainArgs a)
+__global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(MainArgs a)
 {
     __shared__ __align__(16) uint8_t lds_raw[traverse_lds_bytes<MODE, PATH>()];
     WaveLds<PATH == PATH_PUSH> *lds = (WaveLds<PATH == PATH_PUSH> *)lds_raw;
