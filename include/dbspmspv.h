@@ -233,7 +233,7 @@ typedef struct {
  * entry held inline, bits 29..26 then that entry's local column; -1 for
  * padding and the sign bit set for a block of the non-COO list) and
  * descriptors,
- * segment words (block row | 1 << 31 for a plain-store row), the block-CSC
+ * segment words (the block row of each segment), the block-CSC
  * pointer, rows and descriptors, the non-COO list's block columns,
  * descriptors, chunk starts and chunk block rows, and the payload.         */
 typedef struct {

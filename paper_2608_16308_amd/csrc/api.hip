@@ -206,7 +206,6 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
         for (int64_t s = 0; s < h->nseg; ++s) {
             const uint64_t sg = h->seg[s];
             const uint32_t first = seg_first(sg), nb = seg_nb(sg);
-            bool heavy = false;
             for (uint32_t i = 0; i < nb; ++i) {
                 const size_t slot = (size_t)16 * s + i;
                 const uint64_t dd = h->desc[first + i];
@@ -224,12 +223,9 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
                     }
                     hv_col.push_back(h->cb_col[first + i]);
                     hv_desc.push_back(dd);
-                    heavy = true;
                 }
             }
-            // a row block with a listed block gets contributions from two
-            // places: its segments commit with atomics then
-            seg_rs[s] = seg_brow(sg) | (seg_single(sg) && !heavy ? 0x80000000u : 0u);
+            seg_rs[s] = seg_brow(sg);
         }
         hv_cstart.push_back((int32_t)hv_col.size());
         csc_desc.resize((size_t)h->nblk);

@@ -312,18 +312,16 @@ __global__ __launch_bounds__(CTPB) void k_conv_write(const void *w, int64_t ld, 
     }
 }
 
-// A thread per block row: its segment words (block row | plain-store flag
-// when the row has one segment and no non-COO block) and non-COO chunks (at
-// most HV_CHUNK consecutive blocks of the row each).
+// A thread per block row: its segment words (the block row) and non-COO
+// chunks (at most HV_CHUNK consecutive blocks of the row each).
 __global__ __launch_bounds__(CTPB) void k_conv_segs(int32_t nbr, const int64_t *pre, uint32_t *seg_rs,
                                                     int32_t *hv_cstart, int32_t *hv_crow)
 {
     const int32_t R = (int32_t)(blockIdx.x * CTPB + threadIdx.x);
     if (R >= nbr) return;
     const int64_t *P = pre + (int64_t)R * PRE, *Q = P + PRE;
-    const int64_t nseg = Q[2] - P[2], heavy = Q[3] - P[3], nch = Q[4] - P[4];
-    const uint32_t flag = (nseg == 1 && heavy == 0) ? 0x80000000u : 0u;
-    for (int64_t s = 0; s < nseg; ++s) seg_rs[P[2] + s] = (uint32_t)R | flag;
+    const int64_t nseg = Q[2] - P[2], nch = Q[4] - P[4];
+    for (int64_t s = 0; s < nseg; ++s) seg_rs[P[2] + s] = (uint32_t)R;
     for (int64_t c = 0; c < nch; ++c) {
         hv_cstart[P[4] + c] = (int32_t)(P[3] + c * HV_CHUNK);
         hv_crow[P[4] + c] = R;

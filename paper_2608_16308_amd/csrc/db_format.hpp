@@ -11,7 +11,7 @@
 //   bits 31..0   first block (primary id)
 //   bits 58..32  block row
 //   bits 62..59  number of blocks - 1 (a segment holds at most 16 blocks)
-//   bit  63      the block row has exactly one segment (plain-store commit)
+//   bit  63      the block row has exactly one segment
 #pragma once
 #include <cstdint>
 

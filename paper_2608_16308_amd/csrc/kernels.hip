@@ -787,7 +787,7 @@ __device__ __forceinline__ uint32_t xd_raw(const void *xd, int64_t j)
 struct MainArgs {
     const int32_t *sl_col;   // pull-segment slots: block column (-1 padding, sign bit: listed)
     const uint64_t *sl_desc; // pull-segment slots: descriptor
-    const uint32_t *seg_rs;  // per segment: block row | single-segment flag << 31
+    const uint32_t *seg_rs;  // per segment: its block row
     const uint8_t *pay;
     uint32_t vb;            // value bytes of the matrix (4, 2 or 0)
     int32_t nbc;
@@ -817,7 +817,6 @@ struct MainArgs {
     int32_t nreg;           // compacted pull: regions (waves of the second kernel's grid)
     int32_t cpw;            // non-COO pass: chunks per workgroup round (1..16)
     int32_t cpm;            // compacted pull below N_nzblk / N_blk = cpm / 1000
-    int32_t atomic_commit;  // 1: every accumulator commit is an atomic (single launch)
 };
 
 // Independent work units per lane and loop iteration: four segments per
@@ -1485,134 +1484,174 @@ __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L)
     }
 }
 
+// Segment loop tasks.  An iteration of a wave takes 4 spq consecutive
+// segments, spq per quarter (SLOTS when there is enough work to keep every
+// wave busy with that many, else 1), so that the wave reads one contiguous
+// stretch of slots; a wave task is G consecutive iterations' worth, tasks
+// dealt out grid-stride.  Each quarter follows the block row of its segments
+// through the task and folds the segments of one row in registers, so that a
+// row is committed (fp64 atomics: other quarters, tasks and the non-COO pass
+// add to the same rows) once per quarter and stretch of the task it covers.
+// G is at most PULL_TASK_ITERS and leaves every wave about
+// PULL_TASKS_PER_WAVE tasks: longer tasks fold more but balance the waves
+// worse (R-MAT workloads concentrate their heavy segments in a few block
+// rows).  The Boolean modes keep G = 1: a BFS level commits few rows, and
+// longer tasks only unbalanced its levels.
+#ifndef PULL_TASK_ITERS
+#define PULL_TASK_ITERS 2
+#endif
+#ifndef PULL_TASKS_PER_WAVE
+#define PULL_TASKS_PER_WAVE 4
+#endif
+
 template <int MODE, bool LDSBITS>
 __device__ __forceinline__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<false> *hs,
                           bool spec)
 {
     const int lane = lane_id(), q = lane >> 4, i = lane & 15;
     constexpr int IM = inline_max<MODE>();
-    // segments per quarter and iteration: SLOTS when there is enough work to
-    // keep every wave busy with SLOTS of them, else 1
-    const int spq = a.nseg >= (int64_t)nw * 4 * SLOTS * 2 ? SLOTS : 1;
-    const int64_t groups = (a.nseg + 4 * spq - 1) / (4 * spq);
-    for (int64_t u = gw; u < groups; u += nw) {
-        uint32_t s[SLOTS];
-        uint64_t d[SLOTS];
-        bool vs[SLOTS], act[SLOTS];
-        int32_t b[SLOTS], J[SLOTS];
-        uint32_t am[SLOTS], mx[SLOTS];
-        // segment word, block column and (spec) descriptor: independent
-        // loads, non-temporal (each slot is read once per call), so that the
-        // stream does not push x out of the L2
-#pragma unroll
-        for (int k = 0; k < SLOTS; ++k) {
-            const int64_t sid = u * 4 * spq + q * spq + k;
-            vs[k] = k < spq && sid < a.nseg;
-            s[k] = vs[k] ? __builtin_nontemporal_load(&a.seg_rs[sid]) : 0u;
-            b[k] = (int32_t)(sid * 16 + i);
-            const int32_t w = vs[k] ? __builtin_nontemporal_load(&a.sl_col[b[k]]) : SLOT_PAD;
-            J[k] = w >= 0 ? slot_col(w) : -1;
-            d[k] = (vs[k] && spec) ? __builtin_nontemporal_load(&a.sl_desc[b[k]]) : 0ull;
-        }
-        // block activity: the LDS bitmap when it fits, else the vector-block
-        // mask (gathered here then, and kept for the whole-wave blocks)
-#pragma unroll
-        for (int k = 0; k < SLOTS; ++k) {
-            am[k] = vs[k] ? row_admit(a, (int32_t)(s[k] & 0x7FFFFFFFu)) : 0u;
-            act[k] = J[k] >= 0 && am[k] != 0;
-            if constexpr (LDSBITS) act[k] = act[k] && block_active(J[k]);
-        }
-        if constexpr (!LDSBITS) {
-#pragma unroll
-            for (int k = 0; k < SLOTS; ++k) {
-                mx[k] = act[k] ? mask16(a.xmask, J[k]) : 0u;
-                act[k] = act[k] && mx[k] != 0;
+    // (segment ids fit 32 bits: the upload keeps 16 nseg below 2^31)
+    const int32_t nseg = (int32_t)a.nseg;
+    const int32_t spq = nseg >= nw * 4 * SLOTS * 2 ? SLOTS : 1, W = 4 * spq;
+    int32_t G = nseg / (nw * W * PULL_TASKS_PER_WAVE);
+    constexpr int32_t GMAX = valued<MODE>() ? PULL_TASK_ITERS : 1;
+    G = G < 1 ? 1 : (G > GMAX ? GMAX : G);
+    const int32_t ntask = (nseg + G * W - 1) / (G * W);
+    for (int32_t task = gw; task < ntask; task += nw) {
+        const int32_t ts = task * G * W + q * spq;
+        // the open run of the quarter: its block row, lane i's share of row
+        // i (fp64 across segments) and the rows hit
+        int32_t Rc = -1;
+        double racc = 0.0;
+        int32_t pacc = INT_MAX;
+        uint32_t hc = 0;
+        auto commit = [&]() {
+            if (Rc < 0) return;
+            if ((hc >> i) & 1u) {
+                const int64_t row = (int64_t)Rc * BS + i;
+                if constexpr (valued<MODE>()) atomicAdd(&a.yacc[row], racc);
+                if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], pacc);
             }
-        }
-        if (!spec) {
-#pragma unroll
-            for (int k = 0; k < SLOTS; ++k) d[k] = act[k] ? __builtin_nontemporal_load(&a.sl_desc[b[k]]) : 0ull;
-        }
-        // nothing to multiply anywhere in the wave: the LDS rows are untouched
-        if (!ballot(act[0] || act[1] || act[2] || act[3])) continue;
-        // Issue every gather that depends only on the descriptors at once:
-        // x of the entries of the inline COO blocks (one lane each) and (in
-        // flat_pass) the records of the stored COO blocks; the inline products
-        // are formed while the record loads are in flight.  Blocks of the
-        // other formats are not in the slots' work (negative block column):
-        // pull_rows takes them.
-        uint32_t hit[SLOTS], cnt[SLOTS];
-        uint32_t xr[SLOTS][IM];
-#pragma unroll
-        for (int k = 0; k < SLOTS; ++k) {
-            const bool inl = act[k] && desc_inline(d[k]);
-            const uint32_t nnz = desc_nnz(d[k]);
-            if constexpr (!LDSBITS && !valued<MODE>()) {
-                // the vector-block mask is already here: it is the x word
-                xr[k][0] = mx[k] << ((J[k] & 1) * 16);
-            } else {
-#pragma unroll
-                for (int e = 0; e < IM; ++e)
-                    xr[k][e] = (inl && (uint32_t)e < nnz) ? x_gather<MODE>(a, J[k], inline_cd(d[k], e, a.vb) & 15u)
-                                                          : 0u;
-            }
-            const bool flat = act[k] && flat_coo(d[k]);
-            cnt[k] = flat ? nnz : 0u;
-            if (flat) hs->stage(k * WAVE + lane, d[k], J[k], LDSBITS ? 0u : mx[k], am[k], 0);
-        }
-        auto inline_products = [&]() {
-#pragma unroll
-            for (int k = 0; k < SLOTS; ++k) {
-                hit[k] = 0;
-                if (act[k] && desc_inline(d[k]))
-                    hit[k] = inline_block<MODE>(a, d[k], J[k], am[k], xr[k], sy + k * WAVE + q * 16,
-                                                sp + k * WAVE + q * 16);
-            }
+            if (i == 0 && hc) or_mask16(a.ybits, Rc, hc);
         };
-        if (ballot(cnt[0] | cnt[1] | cnt[2] | cnt[3])) {
-            wave_lds_sync();
-            flat_pass<MODE, false, !LDSBITS, false, false>(a, hs, cnt, d, sy, sp, inline_products);
+        for (int32_t it = 0; it < G; ++it) {
+            uint32_t s[SLOTS];
+            uint64_t d[SLOTS];
+            bool vs[SLOTS], act[SLOTS];
+            int32_t b[SLOTS], J[SLOTS];
+            uint32_t am[SLOTS], mx[SLOTS];
+            // segment word, block column and (spec) descriptor: independent
+            // loads, non-temporal (each slot is read once per call), so that
+            // the stream does not push x out of the L2
 #pragma unroll
-            for (int k = 0; k < SLOTS; ++k) hit[k] |= hs->hitw[k * 4 + q];
-        } else {
-            inline_products();
-        }
-        wave_lds_sync();
-        uint32_t hq[SLOTS];
+            for (int k = 0; k < SLOTS; ++k) {
+                const int32_t sid = ts + it * W + k;
+                vs[k] = k < spq && sid < nseg;
+                s[k] = vs[k] ? __builtin_nontemporal_load(&a.seg_rs[sid]) : 0u;
+                b[k] = sid * 16 + i;
+                const int32_t w = vs[k] ? __builtin_nontemporal_load(&a.sl_col[b[k]]) : SLOT_PAD;
+                J[k] = w >= 0 ? slot_col(w) : -1;
+                d[k] = (vs[k] && spec) ? __builtin_nontemporal_load(&a.sl_desc[b[k]]) : 0ull;
+            }
+            // block activity: the LDS bitmap when it fits, else the
+            // vector-block mask (gathered here then, and kept for the
+            // whole-wave blocks)
 #pragma unroll
-        for (int k = 0; k < SLOTS; ++k) hq[k] = or16_in_quarter(hit[k]);
+            for (int k = 0; k < SLOTS; ++k) {
+                am[k] = vs[k] ? row_admit(a, (int32_t)s[k]) : 0u;
+                act[k] = J[k] >= 0 && am[k] != 0;
+                if constexpr (LDSBITS) act[k] = act[k] && block_active(J[k]);
+            }
+            if constexpr (!LDSBITS) {
 #pragma unroll
-        for (int k = 0; k < SLOTS; ++k) {
-            const int32_t R = (int32_t)(s[k] & 0x7FFFFFFFu);
-            const float *my = sy + k * WAVE;
-            bool carry = false;
-            if (k + 1 < SLOTS) carry = vs[k] && vs[k + 1] && (int32_t)(s[k + 1] & 0x7FFFFFFFu) == R;
-            if (carry) {
-                // the next slot continues this block row: fold the partial sums into it
-                if constexpr (valued<MODE>()) sy[(k + 1) * WAVE + lane] += my[lane];
-                if constexpr (MODE == M_BFS) sp[(k + 1) * WAVE + lane] = min(sp[(k + 1) * WAVE + lane], sp[k * WAVE + lane]);
-                if (k + 1 < SLOTS) hq[k + 1] |= hq[k];
-            } else if (vs[k]) {
-                if ((hq[k] >> i) & 1u) {
-                    const int64_t row = (int64_t)R * BS + i;
-                    const bool single = (s[k] >> 31) != 0 && !a.atomic_commit;
-                    if constexpr (valued<MODE>()) {
-                        const float v = my[lane];
-                        if (single) a.yacc[row] = (double)v;
-                        else atomicAdd(&a.yacc[row], (double)v);
+                for (int k = 0; k < SLOTS; ++k) {
+                    mx[k] = act[k] ? mask16(a.xmask, J[k]) : 0u;
+                    act[k] = act[k] && mx[k] != 0;
+                }
+            }
+            if (!spec) {
+#pragma unroll
+                for (int k = 0; k < SLOTS; ++k) d[k] = act[k] ? __builtin_nontemporal_load(&a.sl_desc[b[k]]) : 0ull;
+            }
+            // with nothing to multiply anywhere in the wave the LDS rows stay
+            // untouched; the runs are still followed
+            const bool any = ballot(act[0] || act[1] || act[2] || act[3]) != 0;
+            uint32_t hq[SLOTS];
+            if (any) {
+                // Issue every gather that depends only on the descriptors at
+                // once: x of the entries of the inline COO blocks (one lane
+                // each) and (in flat_pass) the records of the stored COO
+                // blocks; the inline products are formed while the record
+                // loads are in flight.  Blocks of the other formats are not in
+                // the slots' work (negative block column): pull_rows takes them.
+                uint32_t hit[SLOTS], cnt[SLOTS];
+                uint32_t xr[SLOTS][IM];
+#pragma unroll
+                for (int k = 0; k < SLOTS; ++k) {
+                    const bool inl = act[k] && desc_inline(d[k]);
+                    const uint32_t nnz = desc_nnz(d[k]);
+                    if constexpr (!LDSBITS && !valued<MODE>()) {
+                        // the vector-block mask is already here: it is the x word
+                        xr[k][0] = mx[k] << ((J[k] & 1) * 16);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < IM; ++e)
+                            xr[k][e] = (inl && (uint32_t)e < nnz)
+                                           ? x_gather<MODE>(a, J[k], inline_cd(d[k], e, a.vb) & 15u)
+                                           : 0u;
                     }
-                    if constexpr (MODE == M_BFS) {
-                        const int32_t p = sp[k * WAVE + lane];
-                        if (single) a.parent[row] = p;
-                        else atomicMin(&a.parent[row], p);
+                    const bool flat = act[k] && flat_coo(d[k]);
+                    cnt[k] = flat ? nnz : 0u;
+                    if (flat) hs->stage(k * WAVE + lane, d[k], J[k], LDSBITS ? 0u : mx[k], am[k], 0);
+                }
+                auto inline_products = [&]() {
+#pragma unroll
+                    for (int k = 0; k < SLOTS; ++k) {
+                        hit[k] = 0;
+                        if (act[k] && desc_inline(d[k]))
+                            hit[k] = inline_block<MODE>(a, d[k], J[k], am[k], xr[k], sy + k * WAVE + q * 16,
+                                                        sp + k * WAVE + q * 16);
+                    }
+                };
+                if (ballot(cnt[0] | cnt[1] | cnt[2] | cnt[3])) {
+                    wave_lds_sync();
+                    flat_pass<MODE, false, !LDSBITS, false, false>(a, hs, cnt, d, sy, sp, inline_products);
+#pragma unroll
+                    for (int k = 0; k < SLOTS; ++k) hit[k] |= hs->hitw[k * 4 + q];
+                } else {
+                    inline_products();
+                }
+                wave_lds_sync();
+#pragma unroll
+                for (int k = 0; k < SLOTS; ++k) hq[k] = or16_in_quarter(hit[k]);
+            }
+            // follow the runs: a new block row commits the open run and opens
+            // the next one
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k) {
+                if (vs[k]) {
+                    const int32_t R = (int32_t)s[k];
+                    if (R != Rc) {
+                        commit();
+                        Rc = R;
+                        racc = 0.0;
+                        pacc = INT_MAX;
+                        hc = 0;
+                    }
+                    if (any) {
+                        hc |= hq[k];
+                        if constexpr (valued<MODE>()) racc += (double)sy[k * WAVE + lane];
+                        if constexpr (MODE == M_BFS) pacc = min(pacc, sp[k * WAVE + lane]);
                     }
                 }
-                if (i == 0 && hq[k]) or_mask16(a.ybits, R, hq[k]);
+                if (any) {
+                    if constexpr (valued<MODE>()) sy[k * WAVE + lane] = 0.f;
+                    if constexpr (MODE == M_BFS) sp[k * WAVE + lane] = INT_MAX;
+                }
             }
-            if constexpr (valued<MODE>()) sy[k * WAVE + lane] = 0.f;
-            if constexpr (MODE == M_BFS) sp[k * WAVE + lane] = INT_MAX;
+            if (any) wave_lds_sync();
         }
-        wave_lds_sync();
+        commit();
     }
 }
 
@@ -1675,7 +1714,7 @@ __device__ void pull_compact(const MainArgs &a, int gw, int64_t rcap)
         if (sid < s1) {
             const int4 *p = (const int4 *)(a.sl_col + sid * 16);
             const int4 c0 = p[0], c1 = p[1], c2 = p[2], c3 = p[3];
-            const uint32_t am = row_admit(a, (int32_t)(a.seg_rs[sid] & 0x7FFFFFFFu));
+            const uint32_t am = row_admit(a, (int32_t)a.seg_rs[sid]);
             const int32_t col[16] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w,
                                      c2.x, c2.y, c2.z, c2.w, c3.x, c3.y, c3.z, c3.w};
             if (am) {
@@ -1941,7 +1980,7 @@ __device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rca
         for (int k = 0; k < SLOTS; ++k) {
             J[k] = v[k] ? slot_col(a.sl_col[slot[k]]) : -1;  // (listed slots are COO blocks)
             d[k] = v[k] ? a.sl_desc[slot[k]] : 0ull;
-            R[k] = v[k] ? (int32_t)(a.seg_rs[slot[k] >> 4] & 0x7FFFFFFFu) : -1;
+            R[k] = v[k] ? (int32_t)a.seg_rs[slot[k] >> 4] : -1;
         }
         // runs of one block row, in entry order (k major)
         uint32_t run[SLOTS];
@@ -2666,8 +2705,8 @@ __global__ __launch_bounds__(TPB, 3) void k_fused(MainArgs a, FusedArgs f)
             pull_loop<MODE, true>(a, gw, nw, (float *)L.acc, (int32_t *)L.acc, &L.hs, spec);
         }
     }
-    // 3. completion.  The traversal's results are device-scope atomics
-    // (a.atomic_commit), complete once the wave's memory counter drains, so
+    // 3. completion.  The traversal's results are device-scope atomics,
+    // complete once the wave's memory counter drains, so
     // a done word needs no cache write-back; the compaction reads them with
     // device-coherent loads.
     wave_drain();
@@ -2929,7 +2968,6 @@ static void fill_main_args(const DevMatrix &A, const DevCtx &C, int mode, const 
     a.nreg = 0;
     a.cpw = TPB / 16;
     a.cpm = 0;
-    a.atomic_commit = 0;
 }
 
 int64_t compact_list_entries(int64_t nseg) { return (nseg + 4 * MAX_MAIN_GRID) * 16; }
@@ -2986,7 +3024,6 @@ hipError_t launch_fused(const DevMatrix &A, DevCtx &C, int mode, int32_t k, cons
     MainArgs a;
     fill_main_args(A, C, mode, C.xd, omask, complement, nullptr, a);
     a.clist = nullptr;  // the segment loop at every activity
-    a.atomic_commit = 1;
     FusedArgs f;
     f.x_idx = x_idx;
     f.x_val = x_val;

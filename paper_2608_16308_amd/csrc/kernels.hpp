@@ -21,7 +21,7 @@ struct DevMatrix {
     int32_t dtype = 0;  // dbs_dtype
     const int32_t *sl_col = nullptr;    // 16 nseg: block column, -1 = padding, sign bit = non-COO (listed)
     const uint64_t *sl_desc = nullptr;  // 16 nseg: descriptor
-    const uint32_t *seg_rs = nullptr;   // nseg: block row | 1 << 31 if the row has one segment
+    const uint32_t *seg_rs = nullptr;   // nseg: block row of the segment
     const int32_t *cb_ptr = nullptr;    // block-CSC view: column pointer (nbc + 1)
     const int32_t *csc_row = nullptr;   // block row per CSC position
     const uint64_t *csc_desc = nullptr; // descriptor per CSC position
