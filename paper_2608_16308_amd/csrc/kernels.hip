@@ -33,8 +33,8 @@
 //    upload-time list ahead of the segment loop, in chunks of up to 16
 //    blocks of one block row, with one lane per row (pull_rows).
 //  * fp32 partial sums per row block go through LDS atomics (ds_add_f32), and
-//    are committed to an fp64 accumulator per row: a plain store when the
-//    block row has one segment, a global fp64 atomic otherwise.
+//    are committed to an fp64 accumulator per row with a global fp64 atomic,
+//    once per run of segments of one block row that a quarter-wave takes.
 //  * wave scans and row reductions use DPP row shifts and broadcasts.
 #include <algorithm>
 #include <climits>
