@@ -817,6 +817,7 @@ struct MainArgs {
     int32_t nreg;           // compacted pull: regions (waves of the second kernel's grid)
     int32_t cpw;            // non-COO pass: chunks per workgroup round (1..16)
     int32_t cpm;            // compacted pull below N_nzblk / N_blk = cpm / 1000
+    int32_t creg;           // compacted pull: regions the list's counts have room for
 };
 
 // Independent work units per lane and loop iteration: four segments per
@@ -1676,18 +1677,32 @@ __device__ __forceinline__ void pull_loop(const MainArgs &a, int gw, int nw, flo
 // The compaction tests activity in an LDS copy of the bitmap; without one
 // (more vector blocks than this many bits) the segment loop is used.
 constexpr int32_t COMPACT_BITMAP_WORDS = 8192;
-// Region r (wave r of the compaction fills it, wave r of the walk takes it)
-// covers rcap / 16 consecutive segments and holds up to rcap entries.  False
-// when the list is absent or too small.
-__device__ __forceinline__ bool compact_pull(const MainArgs &a, int32_t N, int64_t &rcap)
+// The segments are cut into nr regions of L = rcap / 16 consecutive
+// segments (L a multiple of 64, so that a compaction round of one segment per
+// lane never straddles two regions; as short as the count array, creg
+// entries, and WALK_MAX_REGIONS regions per walk wave allow); a region holds
+// up to rcap entries.  Wave w of the compaction fills regions w, w + nreg, ..;
+// wave w of the walk takes the same regions, concatenated (they follow one
+// another in slot order).  R-MAT matrices put most of their stored entries in
+// a few block rows: short strided regions spread such a stretch over many
+// waves of the walk instead of leaving it to one (R-MAT 20, regions of 64
+// instead of 305 segments: 1% uniform 119 -> 106 us, 10% clustered 120 -> 110
+// us, 1% clustered 59 -> 61 us).  False when the list is absent or too small.
+#ifndef WALK_MAX_REGIONS
+#define WALK_MAX_REGIONS 8
+#endif
+__device__ __forceinline__ bool compact_pull(const MainArgs &a, int32_t N, int64_t &rcap, int32_t &nr)
 {
-    const int nw = a.nreg;
-    rcap = (a.nseg + nw - 1) / nw * 16;
-    return a.clist != nullptr && a.nseg > 0 && (int64_t)N * 1000 < (int64_t)a.nbc * a.cpm &&
-           ((a.nbc + 31) >> 5) <= COMPACT_BITMAP_WORDS && (int64_t)nw * rcap <= a.clist_cap;
+    const int64_t nw = a.nreg;
+    const int64_t most = min((int64_t)a.creg, nw * WALK_MAX_REGIONS);
+    const int64_t L = most > 0 ? 64 * ((a.nseg + 64 * most - 1) / (64 * most)) : 0;
+    rcap = L * 16;
+    nr = L > 0 ? (int32_t)((a.nseg + L - 1) / L) : 0;
+    return a.clist != nullptr && a.nseg > 0 && nw > 0 && (int64_t)N * 1000 < (int64_t)a.nbc * a.cpm &&
+           ((a.nbc + 31) >> 5) <= COMPACT_BITMAP_WORDS && (int64_t)nr * rcap <= a.clist_cap;
 }
 
-// First half: wave gw takes the segments of its region, one segment per lane
+// First half: a wave takes the segments of region gw, one segment per lane
 // and round (its 16 slot words by four 16-byte loads), and appends the slots
 // that hold work -- a COO block (the listed
 // non-COO blocks carry the sign bit) whose vector block is active, in an
@@ -1770,17 +1785,20 @@ __global__ __launch_bounds__(TPB) void k_pull_compact(MainArgs a)
     __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE, 1>::WORDS];
     const int32_t N = a.counters[C_NZBLK];
     int64_t rcap;
-    if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, rcap)) return;
+    int32_t nr;
+    if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, rcap, nr)) return;
     const int gw = blockIdx.x * (TPB / WAVE) + (threadIdx.x >> 6);
     const int32_t nwords = (a.nbc + 31) >> 5;
     if (nwords <= COMPACT_BITMAP_WORDS) {  // (always, by compact_pull)
         for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
         __syncthreads();
         pull_rows<MODE, true>(a, rows_lds);
-        if (gw < a.nreg) pull_compact<true>(a, gw, rcap);
+        if (gw < a.nreg)
+            for (int32_t r = gw; r < nr; r += a.nreg) pull_compact<true>(a, r, rcap);
     } else {
         pull_rows<MODE, false>(a, rows_lds);
-        if (gw < a.nreg) pull_compact<false>(a, gw, rcap);
+        if (gw < a.nreg)
+            for (int32_t r = gw; r < nr; r += a.nreg) pull_compact<false>(a, r, rcap);
     }
 }
 
@@ -1946,7 +1964,7 @@ struct ActiveLds {
 };
 
 template <int MODE>
-__device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rcap)
+__device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rcap, int32_t nr)
 {
     const int lane = lane_id();
     float *sy = (float *)L.acc;
@@ -1955,8 +1973,23 @@ __device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rca
     for (int t = lane; t < RUN_CAP * 16; t += WAVE) L.acc[t] = ACC0;
     if (lane < RUN_CAP) L.hm[lane] = 0u;
     wave_lds_sync();
-    const uint32_t cnt = a.ccount[gw];
-    const int32_t *list = a.clist + (int64_t)gw * rcap;
+    // the wave's regions, concatenated (they follow one another in slot
+    // order): entry e lies in region j with pre[j] <= e < pre[j + 1]
+    constexpr int RPW = WALK_MAX_REGIONS;
+    uint32_t pre[RPW + 1];
+    pre[0] = 0;
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) pre[j + 1] = pre[j] + (gw + j * a.nreg < nr ? a.ccount[gw + j * a.nreg] : 0u);
+    const uint32_t cnt = pre[RPW];
+    auto list_at = [&](uint32_t e) {
+        int j = 0;
+#pragma unroll
+        for (int t = 1; t < RPW; ++t) j += e >= pre[t] ? 1 : 0;
+        uint32_t pj = pre[0];
+#pragma unroll
+        for (int t = 1; t < RPW; ++t) pj = j == t ? pre[t] : pj;
+        return a.clist[(int64_t)(gw + j * a.nreg) * rcap + (e - pj)];
+    };
     constexpr int IM = inline_max<MODE>();
     // spread x (fewer than 4 indices per nonzero vector block on average):
     // a stored COO block's entries are tested against its vector block's
@@ -1972,7 +2005,7 @@ __device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rca
         for (int k = 0; k < SLOTS; ++k) {
             const uint32_t e = base + (uint32_t)(k * WAVE + lane);
             v[k] = e < cnt;
-            slot[k] = v[k] ? list[e] : 0;
+            slot[k] = v[k] ? list_at(e) : 0;
         }
         int32_t J[SLOTS], R[SLOTS];
         uint64_t d[SLOTS];
@@ -2130,9 +2163,10 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
     if constexpr (PATH == PATH_PUSH) {
         if (path == PATH_PULL) {
             int64_t rcap;
+            int32_t nr;
             const int gw = blockIdx.x * (TPB / WAVE) + w;
-            if (a.nreg > 0 && compact_pull(a, N, rcap) && gw < a.nreg)
-                pull_active<MODE>(a, ((ActiveLds *)lds_raw)[w], gw, rcap);
+            if (a.nreg > 0 && compact_pull(a, N, rcap, nr) && gw < a.nreg)
+                pull_active<MODE>(a, ((ActiveLds *)lds_raw)[w], gw, rcap, nr);
             return;
         }
     }
@@ -2158,7 +2192,8 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
         // below the compaction threshold: the non-COO blocks and the
         // compaction of the segments (the push kernel walks the regions)
         int64_t rcap;
-        const bool compact = a.nreg > 0 && compact_pull(a, N, rcap);
+        int32_t nr;
+        const bool compact = a.nreg > 0 && compact_pull(a, N, rcap, nr);
         if (!pull_takes_compaction<MODE>() && compact) return;  // k_pull_compact
         if (nwords <= LDS_BITMAP_WORDS) {
             for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
@@ -2167,7 +2202,8 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
             pull_rows<MODE, true>(a, (uint32_t *)lds_raw);
             if constexpr (pull_takes_compaction<MODE>()) {
                 if (compact) {
-                    if (gw < a.nreg) pull_compact<true>(a, gw, rcap);
+                    if (gw < a.nreg)
+                        for (int32_t r = gw; r < nr; r += a.nreg) pull_compact<true>(a, r, rcap);
                     return;
                 }
             }
@@ -2968,10 +3004,11 @@ static void fill_main_args(const DevMatrix &A, const DevCtx &C, int mode, const 
     a.nreg = 0;
     a.cpw = TPB / 16;
     a.cpm = 0;
+    a.creg = compact_list_regions();
 }
 
 int64_t compact_list_entries(int64_t nseg) { return (nseg + 4 * MAX_MAIN_GRID) * 16; }
-int32_t compact_list_regions() { return 4 * MAX_MAIN_GRID; }
+int32_t compact_list_regions() { return 8 * MAX_MAIN_GRID; }
 
 hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void *xd,
                        const uint32_t *omask, int complement, int32_t *parent, int forced_path,
