@@ -1064,7 +1064,7 @@ __device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> 
 //   runs (compacted pull): the staged row word is the owner's run; products
 //         go to the run's LDS rows, rows hit per block in hitw[entry].
 template <int MODE, bool PUSH, bool MXK, bool ANYTYPE, bool RUNS, class Between>
-__device__ void flat_pass(const MainArgs &a, HeavyStage<PUSH> *hs, const uint32_t (&cnt)[SLOTS],
+__device__ __forceinline__ void flat_pass(const MainArgs &a, HeavyStage<PUSH> *hs, const uint32_t (&cnt)[SLOTS],
                           const uint64_t (&d)[SLOTS], float *sy, int32_t *sp, Between &&between)
 {
     const int lane = lane_id();
@@ -1714,7 +1714,7 @@ __device__ __forceinline__ bool compact_pull(const MainArgs &a, int32_t N, int64
 // count goes to ccount[gw].  The activity bitmap is copied into LDS when it
 // fits.
 template <bool LDSBITS>
-__device__ void pull_compact(const MainArgs &a, int gw, int64_t rcap)
+__device__ __forceinline__ void pull_compact(const MainArgs &a, int gw, int64_t rcap)
 {
     const int lane = lane_id();
     const int32_t N = a.counters[C_NZBLK];
@@ -1964,7 +1964,7 @@ struct ActiveLds {
 };
 
 template <int MODE>
-__device__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rcap, int32_t nr)
+__device__ __forceinline__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rcap, int32_t nr)
 {
     const int lane = lane_id();
     float *sy = (float *)L.acc;
