@@ -198,11 +198,15 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
     std::vector<int32_t> sl_col, hv_col, hv_cstart, hv_crow;
     std::vector<uint64_t> sl_desc, hv_desc, csc_desc;
     std::vector<uint32_t> seg_rs;
+    std::vector<int32_t> task_order;
     try {
         const size_t nslots = (size_t)16 * (size_t)h->nseg;
         sl_col.assign(nslots, -1);
         sl_desc.assign(nslots, 0ull);
         seg_rs.resize((size_t)h->nseg);
+        // stored COO entries per group of 16 segments (the work of the
+        // segment loop's entry-parallel pass), for the task order below
+        std::vector<int64_t> gent((size_t)((h->nseg + 15) / 16), 0);
         for (int64_t s = 0; s < h->nseg; ++s) {
             const uint64_t sg = h->seg[s];
             const uint32_t first = seg_first(sg), nb = seg_nb(sg);
@@ -211,6 +215,7 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
                 const uint64_t dd = h->desc[first + i];
                 sl_col[slot] = slot_word(h->cb_col[first + i], dd);
                 sl_desc[slot] = dd;
+                if (desc_type(dd) == T_COO && !desc_inline(dd)) gent[(size_t)(s / 16)] += desc_nnz(dd);
                 if (desc_type(dd) != T_COO) {
                     // pulled from the non-COO list (flagged in the slot by the
                     // sign bit of its word); a new chunk starts at a new block
@@ -227,6 +232,17 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
             }
             seg_rs[s] = seg_brow(sg);
         }
+        // segment-loop tasks by decreasing cost: a wave iteration per group
+        // plus one per 256 stored entries (a window of the entry-parallel
+        // pass); ties keep segment order
+        const int64_t ntask = (h->nseg + PULL_TASK_SEGS - 1) / PULL_TASK_SEGS;
+        std::vector<int64_t> tcost((size_t)ntask, 0);
+        for (size_t g = 0; g < gent.size(); ++g)
+            tcost[g / (PULL_TASK_SEGS / 16)] += 1 + (gent[g] + 255) / 256;
+        task_order.resize((size_t)ntask);
+        for (int64_t t = 0; t < ntask; ++t) task_order[(size_t)t] = (int32_t)t;
+        std::stable_sort(task_order.begin(), task_order.end(),
+                         [&](int32_t x, int32_t y) { return tcost[(size_t)x] > tcost[(size_t)y]; });
         hv_cstart.push_back((int32_t)hv_col.size());
         csc_desc.resize((size_t)h->nblk);
         for (int64_t q = 0; q < h->nblk; ++q) csc_desc[q] = h->desc[h->csc2csr[q]];
@@ -249,13 +265,15 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
         (s2 = dev_upload(A->allocs, hv_desc, &d.hv_desc)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, hv_cstart, &d.hv_cstart)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, hv_crow, &d.hv_crow)) != DBS_OK ||
-        (s2 = dev_upload(A->allocs, h->payload, &d.pay, 16)) != DBS_OK) {
+        (s2 = dev_upload(A->allocs, h->payload, &d.pay, 16)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, task_order, &d.task_order)) != DBS_OK) {
         free_all(A->allocs);
         delete A;
         return s2;
     }
     d.nheavy = (int64_t)hv_col.size();
     d.nchunk = (int64_t)hv_crow.size();
+    d.ntask = (int32_t)task_order.size();
     fill_info(*h, &A->info);
     *out = A;
     return DBS_OK;

@@ -818,6 +818,8 @@ struct MainArgs {
     int32_t cpw;            // non-COO pass: chunks per workgroup round (1..16)
     int32_t cpm;            // compacted pull below N_nzblk / N_blk = cpm / 1000
     int32_t creg;           // compacted pull: regions the list's counts have room for
+    const int32_t *torder;  // segment-loop tasks by decreasing cost (NULL: segment order)
+    int32_t ntask;          // tasks in torder
 };
 
 // Independent work units per lane and loop iteration: four segments per
@@ -1505,6 +1507,9 @@ __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L)
 #define PULL_TASKS_PER_WAVE 4
 #endif
 
+#ifndef ORDER_MODES
+#define ORDER_MODES(M) valued<M>()
+#endif
 template <int MODE, bool LDSBITS>
 __device__ __forceinline__ void pull_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<false> *hs,
                           bool spec)
@@ -1513,12 +1518,30 @@ __device__ __forceinline__ void pull_loop(const MainArgs &a, int gw, int nw, flo
     constexpr int IM = inline_max<MODE>();
     // (segment ids fit 32 bits: the upload keeps 16 nseg below 2^31)
     const int32_t nseg = (int32_t)a.nseg;
+    static_assert(PULL_TASK_SEGS % (4 * SLOTS) == 0, "a task is whole iterations");
     const int32_t spq = nseg >= nw * 4 * SLOTS * 2 ? SLOTS : 1, W = 4 * spq;
-    int32_t G = nseg / (nw * W * PULL_TASKS_PER_WAVE);
-    constexpr int32_t GMAX = valued<MODE>() ? PULL_TASK_ITERS : 1;
-    G = G < 1 ? 1 : (G > GMAX ? GMAX : G);
-    const int32_t ntask = (nseg + G * W - 1) / (G * W);
-    for (int32_t task = gw; task < ntask; task += nw) {
+    // the matrix's task order (tasks of PULL_TASK_SEGS segments) when an
+    // iteration takes 4 SLOTS segments; else G iterations per task in
+    // segment order
+    const bool ordered = ORDER_MODES(MODE) && a.torder != nullptr && spq == SLOTS;
+    int32_t G, ntask;
+    if (ordered) {
+        G = PULL_TASK_SEGS / W;
+        ntask = a.ntask;
+    } else {
+        G = nseg / (nw * W * PULL_TASKS_PER_WAVE);
+        constexpr int32_t GMAX = valued<MODE>() ? PULL_TASK_ITERS : 1;
+        G = G < 1 ? 1 : (G > GMAX ? GMAX : G);
+        ntask = (nseg + G * W - 1) / (G * W);
+    }
+    // ordered tasks are dealt out by rank in snake order: round j gives rank
+    // j nw + nw - 1 - gw to wave gw for even j and j nw + gw for odd j (the
+    // first workgroups also take the first chunks of the non-COO pass);
+    // tasks in segment order grid-stride
+    for (int32_t r0 = 0; r0 < ntask; r0 += nw) {
+        const int32_t r = r0 + ((!ordered || ((r0 / nw) & 1)) ? gw : nw - 1 - gw);
+        if (r >= ntask) continue;
+        const int32_t task = ordered ? a.torder[r] : r;
         const int32_t ts = task * G * W + q * spq;
         // the open run of the quarter: its block row, lane i's share of row
         // i (fp64 across segments) and the rows hit
@@ -3005,6 +3028,8 @@ static void fill_main_args(const DevMatrix &A, const DevCtx &C, int mode, const 
     a.cpw = TPB / 16;
     a.cpm = 0;
     a.creg = compact_list_regions();
+    a.torder = A.task_order;
+    a.ntask = A.ntask;
 }
 
 int64_t compact_list_entries(int64_t nseg) { return (nseg + 4 * MAX_MAIN_GRID) * 16; }

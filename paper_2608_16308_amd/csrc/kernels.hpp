@@ -35,7 +35,16 @@ struct DevMatrix {
     const int32_t *hv_crow = nullptr;    // nchunk
     int64_t nheavy = 0, nchunk = 0;
     const uint8_t *pay = nullptr;
+    // Segment-loop tasks (PULL_TASK_SEGS consecutive segments each) in
+    // descending order of their stored-COO work, so that the waves, dealt
+    // the tasks in this order, get even shares (NULL: the tasks in segment
+    // order, as for a matrix converted on the device).
+    const int32_t *task_order = nullptr;
+    int32_t ntask = 0;
 };
+
+// Segments per segment-loop task: two wave iterations of 16 segments.
+constexpr int32_t PULL_TASK_SEGS = 32;
 
 // Counter slots in the context's device counter array.
 enum Counter : int {
