@@ -721,6 +721,49 @@ __device__ __forceinline__ uint32_t nth_bit16(uint32_t v, uint32_t k)
     return pos;
 }
 
+// Push stages a stored COO block whose vector-block mask leaves some columns
+// out with this tag in place of its format, when the wave iteration's COO
+// records hold more than COO_LIVE_WAVE entries: the staged mask word then
+// holds the block's matching entries (column active, row admitted), read
+// from its coordinates at staging, and the entry-parallel pass walks those
+// only (a chunk of hub blocks otherwise loads every stored entry, most of
+// which miss a sparse x, in a dozen serial windows).
+constexpr uint32_t T_COO_LIVE = 5;
+#ifndef COO_LIVE_WAVE
+#define COO_LIVE_WAVE 256
+#endif
+#ifndef COO_LIVE_MAX
+#define COO_LIVE_MAX 32
+#endif
+static_assert(COO_LIVE_MAX <= 32, "one 32-bit mask per block");
+
+// Matching entries (bit e: entry e) of a COO record of nnz <= COO_LIVE_MAX
+// fp32 entries: its coordinate bytes follow the 4 nnz value bytes, so they
+// start 4-byte aligned.
+__device__ __forceinline__ uint32_t coo_live_mask(const uint8_t *rec, uint32_t nnz, uint32_t mx, uint32_t am)
+{
+    constexpr int NW = (COO_LIVE_MAX + 3) / 4;
+    const uint32_t *cw = (const uint32_t *)(rec + 4u * nnz);
+    uint32_t w[NW];
+#pragma unroll
+    for (int q = 0; q < NW; ++q) w[q] = (uint32_t)(4 * q) < nnz ? cw[q] : 0u;
+    uint32_t m = 0;
+#pragma unroll
+    for (int e = 0; e < COO_LIVE_MAX; ++e) {
+        const uint32_t cd = (w[e >> 2] >> ((e & 3) * 8)) & 0xFFu;
+        const bool hit = (uint32_t)e < nnz && ((mx >> (cd & 15u)) & 1u) && ((am >> (cd >> 4)) & 1u);
+        m |= (hit ? 1u : 0u) << e;
+    }
+    return m;
+}
+
+// The e-th set bit of a 32-bit mask (e below its population count).
+__device__ __forceinline__ uint32_t nth_bit32(uint32_t v, uint32_t e)
+{
+    const uint32_t lo = __popc(v & 0xFFFFu);
+    return e < lo ? nth_bit16(v & 0xFFFFu, e) : 16u + nth_bit16(v >> 16, e - lo);
+}
+
 // Group t's mask restricted to the entries one push task has to multiply
 // (Sec. 3.3.3: the block's structure against blk_x_mask): entries whose column
 // is active in the vector-block mask mx and whose row is admitted (am).  The
@@ -988,6 +1031,11 @@ __device__ __forceinline__ FlatEntries flat_issue(const MainArgs &a, HeavyStage<
         if (type == T_COO) {
             cd = valid ? a.pay[off + (uint64_t)a.vb * nnz + e] : 0u;
             if constexpr (valued<MODE>()) f.val[j] = valid ? VT<MODE>::load(a.pay + off, e) : 0.f;
+        } else if (ANYTYPE && type == T_COO_LIVE) {
+            // the e-th matching entry of the record
+            const uint32_t ei = nth_bit32(hs->mxam[o], e);
+            cd = valid ? a.pay[off + (uint64_t)a.vb * nnz + ei] : 0u;
+            if constexpr (valued<MODE>()) f.val[j] = valid ? VT<MODE>::load(a.pay + off, ei) : 0.f;
         } else if constexpr (ANYTYPE) {
             // the other formats: the e-th live entry, located from the header
             if (valid) {
@@ -1018,8 +1066,11 @@ __device__ __forceinline__ void flat_finish(const MainArgs &a, HeavyStage<PUSH> 
         const uint32_t o = (f.ocd[j] >> 8) & 0xFFu, r = (f.ocd[j] >> 4) & 15u, c = f.ocd[j] & 15u;
         // with the vector-block mask staged, an entry whose column it lacks
         // needs no gather
-        const bool adm = (f.ocd[j] >> 31) && ((hs->mxam[o] >> (16 + r)) & 1u) &&
-                         (!MXK || ((hs->mxam[o] >> c) & 1u));
+        // (a COO_LIVE block stages only matching entries, its mask word
+        // holding which)
+        const bool live = PUSH && ((uint32_t)hs->J[o] >> 28) == T_COO_LIVE;
+        const bool adm = (f.ocd[j] >> 31) &&
+                         (live || (((hs->mxam[o] >> (16 + r)) & 1u) && (!MXK || ((hs->mxam[o] >> c) & 1u))));
         raw[j] = (adm && !known) ? x_gather<MODE>(a, hs->J[o] & 0x0FFFFFFF, c) : 0u;
         if (!adm) f.ocd[j] = 0u;
     }
@@ -1938,6 +1989,17 @@ __device__ __forceinline__ void push_loop(const MainArgs &a, int gw, int nw, flo
             if (!act[k]) d[k] = 0ull;
         }
         uint32_t hit[SLOTS], cnt[SLOTS];
+        // the matching entries of stored COO blocks are read from their
+        // coordinates (one more dependent load) only when the iteration's
+        // COO records hold more than one window of the entry-parallel pass
+        bool coo_live = false;
+        if constexpr (MODE == M_F32) {
+            uint32_t ce = 0;
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k)
+                ce += (act[k] && !desc_inline(d[k]) && desc_type(d[k]) == T_COO) ? desc_nnz(d[k]) : 0u;
+            coo_live = wave_sum(ce) > (uint32_t)COO_LIVE_WAVE;
+        }
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
             hit[k] = 0;
@@ -1951,10 +2013,20 @@ __device__ __forceinline__ void push_loop(const MainArgs &a, int gw, int nw, flo
             // from the record's masks
             const bool flat = act[k] && !desc_inline(d[k]);
             cnt[k] = flat ? desc_nnz(d[k]) : 0u;
+            uint32_t tag = desc_type(d[k]), mword = mx[k] | (am[k] << 16);
             if (flat && desc_type(d[k]) != T_COO)
                 cnt[k] = live_count(load_masks(a.pay + desc_off(d[k])), desc_type(d[k]), mx[k], am[k]);
-            if (cnt[k])
-                hs->stage(k * WAVE + lane, d[k], J[k] | (int32_t)(desc_type(d[k]) << 28), mx[k], am[k], R[k]);
+            if constexpr (MODE == M_F32) {
+                if (coo_live && flat && desc_type(d[k]) == T_COO && cnt[k] <= COO_LIVE_MAX && __popc(mx[k]) < 16) {
+                    mword = coo_live_mask(a.pay + desc_off(d[k]), cnt[k], mx[k], am[k]);
+                    cnt[k] = __popc(mword);
+                    tag = T_COO_LIVE;
+                }
+            }
+            if (cnt[k]) {
+                hs->stage(k * WAVE + lane, d[k], J[k] | (int32_t)(tag << 28), 0u, 0u, R[k]);
+                hs->mxam[k * WAVE + lane] = mword;
+            }
         }
         if (ballot(cnt[0] | cnt[1] | cnt[2] | cnt[3])) {
             wave_lds_sync();

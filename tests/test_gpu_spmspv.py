@@ -281,3 +281,51 @@ def test_single_scan_tile_counts(torch):
             assert oracle.within_tol(y_val.cpu().numpy(), rv, rs, REL_TOL).all()
     log("one scan tile clean call after the flagged ones")
     check_spmspv(ctx, A, om, a, idx, vals, label="one scan tile after errors")
+
+
+def coo_column_matrix(key: int) -> wl.CSR:
+    """Block columns 0..3 of a 4096 x 256 matrix filled with stored COO blocks
+    (2..31 entries each, in random cells), the other block columns sparse:
+    a push over x in those columns stages more than 256 COO entries per wave
+    iteration, so push takes the blocks' matching entries only."""
+    rng = wl.rng_for(wl.W_RAND, 40, key)
+    rows, cols = [], []
+    for R in range(256):
+        for J in range(4):
+            cnt = int(rng.integers(2, 32))
+            cells = rng.choice(256, size=cnt, replace=False)
+            rows.append(R * 16 + cells // 16)
+            cols.append(J * 16 + cells % 16)
+        # a few single entries elsewhere
+        for J in rng.choice(np.arange(4, 16), size=2, replace=False):
+            c = int(rng.integers(0, 256))
+            rows.append(np.array([R * 16 + c // 16]))
+            cols.append(np.array([int(J) * 16 + c % 16]))
+    r, c = np.concatenate(rows), np.concatenate(cols)
+    vals = wl._nonzero_uniform(wl.rng_for(wl.W_RAND, 40, key, 1), -1.0, 1.0, r.size)
+    return wl.csr_from_coo(4096, 256, r, c, vals)
+
+
+def test_push_coo_matching_entries(torch):
+    a = coo_column_matrix(1)
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    rng = wl.rng_for(wl.W_RAND, 41, 0)
+    mw = mask_words(rng.random(a.m) < 0.5)
+    cases = {
+        # one column per vector block (sparse masks: matching entries only)
+        "one_col": np.array([3, 21, 40, 60, 100, 200], dtype=np.int32),
+        # some vector blocks whole (every column: the whole records)
+        "mixed": np.concatenate([np.arange(16, 32), np.array([5, 50, 130])]).astype(np.int32),
+        # a column that no COO block of its vector block uses is still fine
+        "two_cols": np.array([0, 15, 33, 47], dtype=np.int32),
+    }
+    for name, xi in cases.items():
+        xi = np.sort(xi)
+        xv = wl._nonzero_uniform(wl.rng_for(wl.W_RAND, 41, len(xi)), -1.0, 1.0, xi.size)
+        for mask, comp in ((None, False), (mw, False), (mw, True)):
+            label = f"coo columns x={name} push mask={'none' if mask is None else ('comp' if comp else 'on')}"
+            log(label)
+            check_spmspv(ctx, A, om, a, xi, xv.astype(np.float64), path="push", mask=mask, complement=comp,
+                         label=label)
+        check_spmspv(ctx, A, om, a, xi, xv.astype(np.float64), path="auto", label=f"coo columns x={name} auto")
