@@ -2352,7 +2352,7 @@ __global__ __launch_bounds__(TPB) void k_rows(MainArgs a)
 constexpr int FTPB = FINALIZE_TPB;                 // threads per compaction workgroup
 constexpr int FIN_WORDS = FINALIZE_WORDS;
 constexpr int FIN_ROUNDS = FIN_WORDS * 32 / FTPB;  // rows per thread
-static_assert(FIN_WORDS <= FTPB && FIN_ROUNDS >= 1, "finalize tile");
+static_assert(FIN_WORDS <= FTPB && FIN_ROUNDS >= 1 && FIN_WORDS * 32 <= 16 * (FTPB - WAVE), "finalize tile");
 
 template <int MODE>
 __global__ __launch_bounds__(FTPB) void k_finalize(uint32_t *__restrict__ ybits, int32_t nywords,
@@ -2369,6 +2369,11 @@ __global__ __launch_bounds__(FTPB) void k_finalize(uint32_t *__restrict__ ybits,
     __shared__ uint64_t s_prefix;
     __shared__ uint32_t s_word[FIN_WORDS];
     __shared__ uint32_t s_wpos[FIN_WORDS];
+    const int tile = blockIdx.x;
+    const int32_t w = tile * FIN_WORDS + threadIdx.x;
+    // the tile's structure words first: the scatter stores below then do not
+    // delay them
+    const uint32_t word = ((int)threadIdx.x < FIN_WORDS && w < nywords) ? ybits[w] : 0u;
     for (int32_t i = blockIdx.x * FTPB + threadIdx.x; i < n_status; i += gridDim.x * FTPB)
         next_status[i] = 0;
     // clear the blk_x_mask words this call's x indices touched, and put the
@@ -2381,14 +2386,28 @@ __global__ __launch_bounds__(FTPB) void k_finalize(uint32_t *__restrict__ ybits,
             if constexpr (MODE == M_F16) ((uint16_t *)xd)[j] = (uint16_t)0xFFFFu;
         }
     }
-    const int tile = blockIdx.x;
-    const int32_t w = tile * FIN_WORDS + threadIdx.x;
-    const uint32_t word = ((int)threadIdx.x < FIN_WORDS && w < nywords) ? ybits[w] : 0u;
     uint64_t total;
     const uint64_t excl = block_exclusive_scan<FTPB>((uint64_t)__popc(word), &total, lds4);
     if ((int)threadIdx.x < FIN_WORDS) {
         s_word[threadIdx.x] = word;
         s_wpos[threadIdx.x] = (uint32_t)excl;
+    }
+    __syncthreads();
+    // wave 0 runs the look-back while the other waves load the accumulators
+    // of the tile's rows (row (t - 64) + (FTPB - 64) u for thread t >= 64),
+    // so that the two round trips overlap
+    constexpr int RT = FTPB - WAVE, RROUNDS = (FIN_WORDS * 32 + RT - 1) / RT;
+    const int64_t row0 = (int64_t)tile * FIN_WORDS * 32;
+    double v[RROUNDS];
+    uint32_t hm = 0;
+    if (threadIdx.x >= WAVE) {
+#pragma unroll
+        for (int u = 0; u < RROUNDS; ++u) {
+            const int lr = u * RT + (int)threadIdx.x - WAVE;
+            const bool h = lr < FIN_WORDS * 32 && ((s_word[lr >> 5] >> (lr & 31)) & 1u);
+            hm |= (h ? 1u : 0u) << u;
+            v[u] = (valued<MODE>() && h) ? yacc[row0 + lr] : 0.0;
+        }
     }
     if (threadIdx.x < WAVE) {
         uint64_t prefix = 0;
@@ -2404,33 +2423,18 @@ __global__ __launch_bounds__(FTPB) void k_finalize(uint32_t *__restrict__ ybits,
     __syncthreads();
     if (word) ybits[w] = 0u;
     const int64_t base_pos = (int64_t)s_prefix;
-    const int64_t row0 = (int64_t)tile * FIN_WORDS * 32;
-    // up to 16 rounds at a time: the accumulator loads of all go out together
-    constexpr int FB = FIN_ROUNDS < 16 ? FIN_ROUNDS : 16;
-    for (int r0 = 0; r0 < FIN_ROUNDS; r0 += FB) {
-        double v[FB];
-        uint32_t hm = 0;
 #pragma unroll
-        for (int u = 0; u < FB; ++u) {
-            const int lr = (r0 + u) * FTPB + threadIdx.x;  // row within the tile
-            const uint32_t wd = s_word[lr >> 5];
-            const bool h = (wd >> (lr & 31)) & 1u;
-            hm |= (h ? 1u : 0u) << u;
-            v[u] = (valued<MODE>() && h) ? yacc[row0 + lr] : 0.0;
-        }
-#pragma unroll
-        for (int u = 0; u < FB; ++u) {
-            if (!((hm >> u) & 1u)) continue;
-            const int lr = (r0 + u) * FTPB + threadIdx.x;
-            const uint32_t wd = s_word[lr >> 5];
-            const uint32_t bit = lr & 31;
-            const int64_t pos = base_pos + s_wpos[lr >> 5] + __popc(wd & ((1u << bit) - 1u));
-            const int64_t i = row0 + lr;
-            y_idx[pos] = (int32_t)i;
-            if constexpr (MODE == M_F32) ((float *)y_val)[pos] = (float)v[u];
-            if constexpr (MODE == M_F16) ((uint16_t *)y_val)[pos] = f64_to_f16_rne(v[u]);
-            if constexpr (valued<MODE>()) yacc[i] = 0.0;
-        }
+    for (int u = 0; u < RROUNDS; ++u) {
+        if (!((hm >> u) & 1u)) continue;
+        const int lr = u * RT + (int)threadIdx.x - WAVE;
+        const uint32_t wd = s_word[lr >> 5];
+        const uint32_t bit = lr & 31;
+        const int64_t pos = base_pos + s_wpos[lr >> 5] + __popc(wd & ((1u << bit) - 1u));
+        const int64_t i = row0 + lr;
+        y_idx[pos] = (int32_t)i;
+        if constexpr (MODE == M_F32) ((float *)y_val)[pos] = (float)v[u];
+        if constexpr (MODE == M_F16) ((uint16_t *)y_val)[pos] = f64_to_f16_rne(v[u]);
+        if constexpr (valued<MODE>()) yacc[i] = 0.0;
     }
     if (tile == (int)gridDim.x - 1 && threadIdx.x == 0) {
         int32_t tot = (int32_t)(s_prefix + total);
