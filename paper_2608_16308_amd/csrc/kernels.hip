@@ -1861,18 +1861,18 @@ __global__ __launch_bounds__(TPB) void k_pull_compact(MainArgs a)
     int64_t rcap;
     int32_t nr;
     if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, rcap, nr)) return;
-    const int gw = blockIdx.x * (TPB / WAVE) + (threadIdx.x >> 6);
+    // every wave of the grid (its resident size, more waves than the walk's
+    // when this kernel's registers allow) takes regions gw, gw + nw, ..
+    const int gw = blockIdx.x * (TPB / WAVE) + (threadIdx.x >> 6), nw = gridDim.x * (TPB / WAVE);
     const int32_t nwords = (a.nbc + 31) >> 5;
     if (nwords <= COMPACT_BITMAP_WORDS) {  // (always, by compact_pull)
         for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
         __syncthreads();
         pull_rows<MODE, true>(a, rows_lds);
-        if (gw < a.nreg)
-            for (int32_t r = gw; r < nr; r += a.nreg) pull_compact<true>(a, r, rcap);
+        for (int32_t r = gw; r < nr; r += nw) pull_compact<true>(a, r, rcap);
     } else {
         pull_rows<MODE, false>(a, rows_lds);
-        if (gw < a.nreg)
-            for (int32_t r = gw; r < nr; r += a.nreg) pull_compact<false>(a, r, rcap);
+        for (int32_t r = gw; r < nr; r += nw) pull_compact<false>(a, r, rcap);
     }
 }
 
@@ -2924,6 +2924,29 @@ static int resident_grid(size_t dyn_lds)
     return grid;
 }
 
+// Resident workgroups of k_pull_compact with dyn_lds bytes of dynamic LDS.
+template <int MODE>
+static int compact_grid(size_t dyn_lds)
+{
+    static size_t cached_lds[8];
+    static int cached_grid[8];
+    static int ncached = 0;
+    for (int i = 0; i < ncached; ++i)
+        if (cached_lds[i] == dyn_lds) return cached_grid[i];
+    int dev = 0, cus = 0, per_cu = 0, grid = MAX_MAIN_GRID;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_pull_compact<MODE>, TPB, dyn_lds) == hipSuccess &&
+        cus > 0 && per_cu > 0)
+        grid = min(cus * per_cu, MAX_MAIN_GRID);
+    if (ncached < 8) {
+        cached_lds[ncached] = dyn_lds;
+        cached_grid[ncached] = grid;
+        ++ncached;
+    }
+    return grid;
+}
+
 // Chunks per round for k_rows: the fewest (at most 16) that keep its grid
 // within one round of resident workgroups.
 template <int MODE, int NB>
@@ -2976,7 +2999,8 @@ static hipError_t launch_paths(const DevMatrix &A, const MainArgs &a, int forced
         e = hipGetLastError();
         if (e == hipSuccess && b.nreg > 0 && (dyn == 0 || !pull_takes_compaction<MODE>())) {
             const size_t dync = nwords <= COMPACT_BITMAP_WORDS ? (size_t)nwords * 4 : 0;
-            hipLaunchKernelGGL((k_pull_compact<MODE>), dim3(b.nreg / (TPB / WAVE)), dim3(TPB), dync, s, b);
+            const int gc = compact_grid<MODE>(dync);
+            hipLaunchKernelGGL((k_pull_compact<MODE>), dim3(gc), dim3(TPB), dync, s, b);
             e = hipGetLastError();
         }
     }
