@@ -1204,8 +1204,8 @@ template <int MODE, int NB = 1> struct RowsLds {
     static constexpr int AC = VB + (MODE == M_F16 ? NQ * HV_VAL_BYTES / 4 : 0);  // fp64 [vector][chunk][row]
     static constexpr int HM = AC + NB * NQ * 16 * 2;  // rows hit per chunk
     static constexpr int CR = HM + NQ;             // block row per chunk (-1: none)
-    static constexpr int NI = CR + NQ;             // active blocks per wave
-    static constexpr int IT = NI + 8;              // listed blocks (staging index, one byte each)
+    static constexpr int NI = CR + NQ;             // active blocks per wave: Dense, then the others
+    static constexpr int IT = NI + 2 * (NT / WAVE);  // listed blocks (staging index, one byte each)
     static constexpr int XQ = IT + NT / 4;         // fp16, one vector: x of the quarter's block (fp32)
     static constexpr int WORDS = XQ + (MODE == M_F16 && NB == 1 ? NQ * 16 : 0);
 };
@@ -1261,8 +1261,27 @@ __device__ __forceinline__ void row_values(const uint8_t *vals, bool colview, co
 // active for any of them are visited, each row value is loaded once and
 // multiplied with the NB dense x (zeros where a vector has no entry), and
 // the NB sums go to NB accumulator sets (x and accumulators NB-strided).
+// A round's chunk bounds and block row for thread t (chunk c0 + t / 16 of
+// the round starting at chunk c0), so that a caller can issue the first
+// round's loads before anything else it waits for.
+struct RowsPre {
+    int32_t h0, h1, R;
+    bool valid;
+};
+__device__ __forceinline__ RowsPre rows_pre(const MainArgs &a, int64_t c0)
+{
+    const int cs = threadIdx.x >> 4;
+    const int64_t ch = c0 + cs;
+    RowsPre p;
+    p.valid = cs < a.cpw && ch < a.nchunk;
+    p.h0 = p.valid ? a.hv_cstart[ch] : 0;
+    p.h1 = p.valid ? a.hv_cstart[ch + 1] : 0;
+    p.R = p.valid ? a.hv_crow[ch] : 0;
+    return p;
+}
+
 template <int MODE, bool LDSBITS, int NB = 1>
-__device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L)
+__device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L, const RowsPre *first = nullptr)
 {
     using Y = RowsLds<MODE, NB>;
     static_assert(NB == 1 || valued<MODE>(), "batched pull is for valued modes");
@@ -1275,11 +1294,9 @@ __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L)
     constexpr int VW = MODE == M_F16 ? 8 : 16;
     for (int64_t c0 = (int64_t)blockIdx.x * a.cpw; c0 < a.nchunk; c0 += (int64_t)gridDim.x * a.cpw) {
         // 1. metadata, headers and x masks of the round's blocks; the list of the active ones
-        const int64_t ch = c0 + cs;
-        const bool valid = cs < a.cpw && ch < a.nchunk;
-        const int32_t h0 = valid ? a.hv_cstart[ch] : 0;
-        const int32_t h1 = valid ? a.hv_cstart[ch + 1] : 0;
-        const int32_t R = valid ? a.hv_crow[ch] : 0;
+        const RowsPre rp = (first && c0 == (int64_t)blockIdx.x * a.cpw) ? *first : rows_pre(a, c0);
+        const bool valid = rp.valid;
+        const int32_t h0 = rp.h0, h1 = rp.h1, R = rp.R;
         const uint32_t am = valid ? row_admit(a, R) : 0u;
         const int32_t h = h0 + (int32_t)r;
         bool act = h < h1 && am != 0;
@@ -1314,17 +1331,27 @@ __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L)
             L[Y::HM + cs] = 0u;
             L[Y::CR + cs] = valid ? (uint32_t)R : 0xFFFFFFFFu;
         }
-        const uint64_t bm = ballot(act);
-        if (lane == 0) L[Y::NI + wv] = (uint32_t)__popcll(bm);
+        // the list holds the Dense blocks first, so that the four quarters of
+        // a wave mostly take blocks of one kind at a time (the Dense and the
+        // other formats' code paths are not both run)
+        const bool dn = desc_type(d) == T_DENSE;
+        const uint64_t bmd = ballot(act && dn), bmo = ballot(act && !dn);
+        if (lane == 0) {
+            L[Y::NI + wv] = (uint32_t)__popcll(bmd);
+            L[Y::NI + TPB / WAVE + wv] = (uint32_t)__popcll(bmo);
+        }
         __syncthreads();
-        uint32_t base = 0, total = 0;
+        uint32_t based = 0, baseo = 0, totd = 0, total = 0;
 #pragma unroll
         for (int w = 0; w < TPB / WAVE; ++w) {
-            const uint32_t cw = L[Y::NI + w];
-            base += w < wv ? cw : 0u;
-            total += cw;
+            const uint32_t cd = L[Y::NI + w], co = L[Y::NI + TPB / WAVE + w];
+            based += w < wv ? cd : 0u;
+            baseo += w < wv ? co : 0u;
+            totd += cd;
+            total += cd + co;
         }
-        if (act) items[base + __popcll(bm & ((1ull << lane) - 1ull))] = (uint8_t)t;
+        const uint64_t below = (1ull << lane) - 1ull;
+        if (act) items[dn ? based + __popcll(bmd & below) : totd + baseo + __popcll(bmo & below)] = (uint8_t)t;
         __syncthreads();
         // 2. the listed blocks, round-robin over the quarter-waves
         for (uint32_t it = (uint32_t)cs; ballot(it < total); it += Y::NQ) {
@@ -2327,15 +2354,21 @@ __global__ __launch_bounds__(TPB) void k_rows(MainArgs a)
     __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE, NB>::WORDS];
     // BFS: the host has read the frontier size of this level; restart the count
     if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
+    // the first round's chunk bounds and the first bitmap words go out with
+    // the device choice (the loads do not depend on it)
+    const RowsPre first = rows_pre(a, (int64_t)blockIdx.x * a.cpw);
+    const int32_t nwords = (a.nbc + 31) >> 5;
+    const int t0 = threadIdx.x;
+    const uint32_t xb0 = (nwords <= LDS_BITMAP_WORDS && t0 < nwords) ? a.xbits[t0] : 0u;
     const int32_t N = a.counters[C_NZBLK];
     if (N == 0 || a.counters[C_PATH] != PATH_PULL) return;
-    const int32_t nwords = (a.nbc + 31) >> 5;
     if (nwords <= LDS_BITMAP_WORDS) {
-        for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
+        if (t0 < nwords) lds_bits[t0] = xb0;
+        for (int32_t t = t0 + TPB; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
         __syncthreads();
-        pull_rows<MODE, true, NB>(a, rows_lds);
+        pull_rows<MODE, true, NB>(a, rows_lds, &first);
     } else {
-        pull_rows<MODE, false, NB>(a, rows_lds);
+        pull_rows<MODE, false, NB>(a, rows_lds, &first);
     }
 }
 
