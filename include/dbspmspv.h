@@ -63,11 +63,20 @@ typedef enum { DBS_PATH_AUTO = 0, DBS_PATH_PUSH = 1, DBS_PATH_PULL = 2 } dbs_pat
  * one matching column, which measured faster than pull up to about that
  * activity, while clustered x (up to 16 indices per vector block) favours
  * pull from the paper's threshold on.  An explicit th3 > 0 gives the
- * paper's rule alone, and so does dbs_bfs (a spread frontier's pull is
- * cheap once the visited rows are masked out).                            */
+ * paper's rule alone.
+ * BFS levels (dbs_bfs) with the default th3 take push iff the level's push
+ * tasks -- the blocks in the block-CSC lists of the frontier's nonzero
+ * vector blocks, which the scan sums anyway -- are fewer than
+ * DBS_BFS_PUSH_TASKS * nblk.  On R-MAT 22 the paper's rule takes pull on
+ * the levels after the largest one (s_b 0.1-0.5), where the visited rows
+ * leave little for push (1-10% of the blocks as tasks) but pull still
+ * walks every segment: push measured 2-4x faster there, and pull faster
+ * from about 60% of the blocks as tasks on.  An explicit th3 > 0 gives the
+ * paper's rule for BFS too.                                                */
 #define DBS_TH3_DEFAULT 0.01f
 #define DBS_TH3_PAPER 0.01f
 #define DBS_TH3_SPREAD 0.12f
+#define DBS_BFS_PUSH_TASKS 0.25f
 
 /* Low-level block formats (Sec. 3.2.1). */
 typedef enum {
@@ -388,7 +397,9 @@ typedef struct {
 
 /* BFS from `source` (Sec. 4.2, Alg. 5): each level's frontier is the sparse
  * x of a Boolean SpMSpV masked by the complement of the visited set; push or
- * pull is chosen per level by the same rule as dbs_spmspv (or forced).
+ * pull is chosen per level on the device: by the push task count with the
+ * default th3 (DBS_BFS_PUSH_TASKS), by the paper's rule for th3 > 0, or
+ * forced by policy.
  * Edge u -> v iff A[v][u] is stored; A must be square.
  *   d_level[n]   level of each vertex, -1 if unreachable, level[source] = 0
  *   d_parent[n]  smallest-id vertex of the previous level with an edge to v;

@@ -694,10 +694,12 @@ extern "C" dbs_status dbs_bfs(dbs_ctx *ctx, const dbs_matrix *A, int32_t source,
     LAUNCH(ctx, DBS_K_OTHER, launch_bfs_init(A->d, ctx->c, source, d_level, d_parent, s));
     int32_t level = 0, reached = 1, frontier = 1;
     for (;;) {
-        // BFS levels keep the paper's rule: a spread frontier's pull is cheap
-        // once the visited rows are masked out (measured: the spread rule
-        // lost 15% of R-MAT 22 GTEPS)
-        LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, (int)policy, (double)norm_th3(th3), 0.0, s));
+        // BFS levels: with the default th3 push iff the level's push tasks
+        // (blocks in the block-CSC lists of the frontier's column blocks) are
+        // fewer than DBS_BFS_PUSH_TASKS of the matrix's blocks; an explicit
+        // th3 > 0 gives the paper's rule
+        const double tasks_max = th3 > 0.f ? -1.0 : (double)DBS_BFS_PUSH_TASKS * (double)A->d.nblk;
+        LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, (int)policy, (double)norm_th3(th3), 0.0, s, tasks_max));
         if ((st = sync_counters(ctx)) != DBS_OK) {
             ctx->broken = true;
             return st;

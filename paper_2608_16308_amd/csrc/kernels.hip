@@ -234,7 +234,9 @@ __global__ __launch_bounds__(TPB) void k_ballot(const void *__restrict__ x, int3
 // tile fixes N_nzblk (counted by the blocker), the task totals and the
 // global path: push iff N_nzblk < th3 N_blk (Sec. 3.3.1), or, with th3s > 0,
 // also when x is spread (fewer than two indices per nonzero vector block)
-// and N_nzblk < th3s N_blk.
+// and N_nzblk < th3s N_blk; with tasks_max >= 0 (BFS levels) instead push iff
+// the push tasks (blocks in the block-CSC lists of the nonzero vector
+// blocks) number fewer than tasks_max.
 // DX (dense activation, MODE fp32 or fp16, n a multiple of 16, x 16-byte
 // aligned): the blocker is folded into the scan's front end -- each thread
 // reads the x of its vector blocks, writes their densified copy and masks.
@@ -246,7 +248,7 @@ __global__ __launch_bounds__(STPB) void k_scan(uint32_t *__restrict__ xmask, con
                                               uint32_t *__restrict__ xbits,
                                               int32_t *__restrict__ counters, uint64_t *status,
                                               uint64_t *next_status, int32_t n_status,
-                                              int32_t forced_path, double th3, double th3s)
+                                              int32_t forced_path, double th3, double th3s, double tasks_max)
 {
     __shared__ uint64_t lds4[STPB / WAVE];
     __shared__ uint64_t s_cnt[STPB / WAVE];
@@ -398,7 +400,9 @@ __global__ __launch_bounds__(STPB) void k_scan(uint32_t *__restrict__ xmask, con
         counters[C_TASKS] = T;
         items[NT] = make_int4(T, 0, 0, 0);
         int path = forced_path;
-        if (path == 0) {
+        if (path == 0 && tasks_max >= 0.0) {
+            path = (double)T < tasks_max ? PATH_PUSH : PATH_PULL;
+        } else if (path == 0) {
             const bool spread = th3s > 0.0 && (int64_t)pop < 2 * (int64_t)N && (double)N < th3s * (double)nbc;
             path = ((double)N < th3 * (double)nbc || spread) ? PATH_PUSH : PATH_PULL;
         }
@@ -3068,12 +3072,14 @@ hipError_t launch_ballot(const DevMatrix &A, const DevCtx &C, int mode, const vo
     return hipGetLastError();
 }
 
-hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th3, double th3s, hipStream_t s)
+hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th3, double th3s, hipStream_t s,
+                       double tasks_max)
 {
     dim3 g(grid_for(A.nbc, SCAN_TILE, INT_MAX)), b(STPB);
     const int p = C.scan_parity;
     hipLaunchKernelGGL((k_scan<false, 0>), g, b, 0, s, C.xmask, nullptr, nullptr, A.cb_ptr, A.nbc, C.items,
-                       C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3, th3s);
+                       C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3, th3s,
+                       tasks_max);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) C.scan_parity = 1 - p;
     return e;
@@ -3112,10 +3118,10 @@ hipError_t launch_scan_dense(const DevMatrix &A, DevCtx &C, int mode, const void
     const int p = C.scan_parity;
     if (mode == M_F16)
         hipLaunchKernelGGL((k_scan<true, M_F16>), g, b, 0, s, C.xmask, x_dense, C.xd, A.cb_ptr, A.nbc, C.items,
-                           C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3, th3s);
+                           C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3, th3s, -1.0);
     else
         hipLaunchKernelGGL((k_scan<true, M_F32>), g, b, 0, s, C.xmask, x_dense, C.xd, A.cb_ptr, A.nbc, C.items,
-                           C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3, th3s);
+                           C.xbits, C.counters, C.st_scan[p], C.st_scan[1 - p], C.n_st_scan, forced_path, th3, th3s, -1.0);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) C.scan_parity = 1 - p;
     return e;

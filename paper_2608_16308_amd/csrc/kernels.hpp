@@ -131,9 +131,10 @@ hipError_t launch_scatter(const DevMatrix &A, const DevCtx &C, int mode, int32_t
                           const int32_t *x_idx, const void *x_val, hipStream_t s);
 hipError_t launch_ballot(const DevMatrix &A, const DevCtx &C, int mode, const void *x_dense,
                          hipStream_t s);
-// th3s > 0: the spread rule as well (see k_scan)
+// th3s > 0: the spread rule as well; tasks_max >= 0: push iff fewer push
+// tasks than that, in place of both (BFS levels; see k_scan)
 hipError_t launch_scan(const DevMatrix &A, DevCtx &C, int forced_path, double th3, double th3s,
-                       hipStream_t s);
+                       hipStream_t s, double tasks_max = -1.0);
 // Blocker and scan as one single-workgroup kernel, for up to SMALL_X_MAX
 // indices and an activity bitmap of up to SMALL_X_WORDS words (small_x_fits);
 // otherwise launch_scatter + launch_scan.
