@@ -415,7 +415,7 @@ def run_ablation(args, torch, dbs, wl, dev):
         log(f"[ablation] storage {store[-1]}")
     out["storage"] = store
 
-    # (3) BFS under candidate th3
+    # (3) BFS under candidate th3 (0: the default push-task rule of BFS levels)
     if args.bfs_scale > 0:
         g = wl.rmat(args.bfs_scale, values=False)
         srcs = wl.bfs_sources(g, min(args.bfs_sources, 8), key=0)
@@ -424,7 +424,7 @@ def run_ablation(args, torch, dbs, wl, dev):
         level = torch.empty(g.n, dtype=torch.int32, device=dev)
         parent = torch.empty(g.n, dtype=torch.int32, device=dev)
         bfs = []
-        for th3 in (0.01, 0.02, 0.05, 0.1):
+        for th3 in (0.0, 0.01, 0.02, 0.05, 0.1):
             ms = []
             for s0 in srcs:
                 gctx.bfs(G, int(s0), level=level, parent=parent, th3=th3)
@@ -777,6 +777,8 @@ def main():
         hm_gteps = len(gteps) / sum(1.0 / x for x in gteps)
         log(f"[bench] BFS: harmonic mean {hm_gteps:.2f} GTEPS over {len(srcs)} sources; {per_src[:3]}")
         result["bfs"] = {"workload": f"rmat{args.bfs_scale}_bfs_{len(srcs)}_sources", "gteps_hmean": round(hm_gteps, 3),
+                         "selector": "per level push iff the push tasks (blocks in the block-CSC lists of the "
+                                     "frontier's column blocks) < 0.25 nblk",
                          "gteps_min": round(min(gteps), 3), "gteps_max": round(max(gteps), 3),
                          "ms_mean": round(1e3 * float(np.mean(times)), 3), "db_build_s": round(gbuild, 2),
                          "edges_counted": "undirected edges of the source's component", "per_source": per_src}
