@@ -2274,6 +2274,11 @@ constexpr size_t traverse_lds_bytes()
 // compaction (inside the pull kernel it pushed the BFS kernel's arrays out
 // to scratch memory under the earlier 96-register limit).
 template <int MODE> constexpr bool pull_takes_compaction() { return valued<MODE>(); }
+// activity bitmap words per thread that the pull kernel loads before it reads
+// the device choice (the rest after)
+#ifndef PULL_PRE_WORDS
+#define PULL_PRE_WORDS 8
+#endif
 
 template <int MODE, int PATH>
 __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(MainArgs a)
@@ -2282,6 +2287,19 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
     WaveLds<PATH == PATH_PUSH> *lds = (WaveLds<PATH == PATH_PUSH> *)lds_raw;
     // BFS: the host has read the frontier size of this level; restart the count
     if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
+    // pull: the first activity bitmap words this thread copies into LDS go
+    // out with the device choice (they do not depend on it)
+    const int32_t nwords = (a.nbc + 31) >> 5;
+    constexpr int PRE_WORDS = PATH == PATH_PULL ? PULL_PRE_WORDS : 1;
+    uint32_t xbw[PRE_WORDS];
+    if constexpr (PATH == PATH_PULL) {
+        const bool cp = nwords <= LDS_BITMAP_WORDS;
+#pragma unroll
+        for (int k = 0; k < PRE_WORDS; ++k) {
+            const int32_t i = (int32_t)threadIdx.x + k * TPB;
+            xbw[k] = (cp && i < nwords) ? a.xbits[i] : 0u;
+        }
+    }
     const int32_t N = a.counters[C_NZBLK];
     const int32_t path = a.counters[C_PATH];
     if (N == 0) return;
@@ -2314,7 +2332,6 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
         // blocks are used to load their descriptors together with their block
         // columns (measured: a quarter was 1.5% slower at 1% uniform x)
         const bool spec = (int64_t)N * 8 >= (int64_t)a.nbc;
-        const int32_t nwords = (a.nbc + 31) >> 5;
         // below the compaction threshold: the non-COO blocks and the
         // compaction of the segments (the push kernel walks the regions)
         int64_t rcap;
@@ -2322,7 +2339,12 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
         const bool compact = a.nreg > 0 && compact_pull(a, N, rcap, nr);
         if (!pull_takes_compaction<MODE>() && compact) return;  // k_pull_compact
         if (nwords <= LDS_BITMAP_WORDS) {
-            for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
+#pragma unroll
+            for (int k = 0; k < PRE_WORDS; ++k) {
+                const int32_t i = (int32_t)threadIdx.x + k * TPB;
+                if (i < nwords) lds_bits[i] = xbw[k];
+            }
+            for (int32_t i = (int32_t)threadIdx.x + PRE_WORDS * TPB; i < nwords; i += TPB) lds_bits[i] = a.xbits[i];
             __syncthreads();
             // the non-COO pass stages its headers over the wave's whole LDS slice
             pull_rows<MODE, true>(a, (uint32_t *)lds_raw);
