@@ -1819,11 +1819,10 @@ __device__ __forceinline__ bool compact_pull(const MainArgs &a, int32_t N, int64
 // count goes to ccount[gw].  The activity bitmap is copied into LDS when it
 // fits.
 template <bool LDSBITS>
-__device__ __forceinline__ void pull_compact(const MainArgs &a, int gw, int64_t rcap)
+__device__ __forceinline__ void pull_compact(const MainArgs &a, int gw, int64_t rcap, int32_t N, int32_t xpop)
 {
     const int lane = lane_id();
-    const int32_t N = a.counters[C_NZBLK];
-    const bool exact = (int64_t)a.counters[C_XPOP] < 4 * (int64_t)N;
+    const bool exact = (int64_t)xpop < 4 * (int64_t)N;
     const int64_t s0 = (int64_t)gw * (rcap / 16);
     const int64_t s1 = min(a.nseg, s0 + rcap / 16);
     int32_t *out = a.clist + s0 * 16;
@@ -1888,7 +1887,7 @@ template <int MODE>
 __global__ __launch_bounds__(TPB) void k_pull_compact(MainArgs a)
 {
     __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE, 1>::WORDS];
-    const int32_t N = a.counters[C_NZBLK];
+    const int32_t N = a.counters[C_NZBLK], xpop = a.counters[C_XPOP];
     int64_t rcap;
     int32_t nr;
     if (N == 0 || a.counters[C_PATH] != PATH_PULL || !compact_pull(a, N, rcap, nr)) return;
@@ -1900,18 +1899,19 @@ __global__ __launch_bounds__(TPB) void k_pull_compact(MainArgs a)
         for (int32_t t = threadIdx.x; t < nwords; t += TPB) lds_bits[t] = a.xbits[t];
         __syncthreads();
         pull_rows<MODE, true>(a, rows_lds);
-        for (int32_t r = gw; r < nr; r += nw) pull_compact<true>(a, r, rcap);
+        for (int32_t r = gw; r < nr; r += nw) pull_compact<true>(a, r, rcap, N, xpop);
     } else {
         pull_rows<MODE, false>(a, rows_lds);
-        for (int32_t r = gw; r < nr; r += nw) pull_compact<false>(a, r, rcap);
+        for (int32_t r = gw; r < nr; r += nw) pull_compact<false>(a, r, rcap, N, xpop);
     }
 }
 
 // For each of SLOTS wave-uniform targets, the largest a in [0, n) with
 // arr[a] <= target (arr increasing, arr[0] = 0 <= target): a 64-ary search in
 // which the whole wave probes 64 positions per round (log64 n rounds), the
-// SLOTS searches interleaved so that their loads overlap.
-template <int STRIDE>
+// SLOTS searches interleaved so that their loads overlap.  With WIDTH > 1 it
+// stops at a window [res, res + WIDTH) that holds the answer.
+template <int STRIDE, int WIDTH = 1>
 __device__ __forceinline__ void wave_search(const int32_t *__restrict__ arr, int32_t n,
                                             const int32_t (&target)[SLOTS], const bool (&valid)[SLOTS],
                                             int32_t (&res)[SLOTS])
@@ -1926,18 +1926,18 @@ __device__ __forceinline__ void wave_search(const int32_t *__restrict__ arr, int
     for (;;) {
         bool more = false;
 #pragma unroll
-        for (int k = 0; k < SLOTS; ++k) more |= hi[k] - lo[k] > 1;
+        for (int k = 0; k < SLOTS; ++k) more |= hi[k] - lo[k] > WIDTH;
         if (!more) break;
         int32_t v[SLOTS], step[SLOTS], pi[SLOTS];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
             step[k] = (hi[k] - lo[k] + WAVE - 1) / WAVE;
             pi[k] = lo[k] + lane * step[k];
-            v[k] = (hi[k] - lo[k] > 1 && pi[k] < hi[k]) ? arr[(int64_t)pi[k] * STRIDE] : INT_MAX;
+            v[k] = (hi[k] - lo[k] > WIDTH && pi[k] < hi[k]) ? arr[(int64_t)pi[k] * STRIDE] : INT_MAX;
         }
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
-            if (hi[k] - lo[k] <= 1) continue;
+            if (hi[k] - lo[k] <= WIDTH) continue;
             const uint64_t m = ballot(v[k] <= target[k]);  // lane 0 probes lo: always set
             const int L = 63 - __builtin_clzll(m);
             lo[k] += L * step[k];
@@ -1951,15 +1951,15 @@ __device__ __forceinline__ void wave_search(const int32_t *__restrict__ arr, int
 // Push (Sec. 3.3.2): block tasks flattened over the block-CSC lists of the
 // active column blocks; chunks of 64 consecutive tasks, one task per lane,
 // up to SLOTS chunks per wave iteration, grid-stride.  The chunk's first
-// work item comes from a wave search over the item starts; a lane then finds
-// its own item by a 6-step binary search over the next 64 item starts, held
-// one per lane and read by shuffles.
+// work item comes from a wave search over the item starts (its last step
+// taken on a loaded window of items); a lane then finds its own item by a
+// 6-step binary search over the next 64 item starts, held one per lane and
+// read by shuffles.
 template <int MODE>
-__device__ __forceinline__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<true> *hs)
+__device__ __forceinline__ void push_loop(const MainArgs &a, int gw, int nw, float *sy, int32_t *sp, HeavyStage<true> *hs,
+                                          int32_t T, int32_t NT)
 {
     const int lane = lane_id();
-    const int32_t T = a.counters[C_TASKS];
-    const int32_t NT = a.counters[C_NTB];
     const int64_t nchunks = ((int64_t)T + WAVE - 1) / WAVE;
     const int cpw = nchunks >= (int64_t)nw * SLOTS * 2 ? SLOTS : 1;
     for (int64_t u = gw; u * cpw < nchunks; u += nw) {
@@ -1973,19 +1973,30 @@ __device__ __forceinline__ void push_loop(const MainArgs &a, int gw, int nw, flo
             vt[k] = vc[k] && t[k] < T;
             tgt[k] = vc[k] ? (int32_t)(c * WAVE) : 0;
         }
-        wave_search<4>((const int32_t *)a.items, NT, tgt, vc, a0);
-        // lane l holds item a0 + l (the chunk's first task lies in item a0,
-        // and at most 63 further items start inside the chunk): a 6-step
-        // search over the lanes' first tasks finds each lane's item, whose
-        // vector block and block-CSC base come along by shuffles
+        // the search narrows to a window of at most 64 items holding the
+        // chunk's first item; the window and the 64 items after it are then
+        // loaded whole (one round trip for the last search step and the
+        // items), the first item a0 found among them, and lane l takes item
+        // a0 + l (at most 63 further items start inside the chunk) by shuffles
+        int32_t lo[SLOTS];
+        wave_search<4, WAVE>((const int32_t *)a.items, NT, tgt, vc, lo);
         int32_t BJ[SLOTS], Bp[SLOTS];
 #pragma unroll
         for (int k = 0; k < SLOTS; ++k) {
-            const int32_t w = a0[k] + lane;
-            const int4 itm = (vc[k] && w < NT) ? a.items[w] : make_int4(INT_MAX, 0, 0, 0);
-            B[k] = itm.x;
-            BJ[k] = itm.y;
-            Bp[k] = itm.z;
+            const int32_t w0 = lo[k] + lane, w1 = w0 + WAVE;
+            const int4 i0 = (vc[k] && w0 < NT) ? a.items[w0] : make_int4(INT_MAX, 0, 0, 0);
+            const int4 i1 = (vc[k] && w1 < NT) ? a.items[w1] : make_int4(INT_MAX, 0, 0, 0);
+            const uint64_t m = ballot(i0.x <= tgt[k]);  // lane 0 (item lo) is always set for a valid chunk
+            const int L = m ? 63 - __builtin_clzll(m) : 0;
+            a0[k] = lo[k] + L;
+            const int src = (L + lane) & (WAVE - 1);
+            const bool hi = L + lane >= WAVE;
+            const int32_t x0 = __shfl(i0.x, src, WAVE), x1 = __shfl(i1.x, src, WAVE);
+            const int32_t y0 = __shfl(i0.y, src, WAVE), y1 = __shfl(i1.y, src, WAVE);
+            const int32_t z0 = __shfl(i0.z, src, WAVE), z1 = __shfl(i1.z, src, WAVE);
+            B[k] = hi ? x1 : x0;
+            BJ[k] = hi ? y1 : y0;
+            Bp[k] = hi ? z1 : z0;
         }
         int32_t J[SLOTS], p[SLOTS];
 #pragma unroll
@@ -2090,7 +2101,8 @@ struct ActiveLds {
 };
 
 template <int MODE>
-__device__ __forceinline__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rcap, int32_t nr)
+__device__ __forceinline__ void pull_active(const MainArgs &a, ActiveLds &L, int gw, int64_t rcap, int32_t nr,
+                                            int32_t N, int32_t xpop)
 {
     const int lane = lane_id();
     float *sy = (float *)L.acc;
@@ -2123,7 +2135,7 @@ __device__ __forceinline__ void pull_active(const MainArgs &a, ActiveLds &L, int
     // entries then miss); the mask gathers go out with the inline blocks' x
     // gathers and are waited for only once the records' loads are in flight
     constexpr bool MXV = valued<MODE>();
-    const bool mxf = MXV && (int64_t)a.counters[C_XPOP] < 4 * (int64_t)a.counters[C_NZBLK];
+    const bool mxf = MXV && (int64_t)xpop < 4 * (int64_t)N;
     for (uint32_t base = 0; base < cnt;) {
         bool v[SLOTS];
         int32_t slot[SLOTS];
@@ -2300,8 +2312,12 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
             xbw[k] = (cp && i < nwords) ? a.xbits[i] : 0u;
         }
     }
+    // the scan's counts, read together
     const int32_t N = a.counters[C_NZBLK];
     const int32_t path = a.counters[C_PATH];
+    const int32_t xpop = a.counters[C_XPOP];
+    const int32_t T = PATH == PATH_PUSH ? a.counters[C_TASKS] : 0;
+    const int32_t NT = PATH == PATH_PUSH ? a.counters[C_NTB] : 0;
     if (N == 0) return;
     const int w = threadIdx.x >> 6, lane = lane_id();
     if constexpr (PATH == PATH_PUSH) {
@@ -2310,7 +2326,7 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
             int32_t nr;
             const int gw = blockIdx.x * (TPB / WAVE) + w;
             if (a.nreg > 0 && compact_pull(a, N, rcap, nr) && gw < a.nreg)
-                pull_active<MODE>(a, ((ActiveLds *)lds_raw)[w], gw, rcap, nr);
+                pull_active<MODE>(a, ((ActiveLds *)lds_raw)[w], gw, rcap, nr, N, xpop);
             return;
         }
     }
@@ -2326,7 +2342,7 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
     if constexpr (PATH == PATH_PUSH) {
         init_acc();
         wave_lds_sync();
-        push_loop<MODE>(a, gw, nw, sy, sp, &L.hs);
+        push_loop<MODE>(a, gw, nw, sy, sp, &L.hs, T, NT);
     } else {
         // with an eighth or more of the vector blocks active, enough visited
         // blocks are used to load their descriptors together with their block
@@ -2351,7 +2367,7 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
             if constexpr (pull_takes_compaction<MODE>()) {
                 if (compact) {
                     if (gw < a.nreg)
-                        for (int32_t r = gw; r < nr; r += a.nreg) pull_compact<true>(a, r, rcap);
+                        for (int32_t r = gw; r < nr; r += a.nreg) pull_compact<true>(a, r, rcap, N, xpop);
                     return;
                 }
             }
@@ -2885,7 +2901,9 @@ __global__ __launch_bounds__(TPB, 3) void k_fused(MainArgs a, FusedArgs f)
 #pragma unroll
             for (int q = 0; q < SLOTS; ++q) L.acc[q * WAVE + lane] = 0u;
             wave_lds_sync();
-            push_loop<MODE>(a, gw, nw, (float *)L.acc, (int32_t *)L.acc, &L.hs);
+            const int32_t T = __hip_atomic_load(&a.counters[C_TASKS], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const int32_t NT = __hip_atomic_load(&a.counters[C_NTB], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            push_loop<MODE>(a, gw, nw, (float *)L.acc, (int32_t *)L.acc, &L.hs, T, NT);
         } else {
             const bool spec = (int64_t)N * 8 >= (int64_t)a.nbc;
             const int32_t nwords = (a.nbc + 31) >> 5;
