@@ -465,7 +465,8 @@ def profile_cold(args, torch, dbs, wl, dev, ctx, A, points, run):
     bfs = None
     if args.bfs_scale > 0:
         g = wl.rmat(args.bfs_scale, values=False)
-        srcs = wl.bfs_sources(g, args.bfs_sources, key=0)
+        # the first of the bench's BFS sources, so that their bytes match its timed calls
+        srcs = wl.bfs_sources(g, max(16, args.bfs_sources), key=0)[:args.bfs_sources]
         G = dbs.Matrix.from_csr(g.m, g.n, g.row_ptr, g.col_idx, None)
         gctx = dbs.Context(G)
         level = torch.empty(g.n, dtype=torch.int32, device=dev)
