@@ -60,9 +60,9 @@ def test_decode_f32_matrix_dense_activation(torch):
 
 
 # ---------------------------------------------------------------- BFS
-def bfs_check(ctx, A, om, source, policy, label):
+def bfs_check(ctx, A, om, source, policy, label, th3=0.0):
     torch = torch_mod()
-    level, parent, st = ctx.bfs(A, source, policy=policy, stats=True)
+    level, parent, st = ctx.bfs(A, source, policy=policy, th3=th3, stats=True)
     torch.cuda.synchronize()
     el, ep, nl = om.bfs(source)
     gl, gp = level.cpu().numpy(), parent.cpu().numpy()
@@ -139,6 +139,23 @@ def test_bfs_rmat_small(torch):
             st = bfs_check(ctx, A, om, int(s), pol, label)
             if pol == "auto":
                 log(f"  levels={st['levels']} paths={st['path']} frontier={st['frontier']}")
+
+
+def test_bfs_level_selectors(torch):
+    """The default level rule (push iff the push tasks are below a quarter of
+    the blocks) and the paper's rule (th3 > 0) give the same levels and
+    parents; on R-MAT 12 from these sources they also choose differently on
+    some level."""
+    a = wl.rmat(12, values=False)
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    ctx = dbs.Context(A)
+    differ = False
+    for s in wl.bfs_sources(a, 6, key=2):
+        st0 = bfs_check(ctx, A, om, int(s), "auto", f"bfs rmat12 src={s} task rule")
+        st1 = bfs_check(ctx, A, om, int(s), "auto", f"bfs rmat12 src={s} paper rule", th3=0.01)
+        log(f"  src={s} task rule {st0['path']} / paper rule {st1['path']}")
+        differ |= st0["path"] != st1["path"]
+    assert differ, "the two level rules chose the same paths everywhere"
 
 
 def test_bfs_and_spmspv_share_a_context(torch):
