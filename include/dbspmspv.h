@@ -72,7 +72,11 @@ typedef enum { DBS_PATH_AUTO = 0, DBS_PATH_PUSH = 1, DBS_PATH_PULL = 2 } dbs_pat
  * leave little for push (1-10% of the blocks as tasks) but pull still
  * walks every segment: push measured 2-4x faster there, and pull faster
  * from about 60% of the blocks as tasks on.  An explicit th3 > 0 gives the
- * paper's rule for BFS too.                                                */
+ * paper's rule for BFS too.
+ * Dense activations (dbs_spmspv_dense) on a matrix without COO blocks (a
+ * decode layer) take pull under the default selector: push would win only
+ * below about 1% active vector blocks, while launching its kernel for the
+ * device's choice costs every call 2-4 us (of about 25 per call).         */
 #define DBS_TH3_DEFAULT 0.01f
 #define DBS_TH3_PAPER 0.01f
 #define DBS_TH3_SPREAD 0.12f
@@ -363,6 +367,8 @@ dbs_status dbs_spmspv_noalloc(const dbs_matrix *A, dbs_semiring sr, int32_t x_nn
  * (Sec. 4.1).  d_y_dense receives all m outputs in A's dtype (rows with no
  * active product are 0), rounded to nearest even from the fp64 sum.
  * d_y_f32 (NULL allowed) receives the same sums rounded to fp32.
+ * path AUTO with th3 <= 0 on a matrix without COO blocks takes pull (see
+ * DBS_TH3_DEFAULT); th3 > 0 applies the paper's rule on the device.
  * F32 and F16 matrices only.                                               */
 dbs_status dbs_spmspv_dense(dbs_ctx *ctx, const dbs_matrix *A, const void *d_x_dense,
                             dbs_path path, float th3, void *d_y_dense, float *d_y_f32,

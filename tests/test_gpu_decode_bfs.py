@@ -40,6 +40,29 @@ def test_decode_small(torch, shape):
             check_decode(ctx, A, om, a16, p, label)
 
 
+def test_decode_selector(torch):
+    """A decode layer (no COO blocks) with one active vector block: the
+    default selector takes pull without a push launch, th3 > 0 the paper's
+    rule (push below th3 N_blk); both match the oracle."""
+    out_f, in_f = 64, 4096
+    w = wl.decode_layer(out_f, in_f)
+    A, om = gpu_matrix(w), oracle_matrix(w)
+    assert A.info()["blocks_by_type"].get("COO", 0) == 0
+    ctx = dbs.Context(A)
+    a16 = np.zeros(in_f, dtype=np.float16)
+    a16[[37, 40]] = np.float16(0.75)  # one vector block of 256
+    for th3, want in ((0.0, "pull"), (0.01, "push")):
+        x = to_dev(a16)
+        torch_ = torch_mod()
+        y32 = torch_.empty(out_f, dtype=torch_.float32, device="cuda:0")
+        y, st = ctx.spmspv_dense(A, x, th3=th3, y32=y32, stats=True)
+        torch_.cuda.synchronize()
+        log(f"decode selector th3={th3}: {st['path']}")
+        assert st["path"] == want, (th3, st)
+        y64, S, _ = oracle.decode_linear(om, a16)
+        assert oracle.within_tol(y32.cpu().numpy(), y64, S, REL_TOL).all()
+
+
 def test_decode_f32_matrix_dense_activation(torch):
     a = wl.random_csr(150, 260, 0.4, key=(41, 0))
     A, om = gpu_matrix(a), oracle_matrix(a)
