@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <mutex>
 #include <cstring>
 #include <new>
@@ -526,11 +527,17 @@ dbs_status spmspv_launches(const dbs_matrix *A, DevCtx &c, hipStream_t s, int mo
     // kernel is launched.
     int launch_path = (int)path;
     if (path == DBS_PATH_AUTO) {
-        // (the spread rule can take push up to its own threshold)
+        // (the spread rule can take push up to its own threshold: push when
+        // N_nzblk < lim_s and the k distinct indices number fewer than 2 N_nzblk)
         const double lim = (double)norm_th3(th3) * (double)A->d.nbc;
-        const double lim_any = std::max(lim, spread_th3(th3) * (double)A->d.nbc);
+        const double lim_s = spread_th3(th3) * (double)A->d.nbc;
+        const double lim_any = std::max(lim, lim_s);
+        const int64_t nlo = (x_nnz + 15) / 16, nhi = std::min<int64_t>(x_nnz, A->d.nbc);
+        // the smallest N_nzblk the paper's rule leaves to pull
+        const int64_t a = std::max<int64_t>(nlo, (int64_t)std::ceil(lim));
         if ((double)x_nnz < lim) launch_path = DBS_PATH_PUSH;
-        else if ((double)((x_nnz + 15) / 16) >= lim_any) launch_path = DBS_PATH_PULL;
+        else if ((double)nlo >= lim_any) launch_path = DBS_PATH_PULL;
+        else if ((double)nhi < lim_s && 2 * a > x_nnz) launch_path = DBS_PATH_PUSH;  // spread for every such N
     }
     dbs_status st;
     if (small_x_fits(A->d, (int32_t)x_nnz)) {
