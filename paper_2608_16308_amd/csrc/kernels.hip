@@ -1542,15 +1542,39 @@ __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L, const 
                 for (int b = 0; b < NB; ++b) sum[b] = 0.0;
                 int32_t pm = INT_MAX;
                 uint32_t run = 0;
-                for (int cc = c; cc < Y::NQ && (int32_t)L[Y::CR + cc] == Rc; ++cc) {
-                    const uint32_t hm = L[Y::HM + cc];
-                    run |= hm;
-                    if ((hm >> rr) & 1u) {
+                // the run's chunks CG at a time, their LDS reads issued together
+                constexpr int CG = NB == 1 ? 4 : 1;
+                bool in = true;
+                for (int c0 = c; in && c0 < Y::NQ; c0 += CG) {
+                    int32_t crs[CG];
+                    uint32_t hms[CG];
+                    double vs[NB][CG];
+                    int32_t pms[CG];
+#pragma unroll
+                    for (int j = 0; j < CG; ++j) {
+                        const int cc = c0 + j;
+                        const bool ok = cc < Y::NQ;
+                        crs[j] = ok ? (int32_t)L[Y::CR + cc] : -1;
+                        hms[j] = ok ? L[Y::HM + cc] : 0u;
                         if constexpr (valued<MODE>()) {
 #pragma unroll
-                            for (int b = 0; b < NB; ++b) sum[b] += acc[(b * Y::NQ + cc) * 16 + rr];
+                            for (int b = 0; b < NB; ++b) vs[b][j] = ok ? acc[(b * Y::NQ + cc) * 16 + rr] : 0.0;
                         } else {
-                            pm = min(pm, pacc[cc * 16 + rr]);
+                            pms[j] = ok ? pacc[cc * 16 + rr] : INT_MAX;
+                        }
+                    }
+#pragma unroll
+                    for (int j = 0; j < CG; ++j) {
+                        in = in && crs[j] == Rc;
+                        if (!in) break;
+                        run |= hms[j];
+                        if ((hms[j] >> rr) & 1u) {
+                            if constexpr (valued<MODE>()) {
+#pragma unroll
+                                for (int b = 0; b < NB; ++b) sum[b] += vs[b][j];
+                            } else {
+                                pm = min(pm, pms[j]);
+                            }
                         }
                     }
                 }
