@@ -6,7 +6,8 @@
 //   k_scan                single-pass look-back scan over vector blocks: the
 //                         list of nonzero vector blocks, N_nzblk, the push
 //                         task offsets, and the global push/pull choice
-//                         s_b = N_nzblk / N_blk < th3 (Sec. 3.3.1)
+//                         s_b = N_nzblk / N_blk < th3 (Sec. 3.3.1; BFS levels:
+//                         the push task count against a share of the blocks)
 //   (k_small_x            both of the above in one workgroup, for short index
 //                         lists)
 //   k_traverse            pull (weighted row-block segments, or below an
@@ -1261,10 +1262,6 @@ __device__ __forceinline__ void row_values(const uint8_t *vals, bool colview, co
     }
 }
 
-// NB > 1 (valued modes): NB vectors at once (batched decoding): the blocks
-// active for any of them are visited, each row value is loaded once and
-// multiplied with the NB dense x (zeros where a vector has no entry), and
-// the NB sums go to NB accumulator sets (x and accumulators NB-strided).
 // A round's chunk bounds and block row for thread t (chunk c0 + t / 16 of
 // the round starting at chunk c0), so that a caller can issue the first
 // round's loads before anything else it waits for.
@@ -1284,6 +1281,10 @@ __device__ __forceinline__ RowsPre rows_pre(const MainArgs &a, int64_t c0)
     return p;
 }
 
+// NB > 1 (valued modes): NB vectors at once (batched decoding): the blocks
+// active for any of them are visited, each row value is loaded once and
+// multiplied with the NB dense x (zeros where a vector has no entry), and
+// the NB sums go to NB accumulator sets (x and accumulators NB-strided).
 template <int MODE, bool LDSBITS, int NB = 1>
 __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L, const RowsPre *first = nullptr)
 {
