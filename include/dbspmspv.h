@@ -67,12 +67,13 @@ typedef enum { DBS_PATH_AUTO = 0, DBS_PATH_PUSH = 1, DBS_PATH_PULL = 2 } dbs_pat
  * BFS levels (dbs_bfs) with the default th3 take push iff the level's push
  * tasks -- the blocks in the block-CSC lists of the frontier's nonzero
  * vector blocks, which the scan sums anyway -- are fewer than
- * DBS_BFS_PUSH_TASKS * nblk.  On R-MAT 22 the paper's rule takes pull on
- * the levels after the largest one (s_b 0.1-0.5), where the visited rows
- * leave little for push (1-10% of the blocks as tasks) but pull still
- * walks every segment: push measured 2-4x faster there, and pull faster
- * from about 60% of the blocks as tasks on.  An explicit th3 > 0 gives the
- * paper's rule for BFS too.
+ * DBS_BFS_PUSH_TASKS * nblk.  On R-MAT 22 the frontier's vector blocks stay
+ * many (s_b 0.1-0.5) after the largest level, so the paper's rule keeps
+ * pull there, while the visited rows leave push 1-10% of the blocks as
+ * tasks; pull skips the block rows without unvisited rows, and the two
+ * cross at a few percent of the blocks as tasks (whole BFS: the same mean
+ * time within 1% for thresholds of 0.02-0.1 of nblk, 14% slower at 0.25).
+ * An explicit th3 > 0 gives the paper's rule for BFS too.
  * Dense activations (dbs_spmspv_dense) on a matrix without COO blocks (a
  * decode layer) take pull under the default selector: push would win only
  * below about 1% active vector blocks, while launching its kernel for the
@@ -80,7 +81,7 @@ typedef enum { DBS_PATH_AUTO = 0, DBS_PATH_PUSH = 1, DBS_PATH_PULL = 2 } dbs_pat
 #define DBS_TH3_DEFAULT 0.01f
 #define DBS_TH3_PAPER 0.01f
 #define DBS_TH3_SPREAD 0.12f
-#define DBS_BFS_PUSH_TASKS 0.25f
+#define DBS_BFS_PUSH_TASKS 0.1f
 
 /* Low-level block formats (Sec. 3.2.1). */
 typedef enum {
@@ -406,7 +407,10 @@ typedef struct {
  * pull is chosen per level on the device: by the push task count with the
  * default th3 (DBS_BFS_PUSH_TASKS), by the paper's rule for th3 > 0, or
  * forced by policy.
- * Edge u -> v iff A[v][u] is stored; A must be square.
+ * Edge u -> v iff A[v][u] is stored; A must be square.  A matrix built
+ * from CSR on the host also carries which rows hold entries: BFS counts the
+ * others as visited from the start (no edge reaches them), so that pull
+ * levels skip their block rows sooner; the results are the same.
  *   d_level[n]   level of each vertex, -1 if unreachable, level[source] = 0
  *   d_parent[n]  smallest-id vertex of the previous level with an edge to v;
  *                parent[source] = source; -1 if unreachable

@@ -267,7 +267,8 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
         (s2 = dev_upload(A->allocs, hv_cstart, &d.hv_cstart)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, hv_crow, &d.hv_crow)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->payload, &d.pay, 16)) != DBS_OK ||
-        (s2 = dev_upload(A->allocs, task_order, &d.task_order)) != DBS_OK) {
+        (s2 = dev_upload(A->allocs, task_order, &d.task_order)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, h->row_occ, &d.row_occ)) != DBS_OK) {
         free_all(A->allocs);
         delete A;
         return s2;

@@ -416,6 +416,11 @@ extern "C" dbs_status dbs_host_build_csr(int32_t m, int32_t n, int64_t nnz, cons
             for (int ty = 0; ty < DBS_NUM_BLOCK_TYPES; ++ty) h->by_type[ty] += a[ty];
         h->rb_ptr.resize(nbr + 1);
         for (int32_t R = 0; R <= nbr; ++R) h->rb_ptr[R] = (int32_t)rb_nblk[R];
+        // row i is bit i % 16 of block row i / 16's mask, i.e. bit i % 32 of
+        // word i / 32
+        h->row_occ.assign((size_t)(nbr + 1) / 2, 0u);
+        for (int32_t i = 0; i < m; ++i)
+            if (row_ptr[i + 1] > row_ptr[i]) h->row_occ[(size_t)(i >> 5)] |= 1u << (i & 31);
         h->cb_col.resize(nblk);
         h->desc.resize(nblk);
         h->seg.resize(h->nseg);

@@ -26,6 +26,9 @@ struct dbs_host_matrix {
     std::vector<int32_t> csc2csr;  // nblk
     std::vector<uint64_t> desc;    // nblk
     std::vector<uint64_t> seg;     // nseg
+    // (nbr + 1) / 2 words, a 16-bit mask per block row (two per word): the
+    // rows that hold at least one entry
+    std::vector<uint32_t> row_occ;
     std::vector<uint8_t> payload;
 };
 

@@ -1641,13 +1641,52 @@ __device__ __forceinline__ void pull_loop(const MainArgs &a, int gw, int nw, flo
         G = G < 1 ? 1 : (G > GMAX ? GMAX : G);
         ntask = (nseg + G * W - 1) / (G * W);
     }
+    // Boolean modes with an output mask and one 16-segment iteration per
+    // task (BFS levels, masked OR-AND calls): a wave first reads the block
+    // rows of the segments of its next PRE_TASKS tasks and their admitted
+    // rows, four consecutive segments per lane (lane 4 j + p: segments
+    // 4 p .. 4 p + 3 of the j-th task), and then skips the tasks none of whose
+    // rows is admitted without reading their slots; in the other tasks a
+    // segment without admitted rows reads no slot.  Once most rows have been
+    // reached (the BFS levels after the largest), most segments belong to
+    // such block rows.
+    constexpr int32_t PRE_TASKS = WAVE / 4;
+    const bool pre = !valued<MODE>() && a.omask != nullptr && !ordered && G == 1 && spq == SLOTS;
+    uint32_t pre_am01 = 0u, pre_am23 = 0u;  // admitted rows of the lane's segments, two per word
+    uint64_t pre_live = 0ull;               // bit 4 j + p: one of lane 4 j + p's segments has some
     // ordered tasks are dealt out by rank in snake order: round j gives rank
     // j nw + nw - 1 - gw to wave gw for even j and j nw + gw for odd j (the
     // first workgroups also take the first chunks of the non-COO pass);
     // tasks in segment order grid-stride
     for (int32_t r0 = 0; r0 < ntask; r0 += nw) {
+        const int32_t pj = (r0 / nw) % PRE_TASKS;
+        if (pre && pj == 0) {
+            const int32_t rj = r0 + (lane >> 2) * nw + gw;
+            const int64_t sid = (int64_t)rj * 16 + (lane & 3) * 4;
+            uint32_t rs[4] = {0u, 0u, 0u, 0u};
+            if (rj < ntask) {
+                if (sid + 4 <= nseg) {
+                    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+                    const u32x4 v = __builtin_nontemporal_load((const u32x4 *)(a.seg_rs + sid));
+                    rs[0] = v.x;
+                    rs[1] = v.y;
+                    rs[2] = v.z;
+                    rs[3] = v.w;
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) rs[k] = sid + k < nseg ? a.seg_rs[sid + k] : 0u;
+                }
+            }
+            uint32_t am4[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) am4[k] = (rj < ntask && sid + k < nseg) ? row_admit(a, (int32_t)rs[k]) : 0u;
+            pre_am01 = am4[0] | (am4[1] << 16);
+            pre_am23 = am4[2] | (am4[3] << 16);
+            pre_live = ballot((pre_am01 | pre_am23) != 0u);
+        }
         const int32_t r = r0 + ((!ordered || ((r0 / nw) & 1)) ? gw : nw - 1 - gw);
         if (r >= ntask) continue;
+        if (pre && ((pre_live >> (pj * 4)) & 0xFull) == 0ull) continue;
         const int32_t task = ordered ? a.torder[r] : r;
         const int32_t ts = task * G * W + q * spq;
         // the open run of the quarter: its block row, lane i's share of row
@@ -1674,22 +1713,34 @@ __device__ __forceinline__ void pull_loop(const MainArgs &a, int gw, int nw, flo
             // segment word, block column and (spec) descriptor: independent
             // loads, non-temporal (each slot is read once per call), so that
             // the stream does not push x out of the L2
+            uint32_t a01 = 0u, a23 = 0u;
+            if (pre) {
+                a01 = (uint32_t)__shfl((int)pre_am01, pj * 4 + q, WAVE);
+                a23 = (uint32_t)__shfl((int)pre_am23, pj * 4 + q, WAVE);
+            }
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k) {
                 const int32_t sid = ts + it * W + k;
                 vs[k] = k < spq && sid < nseg;
+                bool live = vs[k];
                 s[k] = vs[k] ? __builtin_nontemporal_load(&a.seg_rs[sid]) : 0u;
+                if (pre) {
+                    // segment 4 q + k of the task: lane 4 pj + q above, its k-th
+                    const uint32_t w2 = k < 2 ? a01 : a23;
+                    am[k] = (k & 1) ? (w2 >> 16) : (w2 & 0xFFFFu);
+                    live = live && am[k] != 0u;
+                }
                 b[k] = sid * 16 + i;
-                const int32_t w = vs[k] ? __builtin_nontemporal_load(&a.sl_col[b[k]]) : SLOT_PAD;
+                const int32_t w = live ? __builtin_nontemporal_load(&a.sl_col[b[k]]) : SLOT_PAD;
                 J[k] = w >= 0 ? slot_col(w) : -1;
-                d[k] = (vs[k] && spec) ? __builtin_nontemporal_load(&a.sl_desc[b[k]]) : 0ull;
+                d[k] = (live && spec) ? __builtin_nontemporal_load(&a.sl_desc[b[k]]) : 0ull;
             }
             // block activity: the LDS bitmap when it fits, else the
             // vector-block mask (gathered here then, and kept for the
             // whole-wave blocks)
 #pragma unroll
             for (int k = 0; k < SLOTS; ++k) {
-                am[k] = vs[k] ? row_admit(a, (int32_t)s[k]) : 0u;
+                if (!pre) am[k] = vs[k] ? row_admit(a, (int32_t)s[k]) : 0u;
                 act[k] = J[k] >= 0 && am[k] != 0;
                 if constexpr (LDSBITS) act[k] = act[k] && block_active(J[k]);
             }
@@ -2656,6 +2707,7 @@ __global__ __launch_bounds__(TPB) void k_bfs_init(int32_t n, int32_t source, int
                                                   uint32_t *__restrict__ visited,
                                                   uint32_t *__restrict__ nextm,
                                                   uint32_t *__restrict__ xmask, int32_t nwords,
+                                                  const uint32_t *__restrict__ row_occ,
                                                   int32_t *__restrict__ counters)
 {
     const int64_t stride = (int64_t)gridDim.x * TPB;
@@ -2665,8 +2717,11 @@ __global__ __launch_bounds__(TPB) void k_bfs_init(int32_t n, int32_t source, int
     }
     const int32_t sw = source >> 5;
     const uint32_t sb = 1u << (source & 31);
+    // rows without entries start as visited (no edge reaches them; their
+    // level and parent stay unset): the output mask of every level then
+    // excludes them
     for (int64_t w = (int64_t)blockIdx.x * TPB + threadIdx.x; w < nwords; w += stride) {
-        visited[w] = w == sw ? sb : 0u;
+        visited[w] = (row_occ ? ~row_occ[w] : 0u) | (w == sw ? sb : 0u);
         xmask[w] = w == sw ? sb : 0u;
         nextm[w] = 0u;
     }
@@ -3440,7 +3495,7 @@ hipError_t launch_bfs_init(const DevMatrix &A, const DevCtx &C, int32_t source, 
     int32_t nwords = (A.nbr + 1) / 2;
     dim3 g(grid_for(A.n, TPB, 4096)), b(TPB);
     hipLaunchKernelGGL(k_bfs_init, g, b, 0, s, A.n, source, level, parent, C.visited, C.nextm, C.xmask, nwords,
-                       C.counters);
+                       A.row_occ, C.counters);
     return hipGetLastError();
 }
 

@@ -41,6 +41,12 @@ struct DevMatrix {
     // order, as for a matrix converted on the device).
     const int32_t *task_order = nullptr;
     int32_t ntask = 0;
+    // The rows that hold entries, a 16-bit mask per block row, two per word
+    // ((nbr + 1) / 2 words; NULL when not known, as for a matrix converted
+    // on the device).  BFS counts the other rows as reached from the start:
+    // no edge leads to them, and the pull levels then skip whole block rows
+    // sooner.
+    const uint32_t *row_occ = nullptr;
 };
 
 // Segments per segment-loop task: two wave iterations of 16 segments.

@@ -159,3 +159,30 @@ def test_converted_matrix_spmspv_and_decode(torch):
         y64, S, y16 = oracle.decode_linear(omw, a16)
         assert f16_ulp_dist(y.cpu().numpy(), y16).max() <= 1
         assert oracle.within_tol(y32.cpu().numpy(), y64, S, REL_TOL).all()
+
+
+def test_converted_matrix_bfs(torch):
+    # BFS on a device-converted matrix (no row-occupancy bitmap: no row
+    # starts as reached) and on the host build of the same matrix (rows
+    # without entries start as reached): both equal the oracle
+    a0 = wl.random_csr(3000, 3000, 0.0015, key=(74, 0))
+    d = dense_of(a0, np.float32)
+    d[100:400, :] = 0.0  # block rows without entries and partly empty ones
+    d[1000:1016:3, :] = 0.0
+    Ag, a, _ = convert_and_compare(torch, d, "bfs matrix")
+    Ah = dbs.Matrix.from_csr(a.m, a.n, a.row_ptr, a.col_idx, a.vals)
+    om = oracle_matrix(a)
+    rows_empty = np.nonzero(np.diff(a.row_ptr) == 0)[0]
+    rng = wl.rng_for(wl.W_RAND, 74, 1)
+    sources = [int(rows_empty[0]), int(rows_empty[-1])] + [int(s) for s in rng.choice(a.n, 4, replace=False)]
+    for name, A in (("converted", Ag), ("host", Ah)):
+        ctx = dbs.Context(A)
+        for s in sources:
+            el, ep, nl = om.bfs(s)
+            for policy in ("auto", "push", "pull"):
+                log(f"{name} bfs source={s} policy={policy}")
+                level, parent, st = ctx.bfs(A, s, policy=policy, stats=True)
+                torch.cuda.synchronize()
+                assert np.array_equal(level.cpu().numpy(), el), (name, s, policy)
+                assert np.array_equal(parent.cpu().numpy(), ep), (name, s, policy)
+                assert st["levels"] == nl

@@ -113,6 +113,21 @@ def test_rmat20_or_and(rmat20):
             label = f"rmat20 or_and masked d={d} path={p}"
             log(label)
             check_spmspv(ctx, A, om, a, xi, None, path=p, mask=mw, complement=True, semiring="or_and", label=label)
+    # masks that exclude whole 16-row blocks (85% of them) and half of the
+    # rows of the others: the pull's segment loop skips the segments and
+    # tasks whose block row has no admitted row; uncomplemented too
+    blk = np.repeat(rng.random((a.m + 15) // 16) < 0.85, 16)[:a.m]
+    bits2 = blk | (rng.random(a.m) < 0.5)
+    mw2 = mask_words(bits2)
+    for d in (1e-2, 0.3):
+        xi, _ = wl.sparse_x(a.n, d, "uniform", key=(52, int(d * 1e4)))
+        for p in ("auto", "push", "pull"):
+            label = f"rmat20 or_and block-row mask d={d} path={p}"
+            log(label)
+            check_spmspv(ctx, A, om, a, xi, None, path=p, mask=mw2, complement=True, semiring="or_and", label=label)
+        label = f"rmat20 or_and block-row mask (kept rows) d={d}"
+        log(label)
+        check_spmspv(ctx, A, om, a, xi, None, path="pull", mask=mask_words(~bits2), semiring="or_and", label=label)
 
 
 # ------------------------------------------------------------------ R-MAT 22 BFS
