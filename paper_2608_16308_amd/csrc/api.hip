@@ -718,8 +718,9 @@ extern "C" dbs_status dbs_bfs(dbs_ctx *ctx, const dbs_matrix *A, int32_t source,
             return st;
         }
         const int32_t *h = ctx->h_counters;
+        // the scan's mask popcount is the frontier size
         if (level > 0) {
-            frontier = h[C_FRONTIER];
+            frontier = h[C_XPOP];
             reached += frontier;
         }
         if (h[C_NZBLK] == 0) break;

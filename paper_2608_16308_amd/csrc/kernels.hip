@@ -2373,8 +2373,6 @@ __global__ __launch_bounds__(TPB, PATH == PATH_PULL ? 4 : 1) void k_traverse(Mai
 {
     __shared__ __align__(16) uint8_t lds_raw[traverse_lds_bytes<MODE, PATH>()];
     WaveLds<PATH == PATH_PUSH> *lds = (WaveLds<PATH == PATH_PUSH> *)lds_raw;
-    // BFS: the host has read the frontier size of this level; restart the count
-    if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
     // pull: the first activity bitmap words this thread copies into LDS go
     // out with the device choice (they do not depend on it)
     const int32_t nwords = (a.nbc + 31) >> 5;
@@ -2470,8 +2468,6 @@ template <int MODE, int NB>
 __global__ __launch_bounds__(TPB) void k_rows(MainArgs a)
 {
     __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE, NB>::WORDS];
-    // BFS: the host has read the frontier size of this level; restart the count
-    if (MODE == M_BFS && blockIdx.x == 0 && threadIdx.x == 0) a.counters[C_FRONTIER] = 0;
     // the first round's chunk bounds and the first bitmap words go out with
     // the device choice (the loads do not depend on it)
     const RowsPre first = rows_pre(a, (int64_t)blockIdx.x * a.cpw);
@@ -2711,6 +2707,8 @@ __global__ __launch_bounds__(TPB) void k_bfs_init(int32_t n, int32_t source, int
                                                   int32_t *__restrict__ counters)
 {
     const int64_t stride = (int64_t)gridDim.x * TPB;
+    // the first scan sums the mask popcounts here
+    if (blockIdx.x == 0 && threadIdx.x == 0) counters[C_XPOP] = 0;
     for (int64_t v = (int64_t)blockIdx.x * TPB + threadIdx.x; v < n; v += stride) {
         level[v] = v == source ? 0 : -1;
         parent[v] = v == source ? source : INT_MAX;
@@ -2728,34 +2726,32 @@ __global__ __launch_bounds__(TPB) void k_bfs_init(int32_t n, int32_t source, int
 }
 
 // Next frontier -> current frontier masks, visited |= next, level of the
-// newly reached vertices, frontier size.
-__global__ __launch_bounds__(TPB) void k_bfs_update(int32_t nwords, int32_t next_level,
+// newly reached vertices.  A thread per vertex, so that the level writes of
+// a wave are coalesced; the first thread of each 32 vertices updates their
+// mask words (the 32 threads read the word before it is cleared: one wave,
+// program order).  The frontier size is the next scan's mask popcount
+// (C_XPOP): a count here would take an atomic per wave on one counter, and
+// same-address atomics serialize.
+__global__ __launch_bounds__(TPB) void k_bfs_update(int32_t n, int32_t nwords, int32_t next_level,
                                                     int32_t *__restrict__ level,
                                                     uint32_t *__restrict__ visited,
                                                     uint32_t *__restrict__ nextm,
                                                     uint32_t *__restrict__ xmask,
                                                     int32_t *__restrict__ counters)
 {
-    int32_t w = blockIdx.x * TPB + threadIdx.x;
-    uint32_t cnt = 0;
-    // the scan's entry count is not used by BFS
-    if (w == 0) counters[C_XPOP] = 0;
-    if (w < nwords) {
-        uint32_t nm = nextm[w];
+    const int64_t v = (int64_t)blockIdx.x * TPB + threadIdx.x;
+    const int64_t w = v >> 5;
+    // the next scan sums the mask popcounts here
+    if (v == 0) counters[C_XPOP] = 0;
+    const uint32_t nm = (v < n && w < nwords) ? nextm[w] : 0u;
+    if ((nm >> (v & 31)) & 1u) level[v] = next_level;
+    if ((v & 31) == 0 && v < n && w < nwords) {
         xmask[w] = nm;
         if (nm) {
             visited[w] |= nm;
             nextm[w] = 0u;
-            cnt = __popc(nm);
-            while (nm) {
-                int b = ctz32(nm);
-                nm &= nm - 1;
-                level[(int64_t)w * 32 + b] = next_level;
-            }
         }
     }
-    const uint32_t tot = wave_sum(cnt);
-    if (lane_id() == 0 && tot) atomicAdd(&counters[C_FRONTIER], (int32_t)tot);
 }
 
 __global__ __launch_bounds__(TPB) void k_bfs_finish(int32_t n, int32_t *__restrict__ parent)
@@ -3503,8 +3499,10 @@ hipError_t launch_bfs_update(const DevMatrix &A, const DevCtx &C, int32_t next_l
                              hipStream_t s)
 {
     int32_t nwords = (A.nbr + 1) / 2;
-    dim3 g(grid_for(nwords, TPB, INT_MAX)), b(TPB);
-    hipLaunchKernelGGL(k_bfs_update, g, b, 0, s, nwords, next_level, level, C.visited, C.nextm, C.xmask,
+    // (every mask word holds some row below n: the last one holds block row
+    // nbr - 1, whose first row is below m = n)
+    dim3 g(grid_for(A.n, TPB, INT_MAX)), b(TPB);
+    hipLaunchKernelGGL(k_bfs_update, g, b, 0, s, A.n, nwords, next_level, level, C.visited, C.nextm, C.xmask,
                        C.counters);
     return hipGetLastError();
 }

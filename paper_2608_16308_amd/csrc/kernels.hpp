@@ -60,7 +60,7 @@ enum Counter : int {
     C_YNNZ = 3,      // entries written to y
     C_XBAD = 4,      // x indices out of range, counted by the blocker during this call
     C_ERR_LAST = 5,  // error bits of the last completed call
-    C_FRONTIER = 6,  // BFS: vertices in the next frontier
+    // (6: unused)
     C_NZACC = 7,     // nonzero vector blocks, summed by the scan tiles (consumed by its last tile)
     C_NTB = 8,       // push work items (nonzero vector blocks with a nonempty block column)
     C_XPOP = 9,      // distinct x indices (mask popcounts), summed by the scan tiles
