@@ -618,15 +618,22 @@ extern "C" dbs_status dbs_spmspv_dense(dbs_ctx *ctx, const dbs_matrix *A, const 
     // choice (see DBS_TH3_DEFAULT)
     int p = (int)path;
     if (p == DBS_PATH_AUTO && !(th3 > 0.f) && A->d.nblk > 0 && A->d.nheavy == A->d.nblk) p = DBS_PATH_PULL;
-    if (scan_takes_dense(A->d, d_x_dense)) {
-        LAUNCH(ctx, DBS_K_SCAN,
-               launch_scan_dense(A->d, ctx->c, mode, d_x_dense, p, (double)norm_th3(th3), spread_th3(th3), s));
+    if (p == DBS_PATH_PULL && rows_dx_fits(A->d, d_x_dense)) {
+        // pull known on the host: the non-COO pass reads the activation
+        // itself, without a scan
+        LAUNCH(ctx, DBS_K_MAIN, launch_rows_dx(A->d, ctx->c, mode, d_x_dense, s));
+        LAUNCH(ctx, DBS_K_FINALIZE, launch_finalize_dense(A->d, ctx->c, mode, d_y_dense, d_y_f32, s, false));
     } else {
-        LAUNCH(ctx, DBS_K_SCATTER, launch_ballot(A->d, ctx->c, mode, d_x_dense, s));
-        LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, p, (double)norm_th3(th3), spread_th3(th3), s));
+        if (scan_takes_dense(A->d, d_x_dense)) {
+            LAUNCH(ctx, DBS_K_SCAN,
+                   launch_scan_dense(A->d, ctx->c, mode, d_x_dense, p, (double)norm_th3(th3), spread_th3(th3), s));
+        } else {
+            LAUNCH(ctx, DBS_K_SCATTER, launch_ballot(A->d, ctx->c, mode, d_x_dense, s));
+            LAUNCH(ctx, DBS_K_SCAN, launch_scan(A->d, ctx->c, p, (double)norm_th3(th3), spread_th3(th3), s));
+        }
+        LAUNCH(ctx, DBS_K_MAIN, launch_main(A->d, ctx->c, mode, ctx->c.xd, nullptr, 0, nullptr, p, s));
+        LAUNCH(ctx, DBS_K_FINALIZE, launch_finalize_dense(A->d, ctx->c, mode, d_y_dense, d_y_f32, s));
     }
-    LAUNCH(ctx, DBS_K_MAIN, launch_main(A->d, ctx->c, mode, ctx->c.xd, nullptr, 0, nullptr, p, s));
-    LAUNCH(ctx, DBS_K_FINALIZE, launch_finalize_dense(A->d, ctx->c, mode, d_y_dense, d_y_f32, s));
     if (stats) {
         if ((st = sync_counters(ctx)) != DBS_OK) return st;
         const int32_t *h = ctx->h_counters;

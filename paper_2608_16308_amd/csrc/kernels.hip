@@ -1285,7 +1285,9 @@ __device__ __forceinline__ RowsPre rows_pre(const MainArgs &a, int64_t c0)
 // active for any of them are visited, each row value is loaded once and
 // multiplied with the NB dense x (zeros where a vector has no entry), and
 // the NB sums go to NB accumulator sets (x and accumulators NB-strided).
-template <int MODE, bool LDSBITS, int NB = 1>
+// XL: the vector-block masks come from an LDS table (16 bits per vector
+// block, after the activity bitmap: see k_rows_dx) instead of xmask.
+template <int MODE, bool LDSBITS, int NB = 1, bool XL = false>
 __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L, const RowsPre *first = nullptr)
 {
     using Y = RowsLds<MODE, NB>;
@@ -1309,7 +1311,9 @@ __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L, const 
         const int32_t J = act ? a.hv_col[h] : 0;
         const uint64_t d = act ? a.hv_desc[h] : 0ull;
         if constexpr (LDSBITS) act = act && block_active(J);
-        const uint32_t mx = act ? mask16(a.xmask, J) : 0u;
+        uint32_t mx = 0u;
+        if constexpr (XL) mx = act ? (uint32_t)((const uint16_t *)(lds_bits + ((a.nbc + 31) >> 5)))[J] : 0u;
+        else mx = act ? mask16(a.xmask, J) : 0u;
         // with the activity bitmap in LDS an active block's mask is nonzero,
         // so its header loads go out with the mask's
         if constexpr (!LDSBITS) act = act && mx != 0;
@@ -2486,6 +2490,83 @@ __global__ __launch_bounds__(TPB) void k_rows(MainArgs a)
     }
 }
 
+// Dense activation on a matrix without COO blocks (decoding) with the path
+// known to be pull: the non-COO pass reads the activation itself, with no
+// scan before it.  Each workgroup first forms the 16-bit mask of every vector
+// block (an entry is present iff it is nonzero, -0 included as zero, as in
+// the scan) from the activation into an LDS table after the activity bitmap,
+// and both in LDS; the blocks' x words are then the activation's own (the
+// masks select the products), and nothing of the context's x scratch is
+// written, so the y conversion after it restores none.  Workgroup 0 also
+// records N_nzblk and the path for the call's statistics.
+// The table takes (nbc + 1) / 2 words of dynamic LDS: ROWS_DX_MAX_NBC vector
+// blocks at most.
+constexpr int32_t ROWS_DX_MAX_NBC = 4096;
+template <int MODE>
+__global__ __launch_bounds__(TPB) void k_rows_dx(MainArgs a)
+{
+    __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE, 1>::WORDS];
+    const RowsPre first = rows_pre(a, (int64_t)blockIdx.x * a.cpw);
+    const int32_t nbc = a.nbc, nwords = (nbc + 31) >> 5;
+    uint16_t *lmask = (uint16_t *)(lds_bits + nwords);
+    const int t0 = threadIdx.x, lane = lane_id();
+    constexpr int PER = MODE == M_F16 ? 8 : 4;  // entries per 16 bytes
+    uint32_t cnt = 0;
+    // four vector blocks per thread and pass, their loads issued together
+    constexpr int XB = 4;
+    for (int32_t base = 0; base < nbc; base += XB * TPB) {
+        uint4 v[XB][16 / PER];
+#pragma unroll
+        for (int b = 0; b < XB; ++b) {
+            const int32_t J = base + b * TPB + t0;
+            const uint4 *src = (const uint4 *)a.xd + (int64_t)J * (16 / PER);
+#pragma unroll
+            for (int q = 0; q < 16 / PER; ++q) v[b][q] = J < nbc ? src[q] : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int b = 0; b < XB; ++b) {
+            if (base + b * TPB >= nbc) break;  // (uniform)
+            const int32_t J = base + b * TPB + t0;
+            uint32_t msk = 0;
+#pragma unroll
+            for (int q = 0; q < 16 / PER; ++q) {
+                const uint32_t w[4] = {v[b][q].x, v[b][q].y, v[b][q].z, v[b][q].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if constexpr (MODE == M_F16) {
+                        msk |= ((w[e] & 0x7FFFu) ? 1u : 0u) << (q * 8 + e * 2);
+                        msk |= ((w[e] & 0x7FFF0000u) ? 1u : 0u) << (q * 8 + e * 2 + 1);
+                    } else {
+                        msk |= ((w[e] & 0x7FFFFFFFu) ? 1u : 0u) << (q * 4 + e);
+                    }
+                }
+            }
+            if (J < nbc) lmask[J] = (uint16_t)msk;
+            // a wave's 64 consecutive vector blocks fill two bitmap words
+            const uint64_t bm = ballot(msk != 0u);
+            const int32_t w0 = (base + b * TPB + (t0 & ~(WAVE - 1))) >> 5;
+            if (lane == 0 && w0 < nwords) lds_bits[w0] = (uint32_t)bm;
+            if (lane == 32 && w0 + 1 < nwords) lds_bits[w0 + 1] = (uint32_t)(bm >> 32);
+            cnt += msk ? 1u : 0u;
+        }
+    }
+    // (the staging area of pull_rows serves the count's reduction first)
+    if (blockIdx.x == 0) {
+        const uint32_t c = wave_sum(cnt);
+        if (lane == 0) rows_lds[t0 >> 6] = c;
+    }
+    __syncthreads();
+    if (blockIdx.x == 0 && t0 == 0) {
+        uint32_t c = 0;
+#pragma unroll
+        for (int w = 0; w < TPB / WAVE; ++w) c += rows_lds[w];
+        a.counters[C_NZBLK] = (int32_t)c;
+        a.counters[C_PATH] = PATH_PULL;
+    }
+    __syncthreads();
+    pull_rows<MODE, true, 1, true>(a, rows_lds, &first);
+}
+
 // ---------------------------------------------------------------------------
 // finalize: ascending sparse y from the row-block structure masks
 // ---------------------------------------------------------------------------
@@ -3409,15 +3490,68 @@ hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_i
 }
 
 hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, void *y, float *y32,
-                                 hipStream_t s)
+                                 hipStream_t s, bool restore_x)
 {
     int32_t nyw = (A.nbr + 1) / 2;
-    int64_t items = A.m > C.nxwords ? A.m : C.nxwords;
+    const int32_t nxw = restore_x ? C.nxwords : 0, nx = restore_x ? A.n : 0;
+    int64_t items = A.m > nxw ? A.m : nxw;
     dim3 g(grid_for(items, TPB, 4096)), b(TPB);
     if (mode == M_F16)
-        hipLaunchKernelGGL(k_finalize_dense<M_F16>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, C.nxwords, C.xd, A.n, C.counters);
+        hipLaunchKernelGGL(k_finalize_dense<M_F16>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, nxw, C.xd, nx, C.counters);
     else
-        hipLaunchKernelGGL(k_finalize_dense<M_F32>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, C.nxwords, C.xd, A.n, C.counters);
+        hipLaunchKernelGGL(k_finalize_dense<M_F32>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, nxw, C.xd, nx, C.counters);
+    return hipGetLastError();
+}
+
+bool rows_dx_fits(const DevMatrix &A, const void *x_dense)
+{
+    // (the caller has excluded pattern matrices)
+    return A.nblk > 0 && A.nheavy == A.nblk && scan_takes_dense(A, x_dense) && A.nbc <= ROWS_DX_MAX_NBC;
+}
+
+// Chunks per round for k_rows_dx (as rows_cpw), its residency cached per
+// dynamic LDS size.
+template <int MODE>
+static int32_t rows_dx_cpw(int64_t nchunk, size_t dyn)
+{
+    static size_t cached_lds[8];
+    static int cached_res[8];
+    static int ncached = 0;
+    int res = -1;
+    for (int i = 0; i < ncached; ++i)
+        if (cached_lds[i] == dyn) res = cached_res[i];
+    if (res < 0) {
+        int dev = 0, cus = 0, per_cu = 0;
+        res = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_rows_dx<MODE>, TPB, dyn) == hipSuccess &&
+            cus > 0 && per_cu > 0)
+            res = cus * per_cu;
+        if (ncached < 8) {
+            cached_lds[ncached] = dyn;
+            cached_res[ncached] = res;
+            ++ncached;
+        }
+    }
+    if (res <= 0) return TPB / 16;
+    const int64_t c = (nchunk + res - 1) / res;
+    return (int32_t)std::max<int64_t>(1, std::min<int64_t>(c, TPB / 16));
+}
+
+hipError_t launch_rows_dx(const DevMatrix &A, const DevCtx &C, int mode, const void *x_dense, hipStream_t s)
+{
+    MainArgs a;
+    fill_main_args(A, C, mode, x_dense, nullptr, 0, nullptr, a);
+    const int32_t nwords = (A.nbc + 31) >> 5;
+    const size_t dyn = ((size_t)nwords + ((size_t)A.nbc + 1) / 2) * 4;
+    if (mode == M_F16) {
+        a.cpw = rows_dx_cpw<M_F16>(A.nchunk, dyn);
+        hipLaunchKernelGGL(k_rows_dx<M_F16>, dim3(grid_for(A.nchunk, a.cpw, INT_MAX)), dim3(TPB), dyn, s, a);
+    } else {
+        a.cpw = rows_dx_cpw<M_F32>(A.nchunk, dyn);
+        hipLaunchKernelGGL(k_rows_dx<M_F32>, dim3(grid_for(A.nchunk, a.cpw, INT_MAX)), dim3(TPB), dyn, s, a);
+    }
     return hipGetLastError();
 }
 

@@ -171,8 +171,16 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
 hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_idx,
                            void *y_val, int32_t *y_nnz, const int32_t *x_idx, int32_t k,
                            hipStream_t s);
+// restore_x: also restore the context's densified x and masks (after a scan
+// of the activation; not after launch_rows_dx, which leaves them untouched)
 hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, void *y,
-                                 float *y32, hipStream_t s);
+                                 float *y32, hipStream_t s, bool restore_x = true);
+// Dense activation, pull on a matrix without COO blocks: the non-COO pass
+// reading the activation itself, no scan before it (k_rows_dx), when
+// rows_dx_fits (for a valued matrix: the conditions of scan_takes_dense, no
+// COO block, at most ROWS_DX_MAX_NBC vector blocks).
+bool rows_dx_fits(const DevMatrix &A, const void *x_dense);
+hipError_t launch_rows_dx(const DevMatrix &A, const DevCtx &C, int mode, const void *x_dense, hipStream_t s);
 // Batched dense activations (NB in {2, 4, 8} vectors per pass, nb <= NB of
 // them real): the padded copies into xdb (NB * 16 nbc entries) and their
 // union mask; the pull over a matrix without COO blocks into yaccb (NB * 16
