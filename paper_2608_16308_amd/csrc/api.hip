@@ -196,7 +196,7 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
     d.nseg = h->nseg;
     d.dtype = h->dtype;
     // primary order -> pull-segment slots (see DevMatrix)
-    std::vector<int32_t> sl_col, hv_col, hv_cstart, hv_crow;
+    std::vector<int32_t> sl_col, hv_col, hv_cstart, hv_crow, hv_rowchunks;
     std::vector<uint64_t> sl_desc, hv_desc, csc_desc;
     std::vector<uint32_t> seg_rs;
     std::vector<int32_t> task_order;
@@ -245,6 +245,8 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
         std::stable_sort(task_order.begin(), task_order.end(),
                          [&](int32_t x, int32_t y) { return tcost[(size_t)x] > tcost[(size_t)y]; });
         hv_cstart.push_back((int32_t)hv_col.size());
+        hv_rowchunks.assign((size_t)std::max(h->nbr, 1), 0);
+        for (const int32_t R : hv_crow) ++hv_rowchunks[(size_t)R];
         csc_desc.resize((size_t)h->nblk);
         for (int64_t q = 0; q < h->nblk; ++q) csc_desc[q] = h->desc[h->csc2csr[q]];
     } catch (const std::bad_alloc &) {
@@ -266,6 +268,7 @@ extern "C" dbs_status dbs_matrix_upload(const dbs_host_matrix *h, dbs_matrix **o
         (s2 = dev_upload(A->allocs, hv_desc, &d.hv_desc)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, hv_cstart, &d.hv_cstart)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, hv_crow, &d.hv_crow)) != DBS_OK ||
+        (s2 = dev_upload(A->allocs, hv_rowchunks, &d.hv_rowchunks)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->payload, &d.pay, 16)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, task_order, &d.task_order)) != DBS_OK ||
         (s2 = dev_upload(A->allocs, h->row_occ, &d.row_occ)) != DBS_OK) {
@@ -382,6 +385,7 @@ extern "C" dbs_status dbs_ctx_create(const dbs_matrix *sizing, void *stream, dbs
         (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &visited)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.nxwords, &nextm)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)C_COUNT, &c.counters)) != DBS_OK ||
+        (st = dev_zeros(ctx->allocs, (size_t)nbr, &c.rdone)) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.n_st_scan, &c.st_scan[0])) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.n_st_scan, &c.st_scan[1])) != DBS_OK ||
         (st = dev_zeros(ctx->allocs, (size_t)c.n_st_fin, &c.st_fin[0])) != DBS_OK ||
@@ -620,9 +624,8 @@ extern "C" dbs_status dbs_spmspv_dense(dbs_ctx *ctx, const dbs_matrix *A, const 
     if (p == DBS_PATH_AUTO && !(th3 > 0.f) && A->d.nblk > 0 && A->d.nheavy == A->d.nblk) p = DBS_PATH_PULL;
     if (p == DBS_PATH_PULL && rows_dx_fits(A->d, d_x_dense)) {
         // pull known on the host: the non-COO pass reads the activation
-        // itself, without a scan
-        LAUNCH(ctx, DBS_K_MAIN, launch_rows_dx(A->d, ctx->c, mode, d_x_dense, s));
-        LAUNCH(ctx, DBS_K_FINALIZE, launch_finalize_dense(A->d, ctx->c, mode, d_y_dense, d_y_f32, s, false));
+        // itself, without a scan, and writes y itself
+        LAUNCH(ctx, DBS_K_MAIN, launch_rows_dx(A->d, ctx->c, mode, d_x_dense, d_y_dense, d_y_f32, s));
     } else {
         if (scan_takes_dense(A->d, d_x_dense)) {
             LAUNCH(ctx, DBS_K_SCAN,

@@ -314,6 +314,13 @@ __global__ __launch_bounds__(CTPB) void k_conv_write(const void *w, int64_t ld, 
 
 // A thread per block row: its segment words (the block row) and non-COO
 // chunks (at most HV_CHUNK consecutive blocks of the row each).
+// Chunks of each block row (the count array starts at zero).
+__global__ __launch_bounds__(CTPB) void k_conv_rowchunks(int64_t nchunk, const int32_t *hv_crow, int32_t *rowchunks)
+{
+    const int64_t c = (int64_t)blockIdx.x * CTPB + threadIdx.x;
+    if (c < nchunk) atomicAdd(&rowchunks[hv_crow[c]], 1);
+}
+
 __global__ __launch_bounds__(CTPB) void k_conv_segs(int32_t nbr, const int64_t *pre, uint32_t *seg_rs,
                                                     int32_t *hv_cstart, int32_t *hv_crow)
 {
@@ -444,7 +451,7 @@ dbs_status convert(int32_t m, int32_t n, const void *d_w, int64_t ld, const dbs_
     CONV_TRY(hipMemcpyAsync(pre_d, pre.data(), pre.size() * 8, hipMemcpyHostToDevice, s), "hipMemcpy (prefixes)");
 
     int32_t *sl_col = nullptr, *cb_ptr = nullptr, *csc_row = nullptr, *hv_col = nullptr, *hv_cstart = nullptr,
-            *hv_crow = nullptr;
+            *hv_crow = nullptr, *hv_rowchunks = nullptr;
     uint64_t *sl_desc = nullptr, *csc_desc = nullptr, *hv_desc = nullptr, *blk_desc = nullptr;
     uint32_t *seg_rs = nullptr;
     uint8_t *pay = nullptr;
@@ -459,6 +466,7 @@ dbs_status convert(int32_t m, int32_t n, const void *d_w, int64_t ld, const dbs_
         (st = conv_alloc(A->allocs, (size_t)nheavy, &hv_desc, 0, s)) != DBS_OK ||
         (st = conv_alloc(A->allocs, (size_t)nchunk + 1, &hv_cstart, 0, s)) != DBS_OK ||
         (st = conv_alloc(A->allocs, (size_t)nchunk, &hv_crow, 0, s)) != DBS_OK ||
+        (st = conv_alloc(A->allocs, (size_t)std::max<int64_t>(nbr, 1), &hv_rowchunks, 0, s)) != DBS_OK ||
         (st = conv_alloc(A->allocs, (size_t)bytes, &pay, 0, s, 16)) != DBS_OK)
         return st;
     CONV_TRY(scratch((size_t)nblk * 8, (void **)&blk_desc), "hipMalloc (descriptors)");
@@ -472,6 +480,11 @@ dbs_status convert(int32_t m, int32_t n, const void *d_w, int64_t ld, const dbs_
         hipLaunchKernelGGL(k_conv_segs, dim3((unsigned)((nbr + CTPB - 1) / CTPB)), dim3(CTPB), 0, s, nbr, pre_d,
                            seg_rs, hv_cstart, hv_crow);
         CONV_TRY(hipGetLastError(), "k_conv_segs");
+        if (nchunk > 0) {
+            hipLaunchKernelGGL(k_conv_rowchunks, dim3((unsigned)((nchunk + CTPB - 1) / CTPB)), dim3(CTPB), 0, s,
+                               nchunk, hv_crow, hv_rowchunks);
+            CONV_TRY(hipGetLastError(), "k_conv_rowchunks");
+        }
     }
     const int32_t nheavy32 = (int32_t)nheavy;
     CONV_TRY(hipMemcpyAsync(hv_cstart + nchunk, &nheavy32, 4, hipMemcpyHostToDevice, s), "hipMemcpy (chunks)");
@@ -511,6 +524,7 @@ dbs_status convert(int32_t m, int32_t n, const void *d_w, int64_t ld, const dbs_
     d.hv_desc = hv_desc;
     d.hv_cstart = hv_cstart;
     d.hv_crow = hv_crow;
+    d.hv_rowchunks = hv_rowchunks;
     d.nheavy = nheavy;
     d.nchunk = nchunk;
     d.pay = pay;

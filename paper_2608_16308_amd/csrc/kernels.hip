@@ -868,6 +868,14 @@ struct MainArgs {
     int32_t creg;           // compacted pull: regions the list's counts have room for
     const int32_t *torder;  // segment-loop tasks by decreasing cost (NULL: segment order)
     int32_t ntask;          // tasks in torder
+    // dense output written by the non-COO pass itself (k_rows_dx): the
+    // chunks of each block row, the per-call count of its committed chunks,
+    // the outputs (y in the matrix's value type, optional fp32 copy), m
+    const int32_t *rowchunks;
+    int32_t *rdone;
+    void *ydense;
+    float *y32;
+    int32_t m;
 };
 
 // Independent work units per lane and loop iteration: four segments per
@@ -1287,7 +1295,8 @@ __device__ __forceinline__ RowsPre rows_pre(const MainArgs &a, int64_t c0)
 // the NB sums go to NB accumulator sets (x and accumulators NB-strided).
 // XL: the vector-block masks come from an LDS table (16 bits per vector
 // block, after the activity bitmap: see k_rows_dx) instead of xmask.
-template <int MODE, bool LDSBITS, int NB = 1, bool XL = false>
+// DOUT: the pass also writes the dense output (see k_rows_dx).
+template <int MODE, bool LDSBITS, int NB = 1, bool XL = false, bool DOUT = false>
 __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L, const RowsPre *first = nullptr)
 {
     using Y = RowsLds<MODE, NB>;
@@ -1547,6 +1556,7 @@ __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L, const 
                 for (int b = 0; b < NB; ++b) sum[b] = 0.0;
                 int32_t pm = INT_MAX;
                 uint32_t run = 0;
+                int32_t nrun = 0;  // chunks in the run
                 // the run's chunks CG at a time, their LDS reads issued together
                 constexpr int CG = NB == 1 ? 4 : 1;
                 bool in = true;
@@ -1572,6 +1582,7 @@ __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L, const 
                     for (int j = 0; j < CG; ++j) {
                         in = in && crs[j] == Rc;
                         if (!in) break;
+                        ++nrun;
                         run |= hms[j];
                         if ((hms[j] >> rr) & 1u) {
                             if constexpr (valued<MODE>()) {
@@ -1591,7 +1602,32 @@ __device__ __forceinline__ void pull_rows(const MainArgs &a, uint32_t *L, const 
                     }
                     if constexpr (MODE == M_BFS) atomicMin(&a.parent[row], pm);
                 }
-                if (rr == 0 && run) or_mask16(a.ybits, Rc, run);
+                if constexpr (DOUT) {
+                    // Count the run's chunks once its adds have completed:
+                    // they are device-scope atomics, complete when the wave's
+                    // memory counter drains, so no cache write-back (a
+                    // release fence) is needed.  The workgroup that
+                    // completes the block row converts its rows, taking each
+                    // sum and clearing it in one atomic exchange (performed
+                    // where the adds were), and clears the count.
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+                    __builtin_amdgcn_s_waitcnt(0);
+                    uint32_t last = 0;
+                    if (rr == 0) last = atomicAdd(&a.rdone[Rc], nrun) + nrun == a.rowchunks[Rc] ? 1u : 0u;
+                    last = (uint32_t)__shfl((int)last, lane & ~15, WAVE);
+                    if (last) {
+                        const int64_t row = (int64_t)Rc * BS + rr;
+                        if (row < a.m) {
+                            const double v = atomicExch(&a.yacc[row], 0.0);
+                            if constexpr (MODE == M_F32) ((float *)a.ydense)[row] = (float)v;
+                            else ((uint16_t *)a.ydense)[row] = f64_to_f16_rne(v);
+                            if (a.y32) a.y32[row] = (float)v;
+                        }
+                        if (rr == 0) atomicExch(&a.rdone[Rc], 0);
+                    }
+                } else {
+                    if (rr == 0 && run) or_mask16(a.ybits, Rc, run);
+                }
             }
         }
         __syncthreads();  // the next round overwrites the staging
@@ -2492,13 +2528,17 @@ __global__ __launch_bounds__(TPB) void k_rows(MainArgs a)
 
 // Dense activation on a matrix without COO blocks (decoding) with the path
 // known to be pull: the non-COO pass reads the activation itself, with no
-// scan before it.  Each workgroup first forms the 16-bit mask of every vector
-// block (an entry is present iff it is nonzero, -0 included as zero, as in
-// the scan) from the activation into an LDS table after the activity bitmap,
-// and both in LDS; the blocks' x words are then the activation's own (the
-// masks select the products), and nothing of the context's x scratch is
-// written, so the y conversion after it restores none.  Workgroup 0 also
-// records N_nzblk and the path for the call's statistics.
+// scan before it.  Each workgroup first forms, from the activation, the
+// 16-bit mask of every vector block (an entry is present iff it is nonzero,
+// -0 counting as zero, as in the scan) and the activity bitmap, both in LDS
+// (the mask table after the bitmap); the blocks' x words are then the
+// activation's own (the masks select the products), and nothing of the
+// context's x scratch is written.  The pass also writes the dense output:
+// the workgroup that commits the last chunk of a block row (a per-call
+// count per block row) converts its rows and clears their sums and the
+// count, and rows of block rows without chunks are written as zeros, so
+// that no kernel follows it.  Workgroup 0 records N_nzblk and the path for
+// the call's statistics.
 // The table takes (nbc + 1) / 2 words of dynamic LDS: ROWS_DX_MAX_NBC vector
 // blocks at most.
 constexpr int32_t ROWS_DX_MAX_NBC = 4096;
@@ -2506,6 +2546,7 @@ template <int MODE>
 __global__ __launch_bounds__(TPB) void k_rows_dx(MainArgs a)
 {
     __shared__ __align__(16) uint32_t rows_lds[RowsLds<MODE, 1>::WORDS];
+    // the first round's chunk bounds go out before the mask pass
     const RowsPre first = rows_pre(a, (int64_t)blockIdx.x * a.cpw);
     const int32_t nbc = a.nbc, nwords = (nbc + 31) >> 5;
     uint16_t *lmask = (uint16_t *)(lds_bits + nwords);
@@ -2562,9 +2603,21 @@ __global__ __launch_bounds__(TPB) void k_rows_dx(MainArgs a)
         for (int w = 0; w < TPB / WAVE; ++w) c += rows_lds[w];
         a.counters[C_NZBLK] = (int32_t)c;
         a.counters[C_PATH] = PATH_PULL;
+        a.counters[C_YNNZ] = a.m;
+        a.counters[C_ERR_LAST] = 0;
+    }
+    // block rows without chunks: zero rows
+    for (int64_t R = (int64_t)blockIdx.x * (TPB / 16) + (t0 >> 4); R < (a.m + 15) / 16;
+         R += (int64_t)gridDim.x * (TPB / 16)) {
+        const int64_t row = R * BS + (t0 & 15);
+        if (a.rowchunks[R] == 0 && row < a.m) {
+            if constexpr (MODE == M_F32) ((float *)a.ydense)[row] = 0.f;
+            else ((uint16_t *)a.ydense)[row] = 0;
+            if (a.y32) a.y32[row] = 0.f;
+        }
     }
     __syncthreads();
-    pull_rows<MODE, true, 1, true>(a, rows_lds, &first);
+    pull_rows<MODE, true, 1, true, true>(a, rows_lds, &first);
 }
 
 // ---------------------------------------------------------------------------
@@ -3366,6 +3419,11 @@ static void fill_main_args(const DevMatrix &A, const DevCtx &C, int mode, const 
     a.creg = compact_list_regions();
     a.torder = A.task_order;
     a.ntask = A.ntask;
+    a.rowchunks = nullptr;
+    a.rdone = nullptr;
+    a.ydense = nullptr;
+    a.y32 = nullptr;
+    a.m = A.m;
 }
 
 int64_t compact_list_entries(int64_t nseg) { return (nseg + 4 * MAX_MAIN_GRID) * 16; }
@@ -3490,16 +3548,15 @@ hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_i
 }
 
 hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, void *y, float *y32,
-                                 hipStream_t s, bool restore_x)
+                                 hipStream_t s)
 {
     int32_t nyw = (A.nbr + 1) / 2;
-    const int32_t nxw = restore_x ? C.nxwords : 0, nx = restore_x ? A.n : 0;
-    int64_t items = A.m > nxw ? A.m : nxw;
+    int64_t items = A.m > C.nxwords ? A.m : C.nxwords;
     dim3 g(grid_for(items, TPB, 4096)), b(TPB);
     if (mode == M_F16)
-        hipLaunchKernelGGL(k_finalize_dense<M_F16>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, nxw, C.xd, nx, C.counters);
+        hipLaunchKernelGGL(k_finalize_dense<M_F16>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, C.nxwords, C.xd, A.n, C.counters);
     else
-        hipLaunchKernelGGL(k_finalize_dense<M_F32>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, nxw, C.xd, nx, C.counters);
+        hipLaunchKernelGGL(k_finalize_dense<M_F32>, g, b, 0, s, C.yacc, A.m, y, y32, C.ybits, nyw, C.xmask, C.nxwords, C.xd, A.n, C.counters);
     return hipGetLastError();
 }
 
@@ -3539,10 +3596,16 @@ static int32_t rows_dx_cpw(int64_t nchunk, size_t dyn)
     return (int32_t)std::max<int64_t>(1, std::min<int64_t>(c, TPB / 16));
 }
 
-hipError_t launch_rows_dx(const DevMatrix &A, const DevCtx &C, int mode, const void *x_dense, hipStream_t s)
+hipError_t launch_rows_dx(const DevMatrix &A, const DevCtx &C, int mode, const void *x_dense, void *y,
+                          float *y32, hipStream_t s)
 {
     MainArgs a;
     fill_main_args(A, C, mode, x_dense, nullptr, 0, nullptr, a);
+    a.rowchunks = A.hv_rowchunks;
+    a.rdone = C.rdone;
+    a.ydense = y;
+    a.y32 = y32;
+    a.m = A.m;
     const int32_t nwords = (A.nbc + 31) >> 5;
     const size_t dyn = ((size_t)nwords + ((size_t)A.nbc + 1) / 2) * 4;
     if (mode == M_F16) {

@@ -33,6 +33,7 @@ struct DevMatrix {
     const uint64_t *hv_desc = nullptr;   // nheavy: descriptor
     const int32_t *hv_cstart = nullptr;  // nchunk + 1
     const int32_t *hv_crow = nullptr;    // nchunk
+    const int32_t *hv_rowchunks = nullptr;  // nbr: chunks of each block row
     int64_t nheavy = 0, nchunk = 0;
     const uint8_t *pay = nullptr;
     // Segment-loop tasks (PULL_TASK_SEGS consecutive segments each) in
@@ -105,6 +106,7 @@ struct DevCtx {
     uint32_t *visited = nullptr;  // BFS visited bitmap (row-block words)
     uint32_t *nextm = nullptr;    // BFS next-frontier bitmap
     int32_t *counters = nullptr;  // C_COUNT int32
+    int32_t *rdone = nullptr;     // nbr: chunks of a block row committed so far (dense-output pass)
     // Look-back status words of the two scans, in two copies each: a call
     // uses copy `parity` and clears the other copy for the next call, so no
     // other kernel has to clean up after a scan.
@@ -171,16 +173,16 @@ hipError_t launch_main(const DevMatrix &A, const DevCtx &C, int mode, const void
 hipError_t launch_finalize(const DevMatrix &A, DevCtx &C, int mode, int32_t *y_idx,
                            void *y_val, int32_t *y_nnz, const int32_t *x_idx, int32_t k,
                            hipStream_t s);
-// restore_x: also restore the context's densified x and masks (after a scan
-// of the activation; not after launch_rows_dx, which leaves them untouched)
 hipError_t launch_finalize_dense(const DevMatrix &A, const DevCtx &C, int mode, void *y,
-                                 float *y32, hipStream_t s, bool restore_x = true);
+                                 float *y32, hipStream_t s);
 // Dense activation, pull on a matrix without COO blocks: the non-COO pass
-// reading the activation itself, no scan before it (k_rows_dx), when
+// reading the activation itself, with no scan before it and writing the
+// dense output y (and y32 when not NULL) itself (k_rows_dx), when
 // rows_dx_fits (for a valued matrix: the conditions of scan_takes_dense, no
 // COO block, at most ROWS_DX_MAX_NBC vector blocks).
 bool rows_dx_fits(const DevMatrix &A, const void *x_dense);
-hipError_t launch_rows_dx(const DevMatrix &A, const DevCtx &C, int mode, const void *x_dense, hipStream_t s);
+hipError_t launch_rows_dx(const DevMatrix &A, const DevCtx &C, int mode, const void *x_dense, void *y,
+                          float *y32, hipStream_t s);
 // Batched dense activations (NB in {2, 4, 8} vectors per pass, nb <= NB of
 // them real): the padded copies into xdb (NB * 16 nbc entries) and their
 // union mask; the pull over a matrix without COO blocks into yaccb (NB * 16

@@ -40,6 +40,37 @@ def test_decode_small(torch, shape):
             check_decode(ctx, A, om, a16, p, label)
 
 
+def test_decode_scan_free_pass_empty_block_rows(torch):
+    """The scan-free dense pass (pull known on the host, no COO blocks)
+    writes y itself: block rows without blocks must come out as zeros, the
+    ragged last block row only up to m, and the per-call block-row counts and
+    sums must be cleared for the next call (three calls in a row, then a
+    sparse call on the same context)."""
+    out_f, in_f = 200, 512
+    w = wl.decode_layer(out_f, in_f)
+    d = np.zeros((out_f, in_f), dtype=np.float16)
+    rows = np.repeat(np.arange(out_f), np.diff(w.row_ptr))
+    d[rows, w.col_idx] = w.vals
+    d[32:64, :] = 0        # two block rows without blocks
+    d[100:105, :] = 0      # empty rows inside a block row
+    rr, cc = np.nonzero(d)
+    rp = np.zeros(out_f + 1, dtype=np.int64)
+    np.add.at(rp, rr + 1, 1)
+    a = wl.CSR(out_f, in_f, np.cumsum(rp), cc.astype(np.int32), np.ascontiguousarray(d[rr, cc]))
+    A, om = gpu_matrix(a), oracle_matrix(a)
+    assert A.info()["blocks_by_type"]["coo"] == 0
+    ctx = dbs.Context(A)
+    for key in range(3):
+        a16 = wl.decode_activation(in_f, key=10 + key)
+        for p in ("auto", "pull"):
+            label = f"scan-free decode act={key} path={p}"
+            log(label)
+            check_decode(ctx, A, om, a16, p, label)
+    xi, _ = wl.sparse_x(in_f, 0.05, "uniform", key=(41, 0))
+    xv = np.full(xi.size, np.float16(0.25))
+    check_spmspv(ctx, A, om, a, xi, xv, path="pull", label="sparse call after the scan-free pass")
+
+
 def test_decode_selector(torch):
     """A decode layer (no COO blocks) with one active vector block: the
     default selector takes pull without a push launch, th3 > 0 the paper's
