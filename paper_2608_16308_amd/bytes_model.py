@@ -136,7 +136,10 @@ class BytesModel:
         the blocker reads all n values, writes the padded dense x and the
         n-bit mask; the finalize reads every fp64 accumulator, writes y (V
         bytes per row) and resets the accumulators, the y and x masks and
-        the dense x.  x_idx are the nonzero positions of the activation."""
+        the dense x.  x_idx are the nonzero positions of the activation.
+        (When pull is known on the host, the scan-free pass writes no dense
+        x or masks and runs no scan: it moves about 2 V n + 2 nbc bytes
+        fewer than charged here, under 0.1% of a decode layer's bytes.)"""
         r = self.call(x_idx, path, th3)
         V, m, n = self.V, self.m, self.n
         r["bytes_blocker"] = 2 * V * n + n // 8
